@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Throughput of one aggregation step of the unbiased max-norm quantisers
+(arXiv 2109.12497, Algorithms 1-2) on one MI355X.
+
+A step is the whole hot path over M workers' gradients resident in HBM:
+shared max-norm scale (+ shared scale index) -> quantise every worker ->
+integer sum of the codes -> reconstruct the averaged gradient.  The metric is
+gradient elements (M * d worker-coordinates) per second, and the fraction of
+the 8 TB/s HBM peak the step's algorithmic bytes reach.
+
+Prints one JSON line.  Extra modes:
+  --workload NAME       another workload of synth.WORKLOADS (default resnet18)
+  --no-cpu-baseline     skip the oracle leg (for profiling runs)
+  --copy-probe BYTES    time and run only a plain device copy (counter calibration)
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "G gradient elements/s quantize+sum+dequantize; % of HBM peak GB/s"
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCES = ["paper_2109_12497_amd/csrc/uq_kernels.hip", "paper_2109_12497_amd/csrc/uq_device.hpp"]
+
+
+def algorithmic_bytes(d: int, M: int, K: int, streamed: bool) -> dict:
+    """Bytes each stage must move at minimum (reads + writes), per step."""
+    multi = K > 1
+    b = {
+        "shared_scale": 4 * M * d + (4 * M * d + d if multi else 0),
+        "quantize": M * d * (4 + 1 + (1 if multi else 0)),
+        "sum": (M * d + 4 * d) if not streamed else (d + 4 * d) + (M - 1) * (d + 8 * d),
+        "dequantize": d * (4 + 4 + (1 if multi else 0)),
+    }
+    b["total"] = sum(b.values())
+    return b
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    there is none or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"^traffic_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    s = re.search(r"^source_digest:\s*([0-9a-f]+)", text, re.M)
+    if not m or not s or s.group(1) != source_digest():
+        return None
+    return float(m.group(1))
+
+
+def copy_probe(nbytes: int) -> None:
+    import torch
+
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    reps = 10
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    print(json.dumps({"copy_probe_bytes": nbytes, "read_plus_write_GBps": 2 * nbytes / dt / 1e9}))
+
+
+def cpu_baseline(g, cfg, budget_s: float):
+    """The oracle on the host cores over a bounded sample of the workload."""
+    import numpy as np
+
+    from oracle import oracle
+
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    # ~41 ns per worker-coordinate for the oracle's whole step on one core
+    dn = min(d, max(4096, int(budget_s / (45e-9 * M))))
+    host = g[:, :dn].cpu().numpy()
+    t0 = time.perf_counter()
+    ref = oracle.pipeline(host, scales, seed, d=dn)
+    dt = time.perf_counter() - t0
+    sample = "full workload" if dn == d else f"all {M} workers, coordinates [0, {dn}) of {d}"
+    return {"value": round(M * dn / dt / 1e9, 6), "unit": "G elements/s", "cores": 1, "kind": "oracle",
+            "sample": sample, "seconds": round(dt, 2)}, ref, dn
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet18")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work to aim for")
+    ap.add_argument("--copy-probe", type=int, default=0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the simulated workers' codes are summed on-device; "
+              "multi-GPU runs are not part of this build (use --gpus 1).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return 0
+
+    import synth
+    from paper_2109_12497_amd.step import Step  # fails loudly if libuq.so is not built
+
+    g, cfg = synth.make_gradients(args.workload, device="cuda")
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    streamed = bool(cfg.get("streamed", False))
+    K = len(scales)
+    step = Step(d, M, scales, device="cuda", streamed=streamed)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        step.run(g, seed)
+    torch.cuda.synchronize()
+
+    stages = ["shared_scale", "quantize", "sum", "dequantize"]
+    ev = {s: [] for s in stages}
+
+    def mark():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        a = mark()
+        step.shared_scale(g)
+        b = mark()
+        ev["shared_scale"].append((a, b))
+        if streamed:
+            for m in range(M):
+                a = mark()
+                step.quantize(g[m:m + 1], seed, rows=1, worker0=m)
+                b = mark()
+                step.sum_codes(rows=1, accumulate=1 if m > 0 else 0)
+                c = mark()
+                ev["quantize"].append((a, b))
+                ev["sum"].append((b, c))
+        else:
+            a = mark()
+            step.quantize(g, seed)
+            b = mark()
+            step.sum_codes()
+            c = mark()
+            ev["quantize"].append((a, b))
+            ev["sum"].append((b, c))
+        a = mark()
+        step.dequantize()
+        b = mark()
+        ev["dequantize"].append((a, b))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    ms_per_step = elapsed / args.steps * 1e3
+    stage_ms = {s: sum(x.elapsed_time(y) for x, y in ev[s]) / args.steps for s in stages}
+    launches = {"quantize": M if streamed else 1}
+    nbytes = algorithmic_bytes(d, M, K, streamed)
+    value = M * d * args.steps / elapsed / 1e9
+
+    # dominant kernel: the quantiser (k_quantise); bytes per launch and average launch time
+    q_launch_ms = stage_ms["quantize"] / launches["quantize"]
+    q_bytes_launch = nbytes["quantize"] / launches["quantize"]
+    achieved = q_bytes_launch / (q_launch_ms * 1e-3) / 1e9
+    kernel_name = "k_quantise_multi" if K > 1 else "k_quantise_single"
+    traffic = measured_traffic(kernel_name, args.workload)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "G elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed,
+                   "quantizer": "multi" if K > 1 else "single", "streamed": streamed,
+                   "parallelism": "one GPU, M workers simulated"},
+        "pct_hbm_peak": round(100 * nbytes["total"] / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes_per_launch": q_bytes_launch},
+        "cpu_baseline": None,
+    }
+
+    if not args.no_cpu_baseline:
+        base, ref, dn = cpu_baseline(g, cfg, args.cpu_budget)
+        result["cpu_baseline"] = base
+        # the oracle ran on the same inputs: compare what it covers (free parity check)
+        W = np.float32(step.w[0].item())
+        if dn == d and not streamed:
+            same_w = W == ref["W_oracle"]
+            if not same_w:
+                from oracle import oracle
+
+                ref = oracle.pipeline(g[:, :d].cpu().numpy(), scales, seed, d=d, W=W)
+            ok = (np.array_equal(step.codes[:, :d].cpu().numpy(), ref["codes"]) and
+                  np.array_equal(step.sum[:d].cpu().numpy(), ref["sum"]) and
+                  np.array_equal(step.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32)))
+            result["parity_vs_oracle"] = "bit-exact" if ok else "MISMATCH"
+    print(json.dumps(result))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

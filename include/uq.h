@@ -1,0 +1,159 @@
+/*
+ * uq.h -- C ABI of libuq, the MI355X (gfx950) implementation of the unbiased
+ * single-scale and multi-scale max-norm quantisers of "Unbiased Single-scale
+ * and Multi-scale Quantizers for Distributed Optimization" (arXiv 2109.12497).
+ *
+ * One aggregation step of Algorithm 1 (one scale) or Algorithm 2 (several
+ * scales) for M workers' flat fp32 gradients g^m in R^d is the sequence
+ *
+ *   uq_shared_scale     W = max_m ||g^m||_2 and, for several scales, the
+ *                       shared per-coordinate scale index;
+ *   uq_quantize_single  or uq_quantize_multi: the integer codes of each worker;
+ *   uq_sum_codes        the all-reduce of the codes (an exact integer sum);
+ *   uq_dequantize       the averaged gradient reconstructed from the sum.
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers, except `scales`, which is a HOST
+ *     array of K floats.  The caller owns every buffer; the library never
+ *     allocates device memory and keeps no state between calls.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *     asynchronously on it; no entry point synchronises.  Argument checks are
+ *     done on the host before anything is enqueued; on an error nothing is
+ *     enqueued and no output is touched.
+ *   - Gradients are row-major [rows][ldg] fp32 with ldg >= d, ldg % 4 == 0;
+ *     only the first d entries of a row are read.  Codes are row-major
+ *     [rows][ldc] int8 with ldc >= d, ldc % 16 == 0; only the first d bytes
+ *     of a row are written.  Every array pointer must be 16-byte aligned
+ *     (`w` 4-byte aligned).
+ *   - Scale sets: 1 <= K <= 16 strictly increasing integral floats
+ *     s_0 < ... < s_{K-1} with 1 <= s_0 <= 127 (|code| <= s_0 fits int8).
+ *     The single-scale call takes s in [1, 127] and is the case K = 1.
+ *   - Data-dependent conditions are never errors.  A scale W that is not a
+ *     positive finite number, or for which s_0 / W overflows, selects the zero
+ *     path: every code is 0, every scale index K-1, every output 0.  Zero,
+ *     NaN and infinite gradient coordinates get code 0 (and a row holding a
+ *     NaN or infinity has a non-finite norm, hence the zero path).
+ *   - d == 0 is a valid no-op (uq_shared_scale still writes W = 0).
+ *
+ * Arithmetic contract (bit-exact, independent of launch geometry)
+ *   inv_k = RN32(s_k / W), deq_k = RN32(W / (M * s_k)).
+ *   Scale index (Eq. (11), shared by the minimum over workers): for each
+ *   worker the largest k with RN32(|g| * inv_k) <= s_0 (none: 0; zero or
+ *   non-finite |g|: K-1); the shared index is the minimum over the workers.
+ *   Code (Eq. (8) / Eq. (12)): x = min(RN32(|g| * inv_k), s_0), l = floor(x),
+ *   t = floor((x - l) * 2^32); code = sign(g) * (l + [r < t]), where the
+ *   32-bit uniform word r of worker m at coordinate i has as its high half
+ *   the 16-bit half (i mod 8) of Philox4x32-10 block
+ *   (key = seed, counter = (i / 8, m, 0)) and as its low half the same half
+ *   of block (i / 8, m, 1); half h of a block is bits 16*(h / 4) .. +15 of
+ *   word h mod 4.
+ *   Reconstruction (Eq. (9) / Eq. (13) with 1/M): out_i = RN32(sum_i * deq_k).
+ *   The norm is an fp64 sum of exact fp32 squares in a fixed order that
+ *   depends only on d, so W is deterministic; it can differ from a
+ *   sequential fp64 sum by at most one binary32 ulp.
+ */
+#ifndef UQ_H
+#define UQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum uq_status {
+    UQ_OK = 0,
+    UQ_EINVAL = -1,     /* null pointer, negative size, rows/M < 1, ld < d, size overflow */
+    UQ_ERANGE = -2,     /* scale set, s, K, M * s_k or worker ids out of range        */
+    UQ_EALIGN = -3,     /* misaligned pointer or leading dimension                    */
+    UQ_EWORKSPACE = -4, /* workspace smaller than uq_workspace_bytes(d, M)            */
+    UQ_EHIP = -5        /* the HIP runtime refused a launch (see uq_last_error)       */
+};
+
+#define UQ_MAX_SCALES 16
+
+/*
+ * Shared scale of Sec. 3.1/3.2: W = max_m ||g^m||_2 (the "MaxAllReduce Norm"
+ * of Algorithm 1 and Algorithm 2), and for K > 1 also the shared scale index
+ * of Sec. 3.2 (the per-coordinate rule Eq. (11) followed by scale sharing,
+ * s*_i = min_m s*^m_i).
+ *   g        [M][ldg] fp32, the M workers' gradients (read)
+ *   scales   host array of K floats (may be NULL when K == 1)
+ *   w        one fp32 (written): W
+ *   idx      [d] uint8 (written when K > 1, may be NULL when K == 1): the
+ *            shared scale index k*_i in 0..K-1
+ *   ws       device workspace of at least uq_workspace_bytes(d, M) bytes,
+ *            16-byte aligned; its contents are scratch
+ */
+int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg,
+                    const float* scales, int32_t K, float* w, uint8_t* idx,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes uq_shared_scale needs for (d, M); 0 never returned. */
+size_t uq_workspace_bytes(int64_t d, int32_t M);
+
+/*
+ * Single-scale quantiser Q_s of Eq. (7)-(8) (Sec. 3.1): the integer codes
+ * zeta = sign(g_i) * s * xi_i of `rows` workers.
+ *   g        [rows][ldg] fp32 (read); row r is worker worker0 + r
+ *   w        device pointer to W (one fp32, read)
+ *   s        number of levels, 1..127
+ *   seed     Philox key
+ *   codes    [rows][ldc] int8 (written)
+ * A call with rows = R equals R calls with rows = 1 and consecutive worker0.
+ * worker0 >= 0 and worker0 + rows <= 2^31.
+ */
+int uq_quantize_single(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                       const float* w, int32_t s, uint64_t seed, int8_t* codes, int64_t ldc,
+                       void* stream);
+
+/*
+ * Multi-scale quantiser Q_S of Eq. (10) and (12) (Sec. 3.2) with the shared
+ * scale index from uq_shared_scale: coordinate i of every worker is
+ * quantised on the grid of s*_i = scales[idx[i]] levels; |code| <= s_0.
+ *   idx      [d] uint8 (read); entries >= K are read as K-1
+ * Other arguments as for uq_quantize_single.
+ */
+int uq_quantize_multi(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                      const float* w, const float* scales, int32_t K, const uint8_t* idx,
+                      uint64_t seed, int8_t* codes, int64_t ldc, void* stream);
+
+/*
+ * The all-reduce of Algorithm 1/2 (the step the quantisers keep compatible
+ * with aggregation, Sec. 3.1): sum_i = sum over the rows of code_{r,i}, exact
+ * in int32.
+ *   codes       [rows][ldc] int8 (read)
+ *   accumulate  0: sum = the rows' total; 1: sum += the rows' total
+ *   sum         [d] int32 (written, or read and written)
+ * rows <= 2^24 per call; keeping a running sum in range over many
+ * accumulating calls is the caller's concern.
+ */
+int uq_sum_codes(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,
+                 int32_t* sum, void* stream);
+
+/*
+ * Reconstruction R of Eq. (9) (one scale) / Eq. (13) (several scales) applied
+ * to the summed codes, with the 1/M of the averaging step of Algorithm 1/2:
+ * out_i = W * sum_i / (M * s*_i).
+ *   sum      [d] int32 (read)
+ *   M        number of workers whose codes were summed
+ *   scales   host array of K floats; for one scale K = 1 and scales = {s}
+ *   idx      [d] uint8 shared scale index; must be NULL iff K == 1
+ *   out      [d] fp32 (written)
+ * M * s_k must be exactly representable in fp32 and M * s_0 < 2^31.
+ */
+int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w,
+                  const float* scales, int32_t K, const uint8_t* idx, float* out, void* stream);
+
+/* Static text for a status code. */
+const char* uq_strerror(int status);
+
+/* Detail of the last error reported on the calling thread ("" if none). */
+const char* uq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UQ_H */

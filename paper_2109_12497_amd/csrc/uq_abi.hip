@@ -1,0 +1,294 @@
+// C ABI of libuq: argument checks on the host, then asynchronous launches.
+// Every check completes before the first HIP runtime call, so an invalid
+// call returns its status without touching the device or the runtime.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "uq.h"
+#include "uq_launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok()
+{
+    g_last_error[0] = '\0';
+    return UQ_OK;
+}
+
+bool aligned(const void* p, uintptr_t a)
+{
+    return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+constexpr int64_t kMaxRows = 65535;           // grid y-dimension
+constexpr int64_t kMaxElems = int64_t(1) << 62;
+
+bool integral(float s)
+{
+    return std::isfinite(s) && std::floor(s) == s;
+}
+
+int check_scales(const float* scales, int32_t K, uq::ScaleSet* S)
+{
+    if (K < 1 || K > UQ_MAX_SCALES)
+        return fail(UQ_ERANGE, "K = %d is outside [1, %d]", K, UQ_MAX_SCALES);
+    if (scales == nullptr)
+        return fail(UQ_EINVAL, "scales is NULL");
+    std::memset(S, 0, sizeof *S);
+    for (int32_t k = 0; k < K; ++k) {
+        const float s = scales[k];
+        if (!integral(s) || s < 1.0f)
+            return fail(UQ_ERANGE, "scales[%d] = %g is not an integer >= 1", k, (double)s);
+        if (k > 0 && !(s > scales[k - 1]))
+            return fail(UQ_ERANGE, "scales must be strictly increasing (scales[%d] = %g)", k, (double)s);
+        S->s[k] = s;
+    }
+    if (scales[0] > 127.0f)
+        return fail(UQ_ERANGE, "smallest scale %g exceeds 127 (codes are int8)", (double)scales[0]);
+    S->K = K;
+    return UQ_OK;
+}
+
+// M * s exactly representable in binary32 (finite, at most 24 significant bits).
+bool exact_product(int32_t M, float s)
+{
+    int e = 0;
+    const double frac = std::frexp(static_cast<double>(s), &e);   // s = frac * 2^e, frac in [0.5, 1)
+    uint64_t mant = static_cast<uint64_t>(std::ldexp(frac, 24));  // integral: s has <= 24 bits
+    uint64_t prod = static_cast<uint64_t>(M) * mant;
+    while (prod != 0 && (prod & 1u) == 0)
+        prod >>= 1;
+    return prod < (uint64_t(1) << 24) &&
+           static_cast<double>(M) * static_cast<double>(s) <= 3.4028234663852886e+38;
+}
+
+int check_rows(const void* p, int64_t d, int64_t rows, int64_t ld, int64_t ld_mult, const char* name)
+{
+    if (p == nullptr && d > 0)
+        return fail(UQ_EINVAL, "%s is NULL", name);
+    if (ld < d)
+        return fail(UQ_EINVAL, "leading dimension of %s (%lld) is smaller than d (%lld)", name,
+                    (long long)ld, (long long)d);
+    if (ld % ld_mult != 0)
+        return fail(UQ_EALIGN, "leading dimension of %s (%lld) is not a multiple of %lld", name,
+                    (long long)ld, (long long)ld_mult);
+    if (!aligned(p, 16))
+        return fail(UQ_EALIGN, "%s is not 16-byte aligned", name);
+    if (ld > 0 && rows > kMaxElems / ld)
+        return fail(UQ_EINVAL, "%s: rows * leading dimension overflows", name);
+    return UQ_OK;
+}
+
+int check_vec(const void* p, int64_t d, const char* name)
+{
+    if (p == nullptr && d > 0)
+        return fail(UQ_EINVAL, "%s is NULL", name);
+    if (!aligned(p, 16))
+        return fail(UQ_EALIGN, "%s is not 16-byte aligned", name);
+    return UQ_OK;
+}
+
+int check_w(const float* w)
+{
+    if (w == nullptr)
+        return fail(UQ_EINVAL, "w is NULL");
+    if (!aligned(w, 4))
+        return fail(UQ_EALIGN, "w is not 4-byte aligned");
+    return UQ_OK;
+}
+
+int check_dims(int64_t d, int64_t rows, const char* rows_name)
+{
+    if (d < 0 || d > kMaxElems)
+        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
+    if (rows < 1 || rows > kMaxRows)
+        return fail(rows < 1 ? UQ_EINVAL : UQ_ERANGE, "%s = %lld is outside [1, %lld]", rows_name,
+                    (long long)rows, (long long)kMaxRows);
+    return UQ_OK;
+}
+
+int launched(hipError_t e)
+{
+    if (e != hipSuccess)
+        return fail(UQ_EHIP, "HIP launch failed: %s", hipGetErrorString(e));
+    return ok();
+}
+
+#define UQ_TRY(expr)                  \
+    do {                              \
+        const int uq_rc_ = (expr);    \
+        if (uq_rc_ != UQ_OK)          \
+            return uq_rc_;            \
+    } while (0)
+
+}  // namespace
+
+namespace uq {
+
+int64_t grid_cap()
+{
+    static int cus_by_device[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 256 * 16;
+    if (cus_by_device[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+        cus_by_device[dev] = cus;
+    }
+    return static_cast<int64_t>(cus_by_device[dev]) * 16;
+}
+
+}  // namespace uq
+
+extern "C" {
+
+size_t uq_workspace_bytes(int64_t d, int32_t M)
+{
+    const uq::NormPlan p = uq::norm_plan(d < 0 ? 0 : d);
+    const int64_t rows = M < 1 ? 1 : M;
+    const int64_t chunks = p.nchunks < 1 ? 1 : p.nchunks;
+    const size_t bytes = static_cast<size_t>(rows) * static_cast<size_t>(chunks) * sizeof(double);
+    return (bytes + 255) / 256 * 256;
+}
+
+int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
+                    float* w, uint8_t* idx, void* ws, size_t ws_bytes, void* stream)
+{
+    UQ_TRY(check_dims(d, M, "M"));
+    UQ_TRY(check_rows(g, d, M, ldg, 4, "g"));
+    UQ_TRY(check_w(w));
+    uq::ScaleSet S;
+    if (K == 1 && scales == nullptr) {
+        std::memset(&S, 0, sizeof S);
+        S.s[0] = 1.0f;
+        S.K = 1;
+    } else {
+        UQ_TRY(check_scales(scales, K, &S));
+    }
+    if (K > 1)
+        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    if (ws == nullptr)
+        return fail(UQ_EINVAL, "ws is NULL");
+    if (!aligned(ws, 16))
+        return fail(UQ_EALIGN, "ws is not 16-byte aligned");
+    if (ws_bytes < uq_workspace_bytes(d, M))
+        return fail(UQ_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", ws_bytes,
+                    uq_workspace_bytes(d, M));
+    return launched(uq::launch_shared_scale(g, d, M, ldg, S, w, idx, static_cast<double*>(ws),
+                                            static_cast<hipStream_t>(stream)));
+}
+
+static int quantise_common(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                           const float* w, const uq::ScaleSet& S, const uint8_t* idx, uint64_t seed,
+                           int8_t* codes, int64_t ldc, void* stream)
+{
+    UQ_TRY(check_dims(d, rows, "rows"));
+    UQ_TRY(check_rows(g, d, rows, ldg, 4, "g"));
+    UQ_TRY(check_rows(codes, d, rows, ldc, 16, "codes"));
+    UQ_TRY(check_w(w));
+    if (worker0 < 0 || static_cast<int64_t>(worker0) + rows > (int64_t(1) << 31))
+        return fail(UQ_ERANGE, "worker ids %d .. %lld exceed [0, 2^31)", worker0,
+                    (long long)worker0 + rows - 1);
+    if (S.K > 1)
+        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    return launched(uq::launch_quantise(g, d, rows, ldg, worker0, w, S, idx, seed, codes, ldc,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+int uq_quantize_single(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                       int32_t s, uint64_t seed, int8_t* codes, int64_t ldc, void* stream)
+{
+    if (s < 1 || s > 127)
+        return fail(UQ_ERANGE, "s = %d is outside [1, 127]", s);
+    uq::ScaleSet S;
+    std::memset(&S, 0, sizeof S);
+    S.s[0] = static_cast<float>(s);
+    S.K = 1;
+    return quantise_common(g, d, rows, ldg, worker0, w, S, nullptr, seed, codes, ldc, stream);
+}
+
+int uq_quantize_multi(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                      const float* scales, int32_t K, const uint8_t* idx, uint64_t seed, int8_t* codes,
+                      int64_t ldc, void* stream)
+{
+    uq::ScaleSet S;
+    UQ_TRY(check_scales(scales, K, &S));
+    if (K > 1 && idx == nullptr && d > 0)
+        return fail(UQ_EINVAL, "idx is NULL");
+    return quantise_common(g, d, rows, ldg, worker0, w, S, idx, seed, codes, ldc, stream);
+}
+
+int uq_sum_codes(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate, int32_t* sum,
+                 void* stream)
+{
+    if (d < 0 || d > kMaxElems)
+        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
+    if (rows < 1)
+        return fail(UQ_EINVAL, "rows = %d is smaller than 1", rows);
+    if (rows > (1 << 24))
+        return fail(UQ_ERANGE, "rows = %d exceeds 2^24 (int32 sums could overflow)", rows);
+    if (accumulate != 0 && accumulate != 1)
+        return fail(UQ_EINVAL, "accumulate must be 0 or 1");
+    UQ_TRY(check_rows(codes, d, rows, ldc, 16, "codes"));
+    UQ_TRY(check_vec(sum, d, "sum"));
+    return launched(uq::launch_sum(codes, d, rows, ldc, accumulate, sum, static_cast<hipStream_t>(stream)));
+}
+
+int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w, const float* scales, int32_t K,
+                  const uint8_t* idx, float* out, void* stream)
+{
+    if (d < 0 || d > kMaxElems)
+        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
+    if (M < 1)
+        return fail(UQ_EINVAL, "M = %d is smaller than 1", M);
+    uq::ScaleSet S;
+    UQ_TRY(check_scales(scales, K, &S));
+    if ((K == 1) != (idx == nullptr))
+        return fail(UQ_EINVAL, "idx must be NULL exactly when K == 1");
+    for (int32_t k = 0; k < K; ++k)
+        if (!exact_product(M, S.s[k]))
+            return fail(UQ_ERANGE, "M * scales[%d] = %d * %g is not exact in fp32", k, M, (double)S.s[k]);
+    if (static_cast<double>(M) * S.s[0] >= 2147483648.0)
+        return fail(UQ_ERANGE, "M * s_0 >= 2^31 (int32 sums could overflow)");
+    UQ_TRY(check_vec(sum, d, "sum"));
+    UQ_TRY(check_vec(out, d, "out"));
+    UQ_TRY(check_w(w));
+    if (K > 1)
+        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    return launched(uq::launch_dequant(sum, d, M, w, S, idx, out, static_cast<hipStream_t>(stream)));
+}
+
+const char* uq_strerror(int status)
+{
+    switch (status) {
+    case UQ_OK: return "success";
+    case UQ_EINVAL: return "invalid argument";
+    case UQ_ERANGE: return "argument out of range";
+    case UQ_EALIGN: return "misaligned pointer or leading dimension";
+    case UQ_EWORKSPACE: return "workspace too small";
+    case UQ_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+const char* uq_last_error(void)
+{
+    return g_last_error;
+}
+
+}  // extern "C"

@@ -1,0 +1,45 @@
+// Launch planning shared by the kernels and the ABI layer of libuq.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "uq_device.hpp"
+
+namespace uq {
+
+// The norm's reduction tree: chunks of `chunk` coordinates (a multiple of
+// 8192, so every chunk starts 16-byte aligned), at most 1024 chunks per row.
+// It depends on d only, which makes W independent of the device and of the
+// launch geometry.
+struct NormPlan {
+    int64_t chunk;
+    int32_t nchunks;
+};
+
+inline NormPlan norm_plan(int64_t d)
+{
+    const int64_t base = 8192;
+    const int64_t per = base * 1024;
+    const int64_t mult = d > 0 ? (d + per - 1) / per : 1;
+    NormPlan p;
+    p.chunk = base * mult;
+    p.nchunks = static_cast<int32_t>(d > 0 ? (d + p.chunk - 1) / p.chunk : 0);
+    return p;
+}
+
+// Upper bound on blocks for the grid-stride kernels: 16 blocks of 256
+// threads per compute unit of the current device.
+int64_t grid_cap();
+
+hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
+                               float* w, uint8_t* idx, double* part, hipStream_t stream);
+hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                           const float* w, const ScaleSet& S, const uint8_t* idx, uint64_t seed,
+                           int8_t* codes, int64_t ldc, hipStream_t stream);
+hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,
+                      int32_t* sum, hipStream_t stream);
+hipError_t launch_dequant(const int32_t* sum, int64_t d, int32_t M, const float* w, const ScaleSet& S,
+                          const uint8_t* idx, float* out, hipStream_t stream);
+
+}  // namespace uq

@@ -1,0 +1,83 @@
+"""One aggregation step of Algorithm 1 / Algorithm 2 through the C ABI.
+
+`Step` owns the device buffers of a fixed problem shape and issues the
+library calls in the order of the algorithms (Sec. 3.1-3.2):
+shared scale (+ shared index) -> quantise -> integer sum -> reconstruct.
+No arithmetic of the method happens here.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import (uq_dequantize, uq_quantize_multi, uq_quantize_single, uq_shared_scale, uq_sum_codes,
+               uq_workspace_bytes)
+
+
+def round_up(x: int, m: int) -> int:
+    return (x + m - 1) // m * m
+
+
+class Step:
+    """Buffers and call sequence for M workers' gradients g [M, ldg] fp32.
+
+    streamed=False: every worker's codes are materialised ([M, ldc] int8) and
+    summed by one call.  streamed=True: one code row is reused; each worker is
+    quantised and accumulated into the int32 sum in turn.
+    """
+
+    def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None):
+        self.d, self.M = d, M
+        self.scales = [float(s) for s in scales]
+        self.K = len(self.scales)
+        self.streamed = streamed
+        self.ldc = round_up(max(d, 1), 256) if ldc is None else ldc
+        self.device = torch.device(device)
+        if self.device.type == "cuda" and self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
+        self.w = torch.zeros(4, dtype=torch.float32, device=device)  # W lives in w[0]
+        self.idx = torch.zeros(round_up(max(d, 1), 256), dtype=torch.uint8, device=device) if self.K > 1 else None
+        self.ws_bytes = uq_workspace_bytes(d, M)
+        self.ws = torch.zeros(self.ws_bytes // 8, dtype=torch.float64, device=device)
+        rows = 1 if streamed else M
+        self.codes = torch.zeros((rows, self.ldc), dtype=torch.int8, device=device)
+        self.sum = torch.zeros(round_up(max(d, 1), 64), dtype=torch.int32, device=device)
+        self.out = torch.zeros(round_up(max(d, 1), 64), dtype=torch.float32, device=device)
+
+    # -- the four stages -------------------------------------------------------
+    def shared_scale(self, g, stream=None):
+        uq_shared_scale(g, self.d, self.M, g.stride(0), self.scales, self.K, self.w, self.idx, self.ws,
+                        self.ws_bytes, stream)
+
+    def quantize(self, g, seed: int, rows: int | None = None, worker0: int = 0, codes=None, stream=None):
+        rows = self.M if rows is None else rows
+        codes = self.codes if codes is None else codes
+        if self.K == 1:
+            uq_quantize_single(g, self.d, rows, g.stride(0), worker0, self.w, int(self.scales[0]), seed, codes,
+                               codes.stride(0), stream)
+        else:
+            uq_quantize_multi(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed,
+                              codes, codes.stride(0), stream)
+
+    def sum_codes(self, rows: int | None = None, accumulate: int = 0, codes=None, stream=None):
+        rows = self.M if rows is None else rows
+        codes = self.codes if codes is None else codes
+        uq_sum_codes(codes, self.d, rows, codes.stride(0), accumulate, self.sum, stream)
+
+    def dequantize(self, stream=None):
+        uq_dequantize(self.sum, self.d, self.M, self.w, self.scales, self.K, self.idx, self.out, stream)
+
+    # -- the whole step ----------------------------------------------------------
+    def run(self, g, seed: int, stream=None):
+        """g: [M, ldg] float32 on the device.  Returns the output view [d]."""
+        assert g.dtype == torch.float32 and g.device == self.device and g.shape[0] == self.M
+        assert g.stride(1) == 1 and g.shape[1] >= self.d
+        self.shared_scale(g, stream)
+        if self.streamed:
+            for m in range(self.M):
+                self.quantize(g[m:m + 1], seed, rows=1, worker0=m, stream=stream)
+                self.sum_codes(rows=1, accumulate=1 if m > 0 else 0, stream=stream)
+        else:
+            self.quantize(g, seed, stream=stream)
+            self.sum_codes(stream=stream)
+        self.dequantize(stream)
+        return self.out[:self.d]

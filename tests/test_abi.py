@@ -1,0 +1,143 @@
+"""The C ABI contract, checked without a GPU.
+
+The library must load, export every function include/uq.h declares, and
+reject every invalid argument with the documented status before it touches
+the HIP runtime (so these calls are safe on a machine with no GPU).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "uq.h")
+
+uq = pytest.importorskip("paper_2109_12497_amd", reason="libuq.so not built")
+L = uq.lib
+
+A = 0x10000  # a 16-byte aligned stand-in address; never dereferenced by a rejected call
+S127 = [127.0]
+S4 = [127.0, 2032.0, 32512.0, 520192.0]
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\*?(uq_[a-z_]+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_five_calls():
+    names = declared_functions()
+    for name in ("uq_shared_scale", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes", "uq_dequantize",
+                 "uq_workspace_bytes", "uq_strerror", "uq_last_error"):
+        assert name in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(uq.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_strerror_and_workspace():
+    assert uq.uq_strerror(0) == "success"
+    for status in (-1, -2, -3, -4, -5):
+        assert uq.uq_strerror(status) not in ("success", "unknown status")
+    assert uq.uq_strerror(12345) == "unknown status"
+    assert uq.uq_workspace_bytes(0, 1) >= 8
+    for d, M in ((1, 1), (2 ** 20, 4), (11_173_962, 8), (2 ** 30, 16)):
+        b = uq.uq_workspace_bytes(d, M)
+        assert b % 256 == 0 and b >= 8 * M
+    assert uq.uq_workspace_bytes(2 ** 30, 16) <= 16 * 1024 * 8 + 256
+
+
+def _hs(vals):
+    return uq._HostScales(vals).array
+
+
+def status_shared(g=A, d=100, M=2, ldg=128, scales=S127, K=1, w=A, idx=A, ws=A, ws_bytes=1 << 20):
+    hs = uq._HostScales(scales)
+    return L.uq_shared_scale(g, d, M, ldg, hs.ptr, K, w, idx, ws, ws_bytes, None)
+
+
+def status_qs(g=A, d=100, rows=2, ldg=128, worker0=0, w=A, s=127, seed=1, codes=A, ldc=128):
+    return L.uq_quantize_single(g, d, rows, ldg, worker0, w, s, seed, codes, ldc, None)
+
+
+def status_qm(g=A, d=100, rows=2, ldg=128, worker0=0, w=A, scales=S4, K=4, idx=A, seed=1, codes=A, ldc=128):
+    hs = uq._HostScales(scales)
+    return L.uq_quantize_multi(g, d, rows, ldg, worker0, w, hs.ptr, K, idx, seed, codes, ldc, None)
+
+
+def status_sum(codes=A, d=100, rows=2, ldc=128, acc=0, sum_=A):
+    return L.uq_sum_codes(codes, d, rows, ldc, acc, sum_, None)
+
+
+def status_deq(sum_=A, d=100, M=2, w=A, scales=S127, K=1, idx=None, out=A):
+    hs = uq._HostScales(scales)
+    return L.uq_dequantize(sum_, d, M, w, hs.ptr, K, idx, out, None)
+
+
+E = dict(inval=uq.UQ_EINVAL, range=uq.UQ_ERANGE, align=uq.UQ_EALIGN, ws=uq.UQ_EWORKSPACE)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(g=None), "inval"), (dict(d=-1), "inval"), (dict(M=0), "inval"), (dict(M=70000), "range"),
+    (dict(ldg=64), "inval"), (dict(ldg=130), "align"), (dict(g=A + 4), "align"), (dict(w=None), "inval"),
+    (dict(w=A + 2), "align"), (dict(ws=None), "inval"), (dict(ws=A + 8), "align"), (dict(ws_bytes=8), "ws"),
+    (dict(K=0), "range"), (dict(K=17, scales=[float(i + 1) for i in range(17)]), "range"),
+    (dict(K=2, scales=[3.0, 3.0]), "range"), (dict(K=2, scales=[3.0, 2.5]), "range"),
+    (dict(K=2, scales=[3.5, 7.0]), "range"), (dict(K=2, scales=[0.0, 7.0]), "range"),
+    (dict(K=2, scales=[128.0, 256.0]), "range"), (dict(K=2, scales=[7.0, float("inf")]), "range"),
+    (dict(K=2, scales=[7.0, float("nan")]), "range"), (dict(K=2, scales=S4[:2], idx=None), "inval"),
+    (dict(K=2, scales=S4[:2], idx=A + 1), "align"), (dict(K=2, scales=None), "inval"),
+])
+def test_shared_scale_rejects(kw, want):
+    assert status_shared(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(s=0), "range"), (dict(s=128), "range"), (dict(g=None), "inval"), (dict(codes=None), "inval"),
+    (dict(w=None), "inval"), (dict(d=-5), "inval"), (dict(rows=0), "inval"), (dict(rows=65536), "range"),
+    (dict(ldg=96), "inval"), (dict(ldg=102), "align"), (dict(ldc=120), "align"), (dict(ldc=96), "inval"),
+    (dict(codes=A + 8), "align"), (dict(g=A + 8), "align"), (dict(worker0=-1), "range"),
+    (dict(worker0=2 ** 31 - 1, rows=2), "range"),
+])
+def test_quantize_single_rejects(kw, want):
+    assert status_qs(**kw) == E[want]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(idx=None), "inval"), (dict(idx=A + 4), "align"), (dict(K=0), "range"),
+    (dict(scales=[127.0, 100.0, 200.0, 300.0]), "range"), (dict(scales=None), "inval"),
+    (dict(rows=0), "inval"), (dict(w=None), "inval"),
+])
+def test_quantize_multi_rejects(kw, want):
+    assert status_qm(**kw) == E[want]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(codes=None), "inval"), (dict(sum_=None), "inval"), (dict(rows=0), "inval"),
+    (dict(rows=(1 << 24) + 1), "range"), (dict(acc=2), "inval"), (dict(ldc=120), "align"),
+    (dict(ldc=64), "inval"), (dict(sum_=A + 4), "align"), (dict(d=-1), "inval"),
+])
+def test_sum_codes_rejects(kw, want):
+    assert status_sum(**kw) == E[want]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(sum_=None), "inval"), (dict(out=None), "inval"), (dict(w=None), "inval"), (dict(M=0), "inval"),
+    (dict(idx=A), "inval"), (dict(K=4, scales=S4, idx=None), "inval"), (dict(out=A + 4), "align"),
+    (dict(M=3, K=2, scales=[7.0, 11184811.0], idx=A), "range"),  # 3 * 11184811 = 2^25 + 1
+    (dict(M=2 ** 24 + 1), "range"), (dict(M=20_000_000, scales=[127.0]), "range"),
+    (dict(K=4, scales=S4, idx=A + 2), "align"),
+])
+def test_dequantize_rejects(kw, want):
+    assert status_deq(**kw) == E[want]
+
+
+def test_binding_raises_with_detail():
+    with pytest.raises(uq.UQError) as e:
+        uq.uq_quantize_single(A, 100, 2, 128, 0, A, 200, 1, A, 128, stream=0)
+    assert e.value.status == uq.UQ_ERANGE and "s = 200" in str(e.value)

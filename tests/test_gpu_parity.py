@@ -1,0 +1,292 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar (include/uq.h arithmetic contract): scale index, codes, sums and the
+reconstructed output bit-exact; W within one binary32 ulp of the oracle's
+sequential fp64 norm, and every later stage is checked with the oracle fed
+the device's W.  Small cases span several tiles and ragged tails; the full
+workloads are checked in full where the oracle finishes in seconds and on
+sampled coordinate windows otherwise.
+"""
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only hosts, run only with a GPU
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import synth  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+import paper_2109_12497_amd as uq  # noqa: E402
+from paper_2109_12497_amd.step import Step  # noqa: E402
+
+DEV = torch.device("cuda:0")
+S_SINGLE = [127.0]
+S_MULTI4 = synth.scales_for(8, 4)
+
+
+def ulps(a, b) -> int:
+    return abs(int(np.float32(a).view(np.int32)) - int(np.float32(b).view(np.int32)))
+
+
+def gpu_step(host_g, d, scales, seed, streamed=False):
+    g = torch.from_numpy(np.ascontiguousarray(host_g)).to(DEV)
+    M = host_g.shape[0]
+    step = Step(d, M, scales, device=DEV, streamed=streamed)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    res = dict(W=np.float32(step.w[0].item()), sum=step.sum[:d].cpu().numpy(),
+               out=step.out[:d].cpu().numpy(),
+               idx=None if step.idx is None else step.idx[:d].cpu().numpy())
+    if not streamed:
+        res["codes"] = step.codes[:, :d].cpu().numpy()
+    return res, step, g
+
+
+def assert_matches_oracle(res, host_g, d, scales, seed, worker0=0):
+    ref = O.pipeline(host_g, scales, seed, d=d, W=res["W"], worker0=worker0)
+    assert ulps(res["W"], ref["W_oracle"]) <= 1, (res["W"], ref["W_oracle"])
+    if len(scales) > 1:
+        assert np.array_equal(res["idx"], ref["idx"]), "scale index differs"
+    if "codes" in res:
+        bad = np.argwhere(res["codes"] != ref["codes"])
+        assert bad.size == 0, f"codes differ at {bad[:5].tolist()}"
+    assert np.array_equal(res["sum"], ref["sum"]), "sums differ"
+    assert np.array_equal(res["out"].view(np.int32), ref["out"].view(np.int32)), "outputs differ"
+    return ref
+
+
+# ---------------------------------------------------------------------------
+# Small shapes: several tiles, ragged tails, edge values
+# ---------------------------------------------------------------------------
+
+SHAPES = [1, 2, 3, 4, 5, 7, 8, 9, 15, 16, 17, 31, 33, 255, 1000, 2049, 4097, 10007, 65539]
+
+
+@pytest.mark.parametrize("d", SHAPES)
+@pytest.mark.parametrize("scales", [S_SINGLE, [7.0], [1.0], S_MULTI4, [7.0, 112.0], synth.scales_for(8, 8)],
+                         ids=["s127", "s7", "s1", "K4", "K2", "K8"])
+def test_small_shapes(d, scales):
+    M = 3
+    host = synth.mixed_rows(M, d, seed=d, ldg=synth.round_up(d, 64))
+    res, _, _ = gpu_step(host, d, scales, seed=1000 + d)
+    assert_matches_oracle(res, host, d, scales, seed=1000 + d)
+
+
+@pytest.mark.parametrize("M", [1, 2, 5, 16])
+def test_worker_counts(M):
+    d = 12_345
+    host = synth.gaussian_rows(M, d, seed=M, ldg=synth.round_up(d, 64))
+    for scales in (S_SINGLE, S_MULTI4):
+        res, _, _ = gpu_step(host, d, scales, seed=77)
+        assert_matches_oracle(res, host, d, scales, seed=77)
+
+
+def test_seed_high_word_and_worker_offset():
+    d, M = 3001, 2
+    host = synth.gaussian_rows(M, d, seed=5, ldg=3008)
+    seed = (0xDEADBEEF << 32) | 0x12345678
+    g = torch.from_numpy(host).to(DEV)
+    step = Step(d, M, S_MULTI4, device=DEV)
+    step.shared_scale(g)
+    step.quantize(g, seed, rows=M, worker0=1000)
+    torch.cuda.synchronize()
+    W = np.float32(step.w[0].item())
+    ref = O.pipeline(host, S_MULTI4, seed, d=d, W=W, worker0=1000)
+    assert np.array_equal(step.codes[:, :d].cpu().numpy(), ref["codes"])
+
+
+def test_one_call_equals_per_worker_calls():
+    """rows = M in one call (one grid) equals M calls with rows = 1 (another grid)."""
+    d, M = 50_003, 6
+    host = synth.mixed_rows(M, d, seed=3, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(host).to(DEV)
+    for scales in (S_SINGLE, S_MULTI4):
+        step = Step(d, M, scales, device=DEV)
+        step.shared_scale(g)
+        step.quantize(g, seed=9)
+        whole = step.codes.clone()
+        for m in range(M):
+            step.quantize(g[m:m + 1], seed=9, rows=1, worker0=m, codes=step.codes[m:m + 1])
+        torch.cuda.synchronize()
+        assert torch.equal(whole, step.codes)
+
+
+def test_accumulate_equals_set():
+    d, M = 40_000, 5
+    host = synth.gaussian_rows(M, d, seed=8, ldg=40_000)
+    res, step, g = gpu_step(host, d, S_MULTI4, seed=4)
+    res_s, _, _ = gpu_step(host, d, S_MULTI4, seed=4, streamed=True)
+    assert np.array_equal(res["sum"], res_s["sum"])
+    assert np.array_equal(res["out"].view(np.int32), res_s["out"].view(np.int32))
+
+
+def test_repeatable():
+    d, M = 100_000, 4
+    host = synth.mixed_rows(M, d, seed=12, ldg=synth.round_up(d, 64))
+    a, _, _ = gpu_step(host, d, S_MULTI4, seed=5)
+    b, _, _ = gpu_step(host, d, S_MULTI4, seed=5)
+    for k in ("W", "sum", "out", "idx", "codes"):
+        assert np.array_equal(np.asarray(a[k]), np.asarray(b[k]))
+
+
+# ---------------------------------------------------------------------------
+# Degenerate cases
+# ---------------------------------------------------------------------------
+
+def test_zero_gradients():
+    d, M = 1025, 3
+    host = np.zeros((M, 1088), dtype=np.float32)
+    for scales in (S_SINGLE, S_MULTI4):
+        res, _, _ = gpu_step(host, d, scales, seed=1)
+        assert res["W"] == 0 and not res["codes"].any() and not res["sum"].any() and not res["out"].any()
+        if len(scales) > 1:
+            assert np.all(res["idx"] == len(scales) - 1)
+
+
+@pytest.mark.parametrize("bad", [np.inf, -np.inf, np.nan])
+def test_non_finite_inputs_take_zero_path(bad):
+    d, M = 999, 2
+    host = synth.gaussian_rows(M, d, seed=2, ldg=1024)
+    host[1, 500] = bad
+    for scales in (S_SINGLE, S_MULTI4):
+        res, _, _ = gpu_step(host, d, scales, seed=1)
+        assert not np.isfinite(res["W"])
+        assert not res["codes"].any() and not res["out"].any()
+        assert_matches_oracle(res, host, d, scales, seed=1)
+
+
+@pytest.mark.parametrize("W", [0.0, -1.0, np.inf, np.nan, 1e-45, 3e-38])
+def test_forced_scale_values(W):
+    """Stages after the norm with a caller-chosen W, including the zero path
+    and W small enough that the larger scales' reciprocals overflow."""
+    d, M = 4099, 3
+    host = synth.mixed_rows(M, d, seed=6, ldg=4160) * np.float32(1e-30)
+    g = torch.from_numpy(host).to(DEV)
+    for scales in (S_SINGLE, synth.scales_for(8, 8)):
+        step = Step(d, M, scales, device=DEV)
+        step.w.fill_(float(W))
+        if len(scales) > 1:
+            idx_host = O.scale_index_shared(host, np.float32(W), scales, d=d)
+            step.idx[:d].copy_(torch.from_numpy(idx_host))
+        step.quantize(g, seed=3)
+        step.sum_codes()
+        step.dequantize()
+        torch.cuda.synchronize()
+        ref = O.pipeline(host, scales, 3, d=d, W=np.float32(W))
+        assert np.array_equal(step.codes[:, :d].cpu().numpy(), ref["codes"])
+        assert np.array_equal(step.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
+def test_index_entries_beyond_K_read_as_last():
+    d, M = 777, 2
+    host = synth.gaussian_rows(M, d, seed=4, ldg=832)
+    g = torch.from_numpy(host).to(DEV)
+    step = Step(d, M, S_MULTI4, device=DEV)
+    step.shared_scale(g)
+    torch.cuda.synchronize()
+    idx_host = np.random.default_rng(0).integers(0, 256, size=d).astype(np.uint8)
+    step.idx[:d].copy_(torch.from_numpy(idx_host))
+    step.quantize(g, seed=8)
+    step.sum_codes()
+    step.dequantize()
+    torch.cuda.synchronize()
+    W = np.float32(step.w[0].item())
+    codes = np.stack([O.quantize(host[m, :d], W, S_MULTI4, 8, worker=m, idx=idx_host) for m in range(M)])
+    assert np.array_equal(step.codes[:, :d].cpu().numpy(), codes)
+    out = O.dequantize(O.sum_codes(codes), M, W, S_MULTI4, idx_host)
+    assert np.array_equal(step.out[:d].cpu().numpy().view(np.int32), out.view(np.int32))
+
+
+def test_empty_vector():
+    step = Step(0, 2, S_MULTI4, device=DEV)
+    g = torch.ones((2, 64), device=DEV)
+    step.w.fill_(7.0)
+    step.run(g, seed=1)
+    torch.cuda.synchronize()
+    assert step.w[0].item() == 0.0
+
+
+# ---------------------------------------------------------------------------
+# The paper-shaped workloads at full size, in the launch configuration the
+# benchmark times (the same Step calls)
+# ---------------------------------------------------------------------------
+
+def device_norm_check(g, d, W):
+    """W within one ulp of RN32(sqrt(max_m sum g^2)) computed by torch in fp64."""
+    best = 0.0
+    for m in range(g.shape[0]):
+        s = 0.0
+        for c in range(0, d, 1 << 26):
+            x = g[m, c:min(d, c + (1 << 26))].double()
+            s += float(torch.dot(x, x))
+        best = max(best, s)
+    assert ulps(W, np.float32(math.sqrt(best))) <= 1
+
+
+def check_windows(step, g, d, scales, seed, windows, streamed):
+    W = np.float32(step.w[0].item())
+    M = g.shape[0]
+    for i0, n in windows:
+        i1 = min(d, i0 + n)
+        host = g[:, i0:i1].cpu().numpy()
+        idx = O.scale_index_shared(host, W, scales) if len(scales) > 1 else None
+        if idx is not None:
+            assert np.array_equal(step.idx[i0:i1].cpu().numpy(), idx), f"idx window {i0}"
+        codes = np.stack([O.quantize(host[m], W, scales, seed, worker=m, i0=i0, idx=idx) for m in range(M)])
+        if not streamed:
+            assert np.array_equal(step.codes[:, i0:i1].cpu().numpy(), codes), f"codes window {i0}"
+        sums = O.sum_codes(codes)
+        assert np.array_equal(step.sum[i0:i1].cpu().numpy(), sums), f"sum window {i0}"
+        out = O.dequantize(sums, M, W, scales, idx)
+        assert np.array_equal(step.out[i0:i1].cpu().numpy().view(np.int32), out.view(np.int32)), f"out {i0}"
+
+
+def sample_windows(d, n_windows=12, width=1 << 14, seed=0):
+    rng = np.random.default_rng(seed)
+    starts = [0, max(0, d - width - 5)] + [int(x) for x in rng.integers(0, d - width, size=n_windows)]
+    return [(s, width + 5) for s in starts]
+
+
+@pytest.mark.parametrize("name", ["small-gaussian", "resnet18", "resnet50"])
+def test_workload_full_parity(name):
+    g, cfg = synth.make_gradients(name, device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    step = Step(d, M, scales, device=DEV)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    host = g[:, :d].cpu().numpy()
+    res = dict(W=np.float32(step.w[0].item()), codes=step.codes[:, :d].cpu().numpy(),
+               sum=step.sum[:d].cpu().numpy(), out=step.out[:d].cpu().numpy(),
+               idx=None if step.idx is None else step.idx[:d].cpu().numpy())
+    assert_matches_oracle(res, host, d, scales, seed)
+
+
+@pytest.mark.parametrize("name", ["vgg16-single", "vgg16-multi"])
+def test_workload_sampled_parity(name):
+    g, cfg = synth.make_gradients(name, device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    step = Step(d, M, scales, device=DEV)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    device_norm_check(g, d, np.float32(step.w[0].item()))
+    check_windows(step, g, d, scales, seed, sample_windows(d, seed=d), streamed=False)
+    # properties over every coordinate: sum = integer sum of the rows' codes
+    assert torch.equal(step.codes[:, :d].to(torch.int32).sum(dim=0), step.sum[:d])
+    assert int(step.codes[:, :d].abs().max()) <= scales[0]
+
+
+def test_student_t_streamed_sampled_parity():
+    cfg = synth.WORKLOADS["student-t"]
+    g, cfg = synth.make_gradients("student-t", device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    step = Step(d, M, scales, device=DEV, streamed=True)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    device_norm_check(g, d, np.float32(step.w[0].item()))
+    check_windows(step, g, d, scales, seed, sample_windows(d, n_windows=8, seed=5), streamed=True)
+    assert int(step.sum[:d].abs().max()) <= M * scales[0]
