@@ -34,7 +34,7 @@ def algorithmic_bytes(d: int, M: int, K: int, streamed: bool) -> dict:
     multi = K > 1
     b = {
         "shared_scale": 4 * M * d + (4 * M * d + d if multi else 0),
-        "quantize": M * d * (4 + 1 + (1 if multi else 0)),
+        "quantize": M * d * (4 + 1) + (d if multi else 0),  # the shared index is read once
         "sum": (M * d + 4 * d) if not streamed else (d + 4 * d) + (M - 1) * (d + 8 * d),
         "dequantize": d * (4 + 4 + (1 if multi else 0)),
     }

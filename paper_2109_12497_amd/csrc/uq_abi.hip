@@ -143,14 +143,14 @@ int64_t grid_cap()
     static int cus_by_device[64] = {0};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
-        return 256 * 16;
+        return 256 * 64;
     if (cus_by_device[dev] == 0) {
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
         cus_by_device[dev] = cus;
     }
-    return static_cast<int64_t>(cus_by_device[dev]) * 16;
+    return static_cast<int64_t>(cus_by_device[dev]) * 64;
 }
 
 }  // namespace uq

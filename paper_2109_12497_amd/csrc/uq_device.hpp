@@ -49,7 +49,8 @@ struct ScaleSet {
 // Philox4x32-10 block function: ten rounds, each multiplying counter words 0
 // and 2 by the Philox multipliers (32x32 -> 64 bit), xoring the high halves
 // into the other two words together with the round key, and permuting; the
-// key advances by the Weyl increments after every round.
+// key advances by the Weyl increments after every round.  The three-way xors
+// are single v_bitop3_b32 instructions (truth table 0x96 = a ^ b ^ c).
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                                uint32_t k0, uint32_t k1)
 {
@@ -57,8 +58,8 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
     for (int round = 0; round < 10; ++round) {
         const uint64_t pa = static_cast<uint64_t>(0xD2511F53u) * c0;
         const uint64_t pb = static_cast<uint64_t>(0xCD9E8D57u) * c2;
-        const uint32_t n0 = static_cast<uint32_t>(pb >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = static_cast<uint32_t>(pa >> 32) ^ c3 ^ k1;
+        const uint32_t n0 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(pb >> 32), c1, k0, 0x96);
+        const uint32_t n2 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(pa >> 32), c3, k1, 0x96);
         c1 = static_cast<uint32_t>(pb);
         c3 = static_cast<uint32_t>(pa);
         c0 = n0;
@@ -82,32 +83,31 @@ __device__ __forceinline__ bool zero_path(float W, float inv0)
     return !(W > 0.0f) || !(W <= kFloatMax) || !(inv0 <= kFloatMax);
 }
 
-// |g| usable for quantisation: positive and finite (false for 0, NaN, inf).
-__device__ __forceinline__ bool usable(float a)
-{
-    return a > 0.0f && a <= kFloatMax;
-}
+// v_cmp_class mask for finite nonzero values (+-normal, +-denormal).
+constexpr int kFiniteNonzero = (1 << 3) | (1 << 4) | (1 << 7) | (1 << 8);
 
-// Stochastic level choice for one coordinate given the high 16 bits of its
-// uniform word.  Returns the code assuming the low 16 bits do not matter and
-// reports in *tie whether they do (high half equal to the threshold's high
-// half with a nonzero low threshold); *tlow receives the threshold's low half.
-__device__ __forceinline__ int32_t quantise_hi(float v, float inv, float s0, uint32_t hi16,
-                                               bool ok, bool* tie, uint32_t* tlow, int32_t* level)
+// Stochastic level choice for one coordinate from the high 16 bits of its
+// uniform word.  inv is 0 on the zero path, so every code is then 0.
+//   x = min(|v| * inv, s0)   (0 for zero / NaN / inf v)
+//   l = floor(x), t = floor((x - l) * 2^32), code = sign(v) * (l + [r < t])
+// With only r's high half known, [r < t] is decided unless the halves tie
+// (hi16 == t >> 16), reported in *tie; *t_out and *l_out let the caller
+// finish a tie with r's low half.  Returns the signed code as a float.
+__device__ __forceinline__ float quantise_hi(float v, float inv, float s0, uint32_t hi16, bool* tie,
+                                             uint32_t* t_out, float* l_out)
 {
-    const float a = fabsf(v);
-    float x = a * inv;
-    x = x > s0 ? s0 : x;
+    const bool ok = __builtin_amdgcn_classf(v, kFiniteNonzero);
+    float x = fabsf(v) * inv;
+    x = ok ? x : 0.0f;
+    x = fminf(x, s0);
     const float lf = floorf(x);
-    const int32_t l = static_cast<int32_t>(lf);
-    const float p = x - lf;
-    const uint32_t t = static_cast<uint32_t>(p * 4294967296.0f);
+    const uint32_t t = static_cast<uint32_t>((x - lf) * 4294967296.0f);
     const uint32_t th = t >> 16;
-    *tlow = t & 0xFFFFu;
-    *tie = ok && hi16 == th && (*tlow != 0u);
-    *level = l;
-    const int32_t mag = l + (hi16 < th ? 1 : 0);
-    return ok ? (v < 0.0f ? -mag : mag) : 0;
+    *tie = hi16 == th;
+    *t_out = t;
+    *l_out = lf;
+    const float mag = lf + (hi16 < th ? 1.0f : 0.0f);
+    return copysignf(mag, v);
 }
 
 __device__ __forceinline__ uint32_t pack4(int32_t a, int32_t b, int32_t c, int32_t d)

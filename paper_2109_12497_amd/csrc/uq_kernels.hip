@@ -78,33 +78,50 @@ __global__ __launch_bounds__(kBlock) void k_sumsq(const float* __restrict__ g, i
 }
 
 // ---------------------------------------------------------------------------
-// Norm, pass 2 (one block): S_m = fixed-order sum of row m's chunk partials;
+// Norm, pass 2 (one block): S_m = fixed-order sum of row m's chunk partials
+// (lane-strided sequential sums, then a fixed butterfly), one wave per row;
 // W = RN32(sqrt(max_m S_m)), NaN if any S_m is NaN.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_finish(const double* __restrict__ part, int32_t nchunks,
                                                    int32_t M, float* __restrict__ w)
 {
-    __shared__ double wave_part[kBlock / 64];
+    __shared__ double wave_best[kBlock / 64];
+    __shared__ int wave_nan[kBlock / 64];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     double best = 0.0;
     bool any_nan = false;
-    for (int32_t m = 0; m < M; ++m) {
+    for (int32_t m = wave; m < M; m += kBlock / 64) {
+        // nchunks <= 1024: at most 16 partials per lane, all loads in flight at once
         const double* p = part + static_cast<int64_t>(m) * nchunks;
+        double x[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int32_t c = lane + 64 * j;
+            x[j] = c < nchunks ? p[c] : 0.0;
+        }
         double s = 0.0;
-        for (int32_t c = threadIdx.x; c < nchunks; c += kBlock)
-            s += p[c];
-        s = wave_sum(s);
-        if (lane == 0)
-            wave_part[wave] = s;
-        __syncthreads();
-        const double S = (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
-        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            s += x[j];
+        const double S = wave_sum(s);
         any_nan = any_nan || (S != S);
         best = S > best ? S : best;
     }
-    if (threadIdx.x == 0)
-        *w = any_nan ? __builtin_nanf("") : static_cast<float>(sqrt(best));
+    if (lane == 0) {
+        wave_best[wave] = best;
+        wave_nan[wave] = any_nan ? 1 : 0;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double b = 0.0;
+        int nan = 0;
+        for (int i = 0; i < kBlock / 64; ++i) {
+            b = wave_best[i] > b ? wave_best[i] : b;
+            nan |= wave_nan[i];
+        }
+        *w = nan ? __builtin_nanf("") : static_cast<float>(sqrt(b));
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -183,113 +200,190 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 // ---------------------------------------------------------------------------
 // Quantisation.  One thread handles a group of 8 consecutive coordinates,
 // which is exactly one Philox block: its eight 16-bit halves are the high
-// halves of the coordinates' uniform words.  The low halves (a second block
-// with counter word 3 = 1) are drawn only for the rare coordinates whose high
-// half equals the threshold's (probability 2^-16 each).
+// halves of the coordinates' uniform words (coordinate j < 4 takes the low
+// half of word j, coordinate j >= 4 the high half of word j - 4).  The low
+// halves (a second block with counter word 3 = 1) are drawn only when some
+// coordinate's high half ties its threshold's (probability 2^-16 each).
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t half_of(const uint32_t w[4], int j)
+{
+    return j < 4 ? (w[j] & 0xFFFFu) : (w[j - 4] >> 16);
+}
+
+// Quantise the 8 coordinates v[] of group q of `worker`; returns the codes.
+__device__ __forceinline__ void quantise_group(const float v[8], const float inv[8], float s0, uint64_t q,
+                                               uint32_t worker, uint32_t key0, uint32_t key1, int32_t code[8])
+{
+    const uint4 hi = philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 0u,
+                                   key0, key1);
+    const uint32_t hw[4] = {hi.x, hi.y, hi.z, hi.w};
+    float c[8], lf[8];
+    uint32_t t[8];
+    bool tie[8];
+    bool any_tie = false;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        c[j] = quantise_hi(v[j], inv[j], s0, half_of(hw, j), &tie[j], &t[j], &lf[j]);
+        any_tie = any_tie || tie[j];
+    }
+    if (__builtin_expect(any_tie, 0)) {
+        const uint4 lo = philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 1u,
+                                       key0, key1);
+        const uint32_t lw[4] = {lo.x, lo.y, lo.z, lo.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (tie[j])
+                c[j] = copysignf(lf[j] + (half_of(lw, j) < (t[j] & 0xFFFFu) ? 1.0f : 0.0f), v[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        code[j] = static_cast<int32_t>(c[j]);
+}
+
+// Wave tiles.  A wave quantises 512 consecutive coordinates (64 Philox blocks)
+// with perfectly coalesced accesses: lane t holds coordinates 4t..4t+3 ("A")
+// and 256+4t..256+4t+3 ("B") of the tile.  The A coordinates of lanes 2u and
+// 2u+1 form block 64T+u, their B coordinates block 64T+32+u.  Even lane 2u
+// computes block 64T+u, odd lane 2u+1 block 64T+32+u, and the pair swaps the
+// 16-bit halves the other needs with one DPP move per word pair.
+__device__ __forceinline__ uint32_t swap_pair(uint32_t x)
+{
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xF, 0xF, false));
+}
+
+// Halves of this lane's A and B coordinates from its own block's words w:
+// a01/a23 pack coordinates A0..A3 (coordinate 2k in the low half), b01/b23
+// likewise for B.  Even lanes keep the low halves of their own words (their
+// A coordinates) and receive the partner's low halves (their B coordinates);
+// odd lanes keep high halves (B) and receive the partner's high halves (A).
+__device__ __forceinline__ void tile_halves(uint4 w, bool odd, uint32_t* a01, uint32_t* a23, uint32_t* b01,
+                                            uint32_t* b23)
+{
+    const uint32_t sel_lo = 0x05040100u;  // low halves of (src1, src0)
+    const uint32_t sel_hi = 0x07060302u;  // high halves of (src1, src0)
+    const uint32_t sel_keep = odd ? sel_hi : sel_lo;
+    const uint32_t sel_send = odd ? sel_lo : sel_hi;
+    const uint32_t keep01 = __builtin_amdgcn_perm(w.y, w.x, sel_keep);
+    const uint32_t keep23 = __builtin_amdgcn_perm(w.w, w.z, sel_keep);
+    const uint32_t recv01 = swap_pair(__builtin_amdgcn_perm(w.y, w.x, sel_send));
+    const uint32_t recv23 = swap_pair(__builtin_amdgcn_perm(w.w, w.z, sel_send));
+    *a01 = odd ? recv01 : keep01;
+    *a23 = odd ? recv23 : keep23;
+    *b01 = odd ? keep01 : recv01;
+    *b23 = odd ? keep23 : recv23;
+}
+
+__device__ __forceinline__ uint32_t half16(uint32_t packed01, uint32_t packed23, int j)
+{
+    const uint32_t w = j < 2 ? packed01 : packed23;
+    return (j & 1) ? (w >> 16) : (w & 0xFFFFu);
+}
+
 template <bool MULTI>
 __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g, int64_t d, int64_t ldg,
                                                      int32_t worker0, const float* __restrict__ wptr,
                                                      ScaleSet S, const uint8_t* __restrict__ idx,
                                                      uint32_t key0, uint32_t key1,
-                                                     int8_t* __restrict__ codes, int64_t ldc)
+                                                     int8_t* __restrict__ codes, int64_t ldc, int32_t tpw)
 {
     __shared__ float inv_s[kMaxScales];
     const float W = *wptr;
-    float inv0;
+    // tables; on the zero path every entry is 0, which makes every code 0
+    const bool zero = zero_path(W, div_rn32(S.s[0], W));
+    float inv0 = 0.0f;
     if (MULTI) {
         if (threadIdx.x < S.K)
-            inv_s[threadIdx.x] = div_rn32(S.s[threadIdx.x], W);
+            inv_s[threadIdx.x] = zero ? 0.0f : div_rn32(S.s[threadIdx.x], W);
         __syncthreads();
-        inv0 = inv_s[0];
     } else {
-        inv0 = div_rn32(S.s[0], W);
+        inv0 = zero ? 0.0f : div_rn32(S.s[0], W);
     }
-    const bool zero = zero_path(W, inv0);
     const float s0 = S.s[0];
-    const int32_t kmax = S.K - 1;
+    const uint32_t kmax = static_cast<uint32_t>(S.K - 1);
 
     const int32_t r = blockIdx.y;
     const uint32_t worker = static_cast<uint32_t>(worker0) + static_cast<uint32_t>(r);
     const float* row = g + static_cast<int64_t>(r) * ldg;
     int8_t* out = codes + static_cast<int64_t>(r) * ldc;
 
-    const int64_t nfull = d >> 3;
-    const int64_t ngroups = (d + 7) >> 3;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < ngroups; q += stride) {
-        const int64_t base = q << 3;
-        const bool full = q < nfull;
-        float v[8];
+    const int lane = threadIdx.x & 63;
+    const bool odd = (lane & 1) != 0;
+    // each wave takes `tpw` consecutive tiles, then strides by the grid
+    const int64_t ntiles = d >> 9;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
+    const int64_t wave_id = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + (threadIdx.x >> 6);
+    for (int64_t c0 = wave_id * tpw; c0 < ntiles; c0 += nwaves * tpw) {
+      const int64_t c1 = c0 + tpw < ntiles ? c0 + tpw : ntiles;
+      for (int64_t T = c0; T < c1; ++T) {
+        const int64_t a_off = (T << 9) + 4 * lane;
+        const int64_t b_off = a_off + 256;
+        const f32x4 A = load_nt(row + a_off);
+        const f32x4 B = load_nt(row + b_off);
+        float v[8] = {A.x, A.y, A.z, A.w, B.x, B.y, B.z, B.w};
         float inv[8];
-        if (full) {
-            const f32x4 a = load_nt(row + base);
-            const f32x4 b = load_nt(row + base + 4);
-            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                v[j] = base + j < d ? row[base + j] : 0.0f;
-        }
         if (MULTI) {
-            uint8_t k8[8];
-            if (full) {
-                const uint2 kk = *reinterpret_cast<const uint2*>(idx + base);
+            const uint32_t ka = *reinterpret_cast<const uint32_t*>(idx + a_off);
+            const uint32_t kb = *reinterpret_cast<const uint32_t*>(idx + b_off);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    k8[j] = static_cast<uint8_t>(kk.x >> (8 * j));
-                    k8[j + 4] = static_cast<uint8_t>(kk.y >> (8 * j));
-                }
-            } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    k8[j] = base + j < d ? idx[base + j] : 0;
-            }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int32_t k = k8[j] < kmax ? k8[j] : kmax;
-                inv[j] = inv_s[k];
+            for (int j = 0; j < 4; ++j) {
+                inv[j] = inv_s[min((ka >> (8 * j)) & 0xFFu, kmax)];
+                inv[j + 4] = inv_s[min((kb >> (8 * j)) & 0xFFu, kmax)];
             }
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 inv[j] = inv0;
         }
-
-        const uint4 hi = philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker,
-                                       0u, key0, key1);
-        const uint32_t hw[4] = {hi.x, hi.y, hi.z, hi.w};
-        int32_t code[8], level[8];
-        uint32_t tlow[8];
+        const uint64_t q = static_cast<uint64_t>(T << 6) + static_cast<uint64_t>(lane >> 1) + (odd ? 32u : 0u);
+        uint32_t a01, a23, b01, b23;
+        tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 0u, key0,
+                                  key1),
+                    odd, &a01, &a23, &b01, &b23);
+        float c[8], lf[8];
+        uint32_t t[8];
         bool tie[8];
         bool any_tie = false;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const uint32_t h16 = j < 4 ? (hw[j] & 0xFFFFu) : (hw[j - 4] >> 16);
-            const bool ok = !zero && usable(fabsf(v[j]));
-            code[j] = quantise_hi(v[j], inv[j], s0, h16, ok, &tie[j], &tlow[j], &level[j]);
+            const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
+            c[j] = quantise_hi(v[j], inv[j], s0, h, &tie[j], &t[j], &lf[j]);
             any_tie = any_tie || tie[j];
         }
-        if (any_tie) {
-            const uint4 lo = philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32),
-                                           worker, 1u, key0, key1);
-            const uint32_t lw[4] = {lo.x, lo.y, lo.z, lo.w};
+        // wave-uniform branch (the DPP exchange needs every lane): draw the
+        // low halves from the purpose-1 blocks when any lane has a tie
+        if (__builtin_expect(__ballot(any_tie) != 0, 0)) {
+            tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 1u, key0,
+                                      key1),
+                        odd, &a01, &a23, &b01, &b23);
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                if (tie[j]) {
-                    const uint32_t l16 = j < 4 ? (lw[j] & 0xFFFFu) : (lw[j - 4] >> 16);
-                    const int32_t mag = level[j] + (l16 < tlow[j] ? 1 : 0);
-                    code[j] = v[j] < 0.0f ? -mag : mag;
-                }
+                const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
+                if (tie[j])
+                    c[j] = copysignf(lf[j] + (h < (t[j] & 0xFFFFu) ? 1.0f : 0.0f), v[j]);
             }
         }
-        if (full) {
-            uint2 packed;
-            packed.x = pack4(code[0], code[1], code[2], code[3]);
-            packed.y = pack4(code[4], code[5], code[6], code[7]);
-            *reinterpret_cast<uint2*>(out + base) = packed;
-        } else {
+        *reinterpret_cast<uint32_t*>(out + a_off) = pack4(static_cast<int32_t>(c[0]), static_cast<int32_t>(c[1]),
+                                                          static_cast<int32_t>(c[2]), static_cast<int32_t>(c[3]));
+        *reinterpret_cast<uint32_t*>(out + b_off) = pack4(static_cast<int32_t>(c[4]), static_cast<int32_t>(c[5]),
+                                                          static_cast<int32_t>(c[6]), static_cast<int32_t>(c[7]));
+      }
+    }
+
+    // Coordinates past the last whole tile (fewer than 512): groups of 8
+    // contiguous coordinates, one per lane of the first wave of block x = 0.
+    if (blockIdx.x == 0 && threadIdx.x < 64) {
+        const int64_t q = (ntiles << 6) + threadIdx.x;
+        const int64_t base = q << 3;
+        if (base < d) {
+            float v[8], inv[8];
+            int32_t code[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const bool in = base + j < d;
+                v[j] = in ? row[base + j] : 0.0f;
+                inv[j] = MULTI ? inv_s[min(static_cast<uint32_t>(in ? idx[base + j] : 0), kmax)] : inv0;
+            }
+            quantise_group(v, inv, s0, static_cast<uint64_t>(q), worker, key0, key1, code);
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 if (base + j < d)
@@ -307,32 +401,69 @@ __device__ __forceinline__ int32_t sbyte(uint32_t w, int j)
     return static_cast<int32_t>(static_cast<int8_t>(w >> (8 * j)));
 }
 
+// Block tiles of 4096 coordinates: thread t sums quads t, t+256, t+512 and
+// t+768 of the tile, so every row load and every store of a wave covers
+// 256 or 1024 contiguous bytes; rows are read four at a time.
+constexpr int64_t kSumTile = 4096;
+
 __global__ __launch_bounds__(kBlock) void k_sum(const int8_t* __restrict__ codes, int64_t d, int32_t rows,
                                                 int64_t ldc, int32_t accumulate, int32_t* __restrict__ sum)
 {
-    const int64_t nquad = d >> 2;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nquad; q += stride) {
-        int4 acc = make_int4(0, 0, 0, 0);
-        if (accumulate)
-            acc = *reinterpret_cast<const int4*>(sum + (q << 2));
-        const int8_t* p = codes + (q << 2);
-        for (int32_t r = 0; r < rows; ++r) {
-            const uint32_t w = load_nt_u32(p + static_cast<int64_t>(r) * ldc);
-            acc.x += sbyte(w, 0);
-            acc.y += sbyte(w, 1);
-            acc.z += sbyte(w, 2);
-            acc.w += sbyte(w, 3);
+  for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
+       tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
+    const int64_t base = tile0 + 4 * threadIdx.x;
+    if (tile0 + kSumTile <= d) {
+        int32_t acc[16];
+        if (accumulate) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int4 a = *reinterpret_cast<const int4*>(sum + base + 1024 * c);
+                acc[4 * c] = a.x; acc[4 * c + 1] = a.y; acc[4 * c + 2] = a.z; acc[4 * c + 3] = a.w;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+                acc[j] = 0;
         }
-        *reinterpret_cast<int4*>(sum + (q << 2)) = acc;
+        int32_t r = 0;
+        for (; r + 4 <= rows; r += 4) {
+            uint32_t w[4][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    w[u][c] = load_nt_u32(codes + static_cast<int64_t>(r + u) * ldc + base + 1024 * c);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[4 * c + j] += sbyte(w[u][c], j);
+        }
+        for (; r < rows; ++r) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t w = load_nt_u32(codes + static_cast<int64_t>(r) * ldc + base + 1024 * c);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[4 * c + j] += sbyte(w, j);
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            *reinterpret_cast<int4*>(sum + base + 1024 * c) =
+                make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
+    } else {
+        // the last, partial tile: one coordinate at a time
+        for (int64_t i = tile0 + threadIdx.x; i < d; i += kBlock) {
+            int32_t acc = accumulate ? sum[i] : 0;
+            for (int32_t r = 0; r < rows; ++r)
+                acc += codes[static_cast<int64_t>(r) * ldc + i];
+            sum[i] = acc;
+        }
     }
-    const int64_t t = (nquad << 2) + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (blockIdx.x == 0 && t < d) {
-        int32_t acc = accumulate ? sum[t] : 0;
-        for (int32_t r = 0; r < rows; ++r)
-            acc += codes[static_cast<int64_t>(r) * ldc + t];
-        sum[t] = acc;
-    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -391,6 +522,27 @@ __global__ __launch_bounds__(kBlock) void k_dequant(const int32_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // Host-side launchers (called by the ABI layer after validation).
 // ---------------------------------------------------------------------------
+// Tiles per wave for the quantiser.  Launch-shape sweeps on MI355X with cold
+// caches: one tile per wave (a one-shot grid) is fastest for one scale; with
+// several scales two consecutive tiles per wave amortise the per-block table
+// set-up and read the shared index in longer runs.
+static int32_t quantise_tiles_per_wave(int32_t K)
+{
+    return K > 1 ? 2 : 1;
+}
+
+// Enough blocks for every unit to get its own thread / wave / tile (the
+// streaming kernels run fastest as one pass with no grid-stride reuse).  The
+// dispatch packet counts work-items in 32 bits, so the grid is capped at 2^22
+// blocks; every kernel strides over whatever the grid does not cover.
+static unsigned one_shot(int64_t units, int64_t per_block)
+{
+    const int64_t kMaxBlocks = int64_t(1) << 22;
+    int64_t blocks = (units + per_block - 1) / per_block;
+    blocks = blocks < 1 ? 1 : (blocks > kMaxBlocks ? kMaxBlocks : blocks);
+    return static_cast<unsigned>(blocks);
+}
+
 static unsigned grid_for(int64_t units, int64_t cap)
 {
     int64_t blocks = (units + kBlock - 1) / kBlock;
@@ -409,7 +561,7 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
     }
     hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, stream, part, plan.nchunks, M, w);
     if (S.K > 1 && d > 0) {
-        const unsigned gx = grid_for((d + 3) / 4, grid_cap());
+        const unsigned gx = one_shot((d + 3) / 4, kBlock);
         hipLaunchKernelGGL(k_index, dim3(gx), dim3(kBlock), 0, stream, g, d, M, ldg, w, S, idx);
     }
     return hipGetLastError();
@@ -421,19 +573,18 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
 {
     if (d == 0)
         return hipSuccess;
-    int64_t cap = grid_cap() / rows;
-    if (cap < 1)
-        cap = 1;
-    const unsigned gx = grid_for((d + 7) / 8, cap);
+    // `tpw` consecutive 512-coordinate tiles per wave, four waves per block
+    const int32_t tpw = quantise_tiles_per_wave(S.K);
+    const unsigned gx = one_shot(d >> 9, (kBlock / 64) * tpw);
     const uint32_t key0 = static_cast<uint32_t>(seed);
     const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
     dim3 grid(gx, static_cast<unsigned>(rows));
     if (S.K > 1)
         hipLaunchKernelGGL(k_quantise<true>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx,
-                           key0, key1, codes, ldc);
+                           key0, key1, codes, ldc, tpw);
     else
         hipLaunchKernelGGL(k_quantise<false>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S,
-                           idx, key0, key1, codes, ldc);
+                           idx, key0, key1, codes, ldc, tpw);
     return hipGetLastError();
 }
 
@@ -442,7 +593,7 @@ hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc,
 {
     if (d == 0)
         return hipSuccess;
-    const unsigned gx = grid_for((d + 3) / 4, grid_cap());
+    const unsigned gx = one_shot(d, kSumTile);
     hipLaunchKernelGGL(k_sum, dim3(gx), dim3(kBlock), 0, stream, codes, d, rows, ldc, accumulate, sum);
     return hipGetLastError();
 }

@@ -28,7 +28,7 @@ inline NormPlan norm_plan(int64_t d)
     return p;
 }
 
-// Upper bound on blocks for the grid-stride kernels: 16 blocks of 256
+// Upper bound on blocks for the grid-stride kernels: 64 blocks of 256
 // threads per compute unit of the current device.
 int64_t grid_cap();
 
