@@ -24,56 +24,55 @@ namespace uq {
 // in binary64 (each square exact) and stores the partial in part[m*nchunks+c].
 // chunk is a multiple of 1024, so every chunk starts 16-byte aligned.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_sumsq(const float* __restrict__ g, int64_t d, int64_t ldg,
-                                                  int64_t chunk, int32_t nchunks,
+__global__ __launch_bounds__(kBlock) void k_sumsq(const float* __restrict__ g, int64_t d, int32_t M,
+                                                  int64_t ldg, int64_t chunk, int32_t nchunks,
                                                   double* __restrict__ part)
 {
-    const int32_t c = blockIdx.x;
-    const int32_t m = blockIdx.y;
-    const float* row = g + static_cast<int64_t>(m) * ldg;
-    const int64_t begin = static_cast<int64_t>(c) * chunk;
-    const int64_t end = begin + chunk < d ? begin + chunk : d;
-    const int64_t nvec = (end - begin) >> 2;
-    const float* v4 = row + begin;
-
-    double acc0 = 0.0, acc1 = 0.0, acc2 = 0.0, acc3 = 0.0;
-    int64_t j = threadIdx.x;
-    for (; j + 3 * kBlock < nvec; j += 4 * kBlock) {
-        const f32x4 a = load_nt(v4 + 4 * (j));
-        const f32x4 b = load_nt(v4 + 4 * (j + kBlock));
-        const f32x4 e = load_nt(v4 + 4 * (j + 2 * kBlock));
-        const f32x4 f = load_nt(v4 + 4 * (j + 3 * kBlock));
-        acc0 = fma((double)a.x, (double)a.x, acc0); acc1 = fma((double)a.y, (double)a.y, acc1);
-        acc2 = fma((double)a.z, (double)a.z, acc2); acc3 = fma((double)a.w, (double)a.w, acc3);
-        acc0 = fma((double)b.x, (double)b.x, acc0); acc1 = fma((double)b.y, (double)b.y, acc1);
-        acc2 = fma((double)b.z, (double)b.z, acc2); acc3 = fma((double)b.w, (double)b.w, acc3);
-        acc0 = fma((double)e.x, (double)e.x, acc0); acc1 = fma((double)e.y, (double)e.y, acc1);
-        acc2 = fma((double)e.z, (double)e.z, acc2); acc3 = fma((double)e.w, (double)e.w, acc3);
-        acc0 = fma((double)f.x, (double)f.x, acc0); acc1 = fma((double)f.y, (double)f.y, acc1);
-        acc2 = fma((double)f.z, (double)f.z, acc2); acc3 = fma((double)f.w, (double)f.w, acc3);
-    }
-    for (; j < nvec; j += kBlock) {
-        const f32x4 a = load_nt(v4 + 4 * (j));
-        acc0 = fma((double)a.x, (double)a.x, acc0); acc1 = fma((double)a.y, (double)a.y, acc1);
-        acc2 = fma((double)a.z, (double)a.z, acc2); acc3 = fma((double)a.w, (double)a.w, acc3);
-    }
-    // at most three trailing coordinates (only in the last chunk when d % 4 != 0)
-    const int64_t tail = begin + (nvec << 2) + threadIdx.x;
-    if (tail < end) {
-        const double x = row[tail];
-        acc0 = fma(x, x, acc0);
-    }
-    double s = wave_sum((acc0 + acc1) + (acc2 + acc3));
-
     __shared__ double wave_part[kBlock / 64];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    if (lane == 0)
-        wave_part[wave] = s;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const double total = (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
-        part[static_cast<int64_t>(m) * nchunks + c] = total;
+    const int32_t c = blockIdx.x;
+    const int64_t begin = static_cast<int64_t>(c) * chunk;
+    const int64_t end = begin + chunk < d ? begin + chunk : d;
+    const int64_t nvec = (end - begin) >> 2;
+    // grid.y covers the rows (more rows than grid.y: the blocks take them in turn)
+    for (int32_t m = blockIdx.y; m < M; m += gridDim.y) {
+        const float* row = g + static_cast<int64_t>(m) * ldg;
+        const float* v4 = row + begin;
+        double acc0 = 0.0, acc1 = 0.0, acc2 = 0.0, acc3 = 0.0;
+        int64_t j = threadIdx.x;
+        for (; j + 3 * kBlock < nvec; j += 4 * kBlock) {
+            const f32x4 a = load_nt(v4 + 4 * j);
+            const f32x4 b = load_nt(v4 + 4 * (j + kBlock));
+            const f32x4 e = load_nt(v4 + 4 * (j + 2 * kBlock));
+            const f32x4 f = load_nt(v4 + 4 * (j + 3 * kBlock));
+            acc0 = fma((double)a.x, (double)a.x, acc0); acc1 = fma((double)a.y, (double)a.y, acc1);
+            acc2 = fma((double)a.z, (double)a.z, acc2); acc3 = fma((double)a.w, (double)a.w, acc3);
+            acc0 = fma((double)b.x, (double)b.x, acc0); acc1 = fma((double)b.y, (double)b.y, acc1);
+            acc2 = fma((double)b.z, (double)b.z, acc2); acc3 = fma((double)b.w, (double)b.w, acc3);
+            acc0 = fma((double)e.x, (double)e.x, acc0); acc1 = fma((double)e.y, (double)e.y, acc1);
+            acc2 = fma((double)e.z, (double)e.z, acc2); acc3 = fma((double)e.w, (double)e.w, acc3);
+            acc0 = fma((double)f.x, (double)f.x, acc0); acc1 = fma((double)f.y, (double)f.y, acc1);
+            acc2 = fma((double)f.z, (double)f.z, acc2); acc3 = fma((double)f.w, (double)f.w, acc3);
+        }
+        for (; j < nvec; j += kBlock) {
+            const f32x4 a = load_nt(v4 + 4 * j);
+            acc0 = fma((double)a.x, (double)a.x, acc0); acc1 = fma((double)a.y, (double)a.y, acc1);
+            acc2 = fma((double)a.z, (double)a.z, acc2); acc3 = fma((double)a.w, (double)a.w, acc3);
+        }
+        // at most three trailing coordinates (only in the last chunk when d % 4 != 0)
+        const int64_t tail = begin + (nvec << 2) + threadIdx.x;
+        if (tail < end) {
+            const double x = row[tail];
+            acc0 = fma(x, x, acc0);
+        }
+        const double s = wave_sum((acc0 + acc1) + (acc2 + acc3));
+        if (lane == 0)
+            wave_part[wave] = s;
+        __syncthreads();
+        if (threadIdx.x == 0)
+            part[static_cast<int64_t>(m) * nchunks + c] = (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
+        __syncthreads();  // wave_part is reused for the next row
     }
 }
 
@@ -301,6 +300,7 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
     const float s0 = S.s[0];
     const uint32_t kmax = static_cast<uint32_t>(S.K - 1);
 
+    // 2-D grid: tile blocks in x, worker rows in y
     const int32_t r = blockIdx.y;
     const uint32_t worker = static_cast<uint32_t>(worker0) + static_cast<uint32_t>(r);
     const float* row = g + static_cast<int64_t>(r) * ldg;
@@ -409,61 +409,61 @@ constexpr int64_t kSumTile = 4096;
 __global__ __launch_bounds__(kBlock) void k_sum(const int8_t* __restrict__ codes, int64_t d, int32_t rows,
                                                 int64_t ldc, int32_t accumulate, int32_t* __restrict__ sum)
 {
-  for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
-       tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
-    const int64_t base = tile0 + 4 * threadIdx.x;
-    if (tile0 + kSumTile <= d) {
-        int32_t acc[16];
-        if (accumulate) {
+    for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
+         tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
+        const int64_t base = tile0 + 4 * threadIdx.x;
+        if (tile0 + kSumTile <= d) {
+            int32_t acc[16];
+            if (accumulate) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int4 a = *reinterpret_cast<const int4*>(sum + base + 1024 * c);
-                acc[4 * c] = a.x; acc[4 * c + 1] = a.y; acc[4 * c + 2] = a.z; acc[4 * c + 3] = a.w;
+                for (int c = 0; c < 4; ++c) {
+                    const int4 a = *reinterpret_cast<const int4*>(sum + base + 1024 * c);
+                    acc[4 * c] = a.x; acc[4 * c + 1] = a.y; acc[4 * c + 2] = a.z; acc[4 * c + 3] = a.w;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    acc[j] = 0;
             }
-        } else {
+            int32_t r = 0;
+            for (; r + 4 <= rows; r += 4) {
+                uint32_t w[4][4];
 #pragma unroll
-            for (int j = 0; j < 16; ++j)
-                acc[j] = 0;
-        }
-        int32_t r = 0;
-        for (; r + 4 <= rows; r += 4) {
-            uint32_t w[4][4];
+                for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+                    for (int c = 0; c < 4; ++c)
+                        w[u][c] = load_nt_u32(codes + static_cast<int64_t>(r + u) * ldc + base + 1024 * c);
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    w[u][c] = load_nt_u32(codes + static_cast<int64_t>(r + u) * ldc + base + 1024 * c);
+                for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+                    for (int c = 0; c < 4; ++c)
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
+                        for (int j = 0; j < 4; ++j)
+                            acc[4 * c + j] += sbyte(w[u][c], j);
+            }
+            for (; r < rows; ++r) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t w = load_nt_u32(codes + static_cast<int64_t>(r) * ldc + base + 1024 * c);
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        acc[4 * c + j] += sbyte(w[u][c], j);
-        }
-        for (; r < rows; ++r) {
+                        acc[4 * c + j] += sbyte(w, j);
+                }
+            }
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t w = load_nt_u32(codes + static_cast<int64_t>(r) * ldc + base + 1024 * c);
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[4 * c + j] += sbyte(w, j);
+            for (int c = 0; c < 4; ++c)
+                *reinterpret_cast<int4*>(sum + base + 1024 * c) =
+                    make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
+        } else {
+            // the last, partial tile: one coordinate at a time
+            for (int64_t i = tile0 + threadIdx.x; i < d; i += kBlock) {
+                int32_t acc = accumulate ? sum[i] : 0;
+                for (int32_t r = 0; r < rows; ++r)
+                    acc += codes[static_cast<int64_t>(r) * ldc + i];
+                sum[i] = acc;
             }
         }
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            *reinterpret_cast<int4*>(sum + base + 1024 * c) =
-                make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
-    } else {
-        // the last, partial tile: one coordinate at a time
-        for (int64_t i = tile0 + threadIdx.x; i < d; i += kBlock) {
-            int32_t acc = accumulate ? sum[i] : 0;
-            for (int32_t r = 0; r < rows; ++r)
-                acc += codes[static_cast<int64_t>(r) * ldc + i];
-            sum[i] = acc;
-        }
     }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -535,9 +535,10 @@ static int32_t quantise_tiles_per_wave(int32_t K)
 // streaming kernels run fastest as one pass with no grid-stride reuse).  The
 // dispatch packet counts work-items in 32 bits, so the grid is capped at 2^22
 // blocks; every kernel strides over whatever the grid does not cover.
+constexpr int64_t kMaxBlocks = int64_t(1) << 22;
+
 static unsigned one_shot(int64_t units, int64_t per_block)
 {
-    const int64_t kMaxBlocks = int64_t(1) << 22;
     int64_t blocks = (units + per_block - 1) / per_block;
     blocks = blocks < 1 ? 1 : (blocks > kMaxBlocks ? kMaxBlocks : blocks);
     return static_cast<unsigned>(blocks);
@@ -556,8 +557,11 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
 {
     const NormPlan plan = norm_plan(d);
     if (plan.nchunks > 0) {
-        dim3 grid(static_cast<unsigned>(plan.nchunks), static_cast<unsigned>(M));
-        hipLaunchKernelGGL(k_sumsq, grid, dim3(kBlock), 0, stream, g, d, ldg, plan.chunk, plan.nchunks, part);
+        // rows beyond kMaxBlocks / nchunks are taken in turn by the same blocks
+        int64_t gy = kMaxBlocks / plan.nchunks;
+        gy = gy > M ? M : gy;
+        dim3 grid(static_cast<unsigned>(plan.nchunks), static_cast<unsigned>(gy));
+        hipLaunchKernelGGL(k_sumsq, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk, plan.nchunks, part);
     }
     hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, stream, part, plan.nchunks, M, w);
     if (S.K > 1 && d > 0) {
@@ -573,18 +577,22 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
 {
     if (d == 0)
         return hipSuccess;
-    // `tpw` consecutive 512-coordinate tiles per wave, four waves per block
-    const int32_t tpw = quantise_tiles_per_wave(S.K);
-    const unsigned gx = one_shot(d >> 9, (kBlock / 64) * tpw);
     const uint32_t key0 = static_cast<uint32_t>(seed);
     const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
-    dim3 grid(gx, static_cast<unsigned>(rows));
+    // `tpw` consecutive 512-coordinate tiles per wave, four waves per block
+    const int32_t tpw = quantise_tiles_per_wave(S.K);
+    unsigned tile_blocks = one_shot(d >> 9, (kBlock / 64) * tpw);
+    // keep rows x tile blocks within kMaxBlocks; the waves stride over the rest
+    const int64_t per_row = kMaxBlocks / rows / 8 * 8;
+    if (static_cast<int64_t>(tile_blocks) > per_row)
+        tile_blocks = static_cast<unsigned>(per_row < 8 ? 8 : per_row);
+    dim3 grid(tile_blocks, static_cast<unsigned>(rows));
     if (S.K > 1)
-        hipLaunchKernelGGL(k_quantise<true>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx,
-                           key0, key1, codes, ldc, tpw);
+        hipLaunchKernelGGL(k_quantise<true>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx, key0,
+                           key1, codes, ldc, tpw);
     else
-        hipLaunchKernelGGL(k_quantise<false>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S,
-                           idx, key0, key1, codes, ldc, tpw);
+        hipLaunchKernelGGL(k_quantise<false>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx, key0,
+                           key1, codes, ldc, tpw);
     return hipGetLastError();
 }
 
