@@ -106,6 +106,51 @@ def cpu_baseline(g, cfg, budget_s: float):
             "sample": sample, "seconds": round(dt, 2)}, ref, dn
 
 
+def bench_randk(args, g, cfg) -> int:
+    """GlobalRandK step (Sec. 3.3-3.4): select -> gather -> Algorithm 1/2 on
+    the k sampled coordinates -> scatter into the d-vector."""
+    import torch
+
+    from paper_2109_12497_amd.step import RandKStep
+
+    d, M, scales, seed, k = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"], cfg["randk"]
+    st = RandKStep(d, M, k, scales, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        st.run(g, seed)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st.run(g, seed)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stages = ["select", "gather", "aggregate", "scatter"]
+    ev = {s: [] for s in stages}
+
+    def mark():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    for _ in range(args.steps):
+        a = mark(); st.select(seed); b = mark(); st.gather(g); c = mark()
+        st.inner.run(st.sub, seed); e = mark(); st.scatter(); f = mark()
+        ev["select"].append((a, b)); ev["gather"].append((b, c)); ev["aggregate"].append((c, e))
+        ev["scatter"].append((e, f))
+    torch.cuda.synchronize()
+    stage_ms = {s: round(sum(x.elapsed_time(y) for x, y in ev[s]) / args.steps, 4) for s in stages}
+    print(json.dumps({
+        "metric": METRIC, "value": round(M * d * args.steps / elapsed / 1e9, 3), "unit": "G elements/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed, "randk": k,
+                   "quantizer": "multi" if len(scales) > 1 else "single",
+                   "parallelism": "one GPU, M workers simulated"},
+        "stage_ms": stage_ms, "roofline": None, "cpu_baseline": None}))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,8 +185,10 @@ def main() -> int:
     d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
     streamed = bool(cfg.get("streamed", False))
     K = len(scales)
-    step = Step(d, M, scales, device="cuda", streamed=streamed)
     stream = torch.cuda.current_stream()
+    if cfg.get("randk"):
+        return bench_randk(args, g, cfg)
+    step = Step(d, M, scales, device="cuda", streamed=streamed)
     torch.cuda.synchronize()
 
     for _ in range(args.warmup):

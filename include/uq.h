@@ -146,6 +146,49 @@ int uq_sum_codes(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int3
 int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w,
                   const float* scales, int32_t K, const uint8_t* idx, float* out, void* stream);
 
+/* ------------------------------------------------------------------------
+ * GlobalRandK sparsification (Sec. 3.3 GlobalRandKMaxNorm, Sec. 3.4
+ * GlobalRandKMaxNormMultiScale): K coordinates chosen uniformly at random,
+ * the same for every worker, are quantised as a K-dimensional problem with
+ * the calls above and written back into the d-vector (0 elsewhere; there is
+ * no d/K rescaling).  A step is: uq_randk_select -> uq_gather ->
+ * uq_shared_scale / uq_quantize_* / uq_sum_codes / uq_dequantize on the
+ * [M][K] sub-vectors -> uq_scatter.  In these four calls K is the number of
+ * sampled coordinates (the paper's K), not a number of scales.
+ * ------------------------------------------------------------------------ */
+
+/* Workspace bytes uq_randk_select needs (a fixed size, about 96 KiB). */
+size_t uq_randk_workspace_bytes(int64_t d, int64_t K);
+
+/*
+ * The uniformly random K-subset: coordinate i has the 64-bit key
+ * (hi, lo) = (word i%4 of Philox4x32-10 block (i/4, 0, 2),
+ *             word i%4 of block (i/4, 0, 3)) under key `seed`, and the K
+ * coordinates with the smallest (hi, lo, i) are written to sel[0..K) in
+ * increasing order.
+ *   d      1 <= d < 2^32
+ *   K      1 <= K <= d
+ *   sel    [K] uint32 (written), 16-byte aligned
+ *   ws     device workspace of uq_randk_workspace_bytes(d, K) bytes
+ * The boundary search keeps at most 4096 keys that share the K-th key's top
+ * 24 bits (about d / 2^24 are expected); more would make the result wrong,
+ * which pseudo-random keys do not produce for any d < 2^32.
+ */
+int uq_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, size_t ws_bytes,
+                    void* stream);
+
+/*
+ * sub[m][j] = g[m][sel[j]] for the M rows and j < K (an index >= d reads as 0).
+ *   g      [M][ldg] fp32, ldg >= d      sub   [M][lds] fp32, lds >= K, lds % 4 == 0
+ */
+int uq_gather(const float* g, int64_t d, int32_t M, int64_t ldg, const uint32_t* sel, int64_t K,
+              float* sub, int64_t lds, void* stream);
+
+/*
+ * out[0..d) = 0, then out[sel[j]] = vals[j] for j < K (indices >= d skipped).
+ */
+int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, int64_t d, void* stream);
+
 /* Static text for a status code. */
 const char* uq_strerror(int status);
 

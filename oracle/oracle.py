@@ -62,6 +62,10 @@ def lib():
         L.orc_sum_codes.restype = None
         L.orc_dequantize.argtypes = [P, i64, i32, f32, P, i32, P, P]
         L.orc_dequantize.restype = None
+        L.orc_randk_keys.argtypes = [u64, i64, i64, P, P]
+        L.orc_randk_keys.restype = None
+        L.orc_randk_select.argtypes = [i64, i64, u64, P, P]
+        L.orc_randk_select.restype = None
         _lib = L
     return _lib
 
@@ -193,3 +197,40 @@ def pipeline(g: np.ndarray, scales, seed: int, d: int | None = None, W=None,
     out = dequantize(sums, M, W, s, idx)
     return {"W": W, "W_oracle": W_own, "sumsq": S, "idx": idx, "codes": codes,
             "sum": sums, "out": out}
+
+
+# ---------------------------------------------------------------------------
+# GlobalRandK (Sec. 3.3-3.4)
+# ---------------------------------------------------------------------------
+
+def randk_keys(seed: int, i0: int, n: int):
+    """(hi, lo) 32-bit selection keys of coordinates i0 .. i0+n-1."""
+    hi = np.zeros(n, dtype=np.uint32)
+    lo = np.zeros(n, dtype=np.uint32)
+    lib().orc_randk_keys(seed, i0, n, _ptr(hi), _ptr(lo))
+    return hi, lo
+
+
+def randk_select(d: int, K: int, seed: int) -> np.ndarray:
+    """The K coordinates with the smallest (key, index), ascending (uint32)."""
+    assert 0 < K <= d < 2 ** 32
+    out = np.zeros(K, dtype=np.uint32)
+    scratch = np.zeros(d * 12, dtype=np.uint8)
+    lib().orc_randk_select(d, K, seed, _ptr(out), _ptr(scratch))
+    return out
+
+
+def randk_pipeline(g: np.ndarray, K: int, scales, seed: int, d: int | None = None, W=None,
+                   worker0: int = 0) -> dict:
+    """GlobalRandK step: select K coordinates, run Algorithm 1/2 on the
+    gathered [M, K] sub-vectors, write the reconstruction back (0 elsewhere)."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    M, ldg = g.shape
+    d = ldg if d is None else d
+    sel = randk_select(d, K, seed)
+    sub = np.ascontiguousarray(g[:, sel.astype(np.int64)])
+    r = pipeline(sub, scales, seed, d=K, W=W, worker0=worker0)
+    full = np.zeros(d, dtype=np.float32)
+    full[sel.astype(np.int64)] = r["out"]
+    r.update(sel=sel, sub=sub, full=full)
+    return r

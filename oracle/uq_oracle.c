@@ -38,11 +38,23 @@
  *     all-zero output (scale index K-1 everywhere);
  *   - the all-reduce of the codes is an exact int32 sum; 1/M is folded into
  *     the reconstruction factor fl32(W / (M * s_k)).
+ *
+ * GlobalRandK (Sec. 3.3-3.4): the K coordinates are a uniformly random
+ * K-subset shared by all workers: coordinate i gets the 64-bit key
+ * (hi, lo) = (word i%4 of Philox block (i/4, 0, purpose 2),
+ *             word i%4 of Philox block (i/4, 0, purpose 3))
+ * and the K coordinates with the smallest (key, i) are taken, listed in
+ * increasing order.  The chosen coordinates of every worker are then
+ * quantised as a K-dimensional problem (its own max norm, the same seed);
+ * the reconstruction is written back to those coordinates and every other
+ * coordinate of the averaged gradient is 0 (no d/K rescaling: the paper
+ * applies the quantiser to the sampled coordinates and says nothing more).
  */
 #include <float.h>
 #include <math.h>
 #include <stdint.h>
 #include <stddef.h>
+#include <stdlib.h>
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x32-10, from the published round function: two 32x32->64 products  */
@@ -270,4 +282,62 @@ void orc_dequantize(const int32_t* sum, int64_t n, int32_t M, float W, const flo
         }
         out[i] = (float)sum[i] * deq[k];
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* GlobalRandK selection (Sec. 3.3-3.4): keys, then the K smallest.          */
+/* ------------------------------------------------------------------------ */
+
+/* The 64-bit selection keys of coordinates i0 .. i0+n-1 as (hi, lo) words. */
+void orc_randk_keys(uint64_t seed, int64_t i0, int64_t n, uint32_t* hi, uint32_t* lo)
+{
+    uint32_t key[2] = { (uint32_t)seed, (uint32_t)(seed >> 32) };
+    for (int64_t j = 0; j < n; ++j) {
+        uint64_t i = (uint64_t)(i0 + j);
+        uint64_t block = i / 4;
+        unsigned word = (unsigned)(i % 4);
+        uint32_t ctr[4] = { (uint32_t)block, (uint32_t)(block >> 32), 0u, 2u };
+        uint32_t out[4];
+        orc_philox4x32_10(ctr, key, out);
+        hi[j] = out[word];
+        ctr[3] = 3u;
+        orc_philox4x32_10(ctr, key, out);
+        lo[j] = out[word];
+    }
+}
+
+typedef struct { uint32_t hi, lo; uint32_t idx; } orc_key_t;
+
+static int orc_key_cmp(const void* pa, const void* pb)
+{
+    const orc_key_t* a = (const orc_key_t*)pa;
+    const orc_key_t* b = (const orc_key_t*)pb;
+    if (a->hi != b->hi) return a->hi < b->hi ? -1 : 1;
+    if (a->lo != b->lo) return a->lo < b->lo ? -1 : 1;
+    if (a->idx != b->idx) return a->idx < b->idx ? -1 : 1;
+    return 0;
+}
+
+static int orc_u32_cmp(const void* pa, const void* pb)
+{
+    uint32_t a = *(const uint32_t*)pa, b = *(const uint32_t*)pb;
+    return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+/* The K coordinates of [0, d) with the smallest (key, index), ascending.
+ * scratch holds d entries of 12 bytes (orc_key_t). */
+void orc_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* out, void* scratch)
+{
+    orc_key_t* keys = (orc_key_t*)scratch;
+    uint32_t hi, lo;
+    for (int64_t i = 0; i < d; ++i) {
+        orc_randk_keys(seed, i, 1, &hi, &lo);
+        keys[i].hi = hi;
+        keys[i].lo = lo;
+        keys[i].idx = (uint32_t)i;
+    }
+    qsort(keys, (size_t)d, sizeof(orc_key_t), orc_key_cmp);
+    for (int64_t j = 0; j < K; ++j)
+        out[j] = keys[j].idx;
+    qsort(out, (size_t)K, sizeof(uint32_t), orc_u32_cmp);
 }

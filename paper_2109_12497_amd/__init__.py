@@ -57,12 +57,17 @@ def _load() -> ctypes.CDLL:
     L.uq_quantize_multi.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, P, i64, P]
     L.uq_sum_codes.argtypes = [P, i64, i32, i64, i32, P, P]
     L.uq_dequantize.argtypes = [P, i64, i32, P, P, i32, P, P, P]
+    L.uq_randk_workspace_bytes.argtypes = [i64, i64]
+    L.uq_randk_workspace_bytes.restype = sz
+    L.uq_randk_select.argtypes = [i64, i64, u64, P, P, sz, P]
+    L.uq_gather.argtypes = [P, i64, i32, i64, P, i64, P, i64, P]
+    L.uq_scatter.argtypes = [P, P, i64, P, i64, P]
     L.uq_strerror.argtypes = [ctypes.c_int]
     L.uq_strerror.restype = ctypes.c_char_p
     L.uq_last_error.argtypes = []
     L.uq_last_error.restype = ctypes.c_char_p
     for name in ("uq_shared_scale", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
-                 "uq_dequantize"):
+                 "uq_dequantize", "uq_randk_select", "uq_gather", "uq_scatter"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -134,6 +139,22 @@ def uq_sum_codes(codes, d, rows, ldc, accumulate, sum, stream=None) -> None:
 def uq_dequantize(sum, d, M, w, scales, K, idx, out, stream=None) -> None:
     hs = _HostScales(scales)
     _check(lib.uq_dequantize(_ptr(sum), d, M, _ptr(w), hs.ptr, K, _ptr(idx), _ptr(out), _stream(stream)))
+
+
+def uq_randk_workspace_bytes(d: int, K: int) -> int:
+    return int(lib.uq_randk_workspace_bytes(d, K))
+
+
+def uq_randk_select(d, K, seed, sel, ws, ws_bytes, stream=None) -> None:
+    _check(lib.uq_randk_select(d, K, seed, _ptr(sel), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def uq_gather(g, d, M, ldg, sel, K, sub, lds, stream=None) -> None:
+    _check(lib.uq_gather(_ptr(g), d, M, ldg, _ptr(sel), K, _ptr(sub), lds, _stream(stream)))
+
+
+def uq_scatter(vals, sel, K, out, d, stream=None) -> None:
+    _check(lib.uq_scatter(_ptr(vals), _ptr(sel), K, _ptr(out), d, _stream(stream)))
 
 
 def uq_strerror(status: int) -> str:

@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("uq_kernels.hip", "uq_abi.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("uq_kernels.hip", "uq_randk.hip", "uq_abi.hip")]
 LIB_PATH = os.path.join(HERE, "libuq.so")
 
 HIPCC_FLAGS = [

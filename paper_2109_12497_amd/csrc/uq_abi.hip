@@ -273,6 +273,54 @@ int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w, cons
     return launched(uq::launch_dequant(sum, d, M, w, S, idx, out, static_cast<hipStream_t>(stream)));
 }
 
+size_t uq_randk_workspace_bytes(int64_t d, int64_t K)
+{
+    (void)d;
+    (void)K;
+    return uq::randk_workspace_bytes();
+}
+
+int uq_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, size_t ws_bytes, void* stream)
+{
+    if (d < 1 || d >= (int64_t(1) << 32))
+        return fail(UQ_EINVAL, "d = %lld is outside [1, 2^32)", (long long)d);
+    if (K < 1 || K > d)
+        return fail(UQ_ERANGE, "K = %lld is outside [1, d]", (long long)K);
+    UQ_TRY(check_vec(sel, K, "sel"));
+    if (ws == nullptr)
+        return fail(UQ_EINVAL, "ws is NULL");
+    if (!aligned(ws, 16))
+        return fail(UQ_EALIGN, "ws is not 16-byte aligned");
+    if (ws_bytes < uq_randk_workspace_bytes(d, K))
+        return fail(UQ_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", ws_bytes,
+                    uq_randk_workspace_bytes(d, K));
+    return launched(uq::launch_randk_select(d, K, seed, sel, ws, static_cast<hipStream_t>(stream)));
+}
+
+int uq_gather(const float* g, int64_t d, int32_t M, int64_t ldg, const uint32_t* sel, int64_t K, float* sub,
+              int64_t lds, void* stream)
+{
+    UQ_TRY(check_dims(d, M, "M"));
+    if (K < 1 || K > d)
+        return fail(UQ_ERANGE, "K = %lld is outside [1, d]", (long long)K);
+    UQ_TRY(check_rows(g, d, M, ldg, 1, "g"));
+    UQ_TRY(check_rows(sub, K, M, lds, 4, "sub"));
+    UQ_TRY(check_vec(sel, K, "sel"));
+    return launched(uq::launch_gather(g, d, M, ldg, sel, K, sub, lds, static_cast<hipStream_t>(stream)));
+}
+
+int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, int64_t d, void* stream)
+{
+    if (d < 1 || d > kMaxElems)
+        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
+    if (K < 1 || K > d)
+        return fail(UQ_ERANGE, "K = %lld is outside [1, d]", (long long)K);
+    UQ_TRY(check_vec(vals, K, "vals"));
+    UQ_TRY(check_vec(sel, K, "sel"));
+    UQ_TRY(check_vec(out, d, "out"));
+    return launched(uq::launch_scatter(vals, sel, K, out, d, static_cast<hipStream_t>(stream)));
+}
+
 const char* uq_strerror(int status)
 {
     switch (status) {

@@ -403,66 +403,74 @@ __device__ __forceinline__ int32_t sbyte(uint32_t w, int j)
 
 // Block tiles of 4096 coordinates: thread t sums quads t, t+256, t+512 and
 // t+768 of the tile, so every row load and every store of a wave covers
-// 256 or 1024 contiguous bytes; rows are read four at a time.
+// 256 or 1024 contiguous bytes; rows are read four at a time.  Quads past d
+// (in the last tile) are skipped and the last d % 4 coordinates are summed
+// one by one.
 constexpr int64_t kSumTile = 4096;
+
+__device__ __forceinline__ void sum_rows(const int8_t* __restrict__ codes, int32_t rows, int64_t ldc,
+                                         int64_t base, const bool live[4], int32_t acc[16])
+{
+    int32_t r = 0;
+    for (; r + 4 <= rows; r += 4) {
+        uint32_t w[4][4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                w[u][c] = live[c] ? load_nt_u32(codes + static_cast<int64_t>(r + u) * ldc + base + 1024 * c) : 0u;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[4 * c + j] += sbyte(w[u][c], j);
+    }
+    for (; r < rows; ++r) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const uint32_t w = live[c] ? load_nt_u32(codes + static_cast<int64_t>(r) * ldc + base + 1024 * c) : 0u;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                acc[4 * c + j] += sbyte(w, j);
+        }
+    }
+}
 
 __global__ __launch_bounds__(kBlock) void k_sum(const int8_t* __restrict__ codes, int64_t d, int32_t rows,
                                                 int64_t ldc, int32_t accumulate, int32_t* __restrict__ sum)
 {
+    const int64_t dq = d & ~int64_t(3);  // coordinates covered by whole quads
     for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
          tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
         const int64_t base = tile0 + 4 * threadIdx.x;
-        if (tile0 + kSumTile <= d) {
-            int32_t acc[16];
-            if (accumulate) {
+        bool live[4];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int4 a = *reinterpret_cast<const int4*>(sum + base + 1024 * c);
-                    acc[4 * c] = a.x; acc[4 * c + 1] = a.y; acc[4 * c + 2] = a.z; acc[4 * c + 3] = a.w;
-                }
-            } else {
+        for (int c = 0; c < 4; ++c)
+            live[c] = base + 1024 * c + 4 <= dq;
+        int32_t acc[16];
 #pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    acc[j] = 0;
-            }
-            int32_t r = 0;
-            for (; r + 4 <= rows; r += 4) {
-                uint32_t w[4][4];
+        for (int c = 0; c < 4; ++c) {
+            int4 a = make_int4(0, 0, 0, 0);
+            if (accumulate && live[c])
+                a = *reinterpret_cast<const int4*>(sum + base + 1024 * c);
+            acc[4 * c] = a.x; acc[4 * c + 1] = a.y; acc[4 * c + 2] = a.z; acc[4 * c + 3] = a.w;
+        }
+        sum_rows(codes, rows, ldc, base, live, acc);
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-#pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        w[u][c] = load_nt_u32(codes + static_cast<int64_t>(r + u) * ldc + base + 1024 * c);
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-#pragma unroll
-                    for (int c = 0; c < 4; ++c)
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            acc[4 * c + j] += sbyte(w[u][c], j);
-            }
-            for (; r < rows; ++r) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const uint32_t w = load_nt_u32(codes + static_cast<int64_t>(r) * ldc + base + 1024 * c);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[4 * c + j] += sbyte(w, j);
-                }
-            }
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < 4; ++c)
+            if (live[c])
                 *reinterpret_cast<int4*>(sum + base + 1024 * c) =
                     make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
-        } else {
-            // the last, partial tile: one coordinate at a time
-            for (int64_t i = tile0 + threadIdx.x; i < d; i += kBlock) {
-                int32_t acc = accumulate ? sum[i] : 0;
-                for (int32_t r = 0; r < rows; ++r)
-                    acc += codes[static_cast<int64_t>(r) * ldc + i];
-                sum[i] = acc;
-            }
-        }
+    }
+    // the last d % 4 coordinates
+    const int64_t t = dq + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (blockIdx.x == 0 && t < d) {
+        int32_t acc = accumulate ? sum[t] : 0;
+        for (int32_t r = 0; r < rows; ++r)
+            acc += codes[static_cast<int64_t>(r) * ldc + t];
+        sum[t] = acc;
     }
 }
 

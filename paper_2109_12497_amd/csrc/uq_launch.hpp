@@ -39,6 +39,16 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
                            int8_t* codes, int64_t ldc, hipStream_t stream);
 hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,
                       int32_t* sum, hipStream_t stream);
+// GlobalRandK: at most kRandkCandidates keys sharing the threshold's 24-bit
+// prefix are kept (expected d / 2^24; d < 2^32).
+constexpr int kRandkCandidates = 4096;
+
+size_t randk_workspace_bytes();
+hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, hipStream_t stream);
+hipError_t launch_gather(const float* g, int64_t d, int32_t M, int64_t ldg, const uint32_t* sel, int64_t K,
+                         float* sub, int64_t lds, hipStream_t stream);
+hipError_t launch_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, int64_t d,
+                          hipStream_t stream);
 hipError_t launch_dequant(const int32_t* sum, int64_t d, int32_t M, const float* w, const ScaleSet& S,
                           const uint8_t* idx, float* out, hipStream_t stream);
 

@@ -9,8 +9,8 @@ from __future__ import annotations
 
 import torch
 
-from . import (uq_dequantize, uq_quantize_multi, uq_quantize_single, uq_shared_scale, uq_sum_codes,
-               uq_workspace_bytes)
+from . import (uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_single, uq_randk_select,
+               uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes, uq_workspace_bytes)
 
 
 def round_up(x: int, m: int) -> int:
@@ -80,4 +80,37 @@ class Step:
             self.quantize(g, seed, stream=stream)
             self.sum_codes(stream=stream)
         self.dequantize(stream)
+        return self.out[:self.d]
+
+
+class RandKStep:
+    """GlobalRandK step (Sec. 3.3-3.4): select k coordinates shared by all
+    workers, gather them into [M, k] sub-vectors, run Algorithm 1/2 on those
+    with `Step`, and scatter the reconstruction into the d-vector (0 elsewhere)."""
+
+    def __init__(self, d: int, M: int, k: int, scales, device="cuda"):
+        self.d, self.M, self.k = d, M, k
+        self.inner = Step(k, M, scales, device=device)
+        dev = self.inner.device
+        self.sel = torch.zeros(round_up(k, 64), dtype=torch.int32, device=dev)  # uint32 indices
+        self.sub = torch.zeros((M, round_up(k, 64)), dtype=torch.float32, device=dev)
+        self.rk_ws_bytes = uq_randk_workspace_bytes(d, k)
+        self.rk_ws = torch.zeros(self.rk_ws_bytes // 8, dtype=torch.float64, device=dev)
+        self.out = torch.zeros(round_up(max(d, 1), 64), dtype=torch.float32, device=dev)
+
+    def select(self, seed: int, stream=None):
+        uq_randk_select(self.d, self.k, seed, self.sel, self.rk_ws, self.rk_ws_bytes, stream)
+
+    def gather(self, g, stream=None):
+        uq_gather(g, self.d, self.M, g.stride(0), self.sel, self.k, self.sub, self.sub.stride(0), stream)
+
+    def scatter(self, stream=None):
+        uq_scatter(self.inner.out, self.sel, self.k, self.out, self.d, stream)
+
+    def run(self, g, seed: int, stream=None):
+        assert g.dtype == torch.float32 and g.shape[0] == self.M and g.stride(1) == 1
+        self.select(seed, stream)
+        self.gather(g, stream)
+        self.inner.run(self.sub, seed, stream)
+        self.scatter(stream)
         return self.out[:self.d]

@@ -141,3 +141,45 @@ def test_binding_raises_with_detail():
     with pytest.raises(uq.UQError) as e:
         uq.uq_quantize_single(A, 100, 2, 128, 0, A, 200, 1, A, 128, stream=0)
     assert e.value.status == uq.UQ_ERANGE and "s = 200" in str(e.value)
+
+
+# GlobalRandK entry points -------------------------------------------------
+
+def status_sel(d=1000, K=10, sel=A, ws=A, ws_bytes=1 << 20):
+    return L.uq_randk_select(d, K, 7, sel, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(d=0), "inval"), (dict(d=2 ** 32), "inval"), (dict(K=0), "range"), (dict(K=1001), "range"),
+    (dict(sel=None), "inval"), (dict(sel=A + 4), "align"),
+    (dict(ws=None), "inval"), (dict(ws=A + 8), "align"), (dict(ws_bytes=64), "ws"),
+])
+def test_randk_select_rejects(kw, want):
+    assert status_sel(**kw) == E[want]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(g=None), "inval"), (dict(M=0), "inval"), (dict(K=0), "range"), (dict(K=101), "range"),
+    (dict(ldg=50), "inval"), (dict(lds=10), "inval"), (dict(lds=30), "align"), (dict(sel=None), "inval"),
+    (dict(sub=A + 4), "align"),
+])
+def test_gather_rejects(kw, want):
+    args = dict(g=A, d=100, M=2, ldg=128, sel=A, K=20, sub=A, lds=32)
+    args.update(kw)
+    assert L.uq_gather(args["g"], args["d"], args["M"], args["ldg"], args["sel"], args["K"], args["sub"],
+                       args["lds"], None) == E[want]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(vals=None), "inval"), (dict(sel=None), "inval"), (dict(out=None), "inval"), (dict(K=0), "range"),
+    (dict(K=101), "range"), (dict(d=0), "inval"), (dict(out=A + 4), "align"),
+])
+def test_scatter_rejects(kw, want):
+    args = dict(vals=A, sel=A, K=20, out=A, d=100)
+    args.update(kw)
+    assert L.uq_scatter(args["vals"], args["sel"], args["K"], args["out"], args["d"], None) == E[want]
+
+
+def test_randk_workspace_fixed_and_aligned():
+    b = uq.uq_randk_workspace_bytes(10 ** 6, 10_000)
+    assert b % 256 == 0 and 32 * 1024 < b < 1024 * 1024

@@ -1,0 +1,96 @@
+"""GPU parity for GlobalRandK (Sec. 3.3-3.4): the selected index list
+bit-exact against the oracle, gather/scatter exact, and the whole step
+(selection, Algorithm 1/2 on the sampled coordinates, scatter) bit-exact."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import synth  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+from paper_2109_12497_amd.step import RandKStep  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def gpu_select(d, K, seed):
+    st = RandKStep(d, 1, K, [127.0], device=DEV)
+    st.select(seed)
+    torch.cuda.synchronize()
+    return st.sel[:K].cpu().numpy().view(np.uint32)
+
+
+@pytest.mark.parametrize("d,K,seed", [
+    (1, 1, 0), (2, 1, 5), (5, 5, 1), (7, 3, 2), (100, 99, 3), (1000, 1, 4), (4097, 4096, 5),
+    (65_539, 10_000, 6), (1 << 20, 32_768, 7), (1 << 20, 10_000, (1 << 63) + 12345), (300_000, 250_000, 10),
+    (3_000_001, 10_000, 8), (11_173_962, 10_000, 9),
+])
+def test_selection_matches_oracle(d, K, seed):
+    got = gpu_select(d, K, seed)
+    want = O.randk_select(d, K, seed)
+    assert np.array_equal(got, want)
+
+
+def test_selection_repeatable_and_seeded():
+    a = gpu_select(500_000, 2000, 1)
+    b = gpu_select(500_000, 2000, 1)
+    c = gpu_select(500_000, 2000, 2)
+    assert np.array_equal(a, b) and not np.array_equal(a, c)
+
+
+def test_gather_scatter_exact():
+    d, M, K = 100_003, 3, 777
+    host = synth.mixed_rows(M, d, seed=1, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(host).to(DEV)
+    st = RandKStep(d, M, K, [127.0], device=DEV)
+    st.select(3)
+    st.gather(g)
+    st.inner.out[:K].copy_(torch.arange(K, dtype=torch.float32, device=DEV) + 0.5)
+    st.out.fill_(7.0)
+    st.scatter()
+    torch.cuda.synchronize()
+    sel = st.sel[:K].cpu().numpy().view(np.uint32).astype(np.int64)
+    assert np.array_equal(st.sub[:, :K].cpu().numpy().view(np.int32), host[:, sel].view(np.int32))
+    full = np.zeros(d, dtype=np.float32)
+    full[sel] = np.arange(K, dtype=np.float32) + 0.5
+    assert np.array_equal(st.out[:d].cpu().numpy(), full)
+
+
+@pytest.mark.parametrize("scales", [[127.0], synth.scales_for(8, 2), synth.scales_for(4, 4)],
+                         ids=["single", "two-scale", "K4"])
+def test_randk_step_matches_oracle(scales):
+    d, M, K = 1_000_003, 4, 10_000
+    host = synth.mixed_rows(M, d, seed=7, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(host).to(DEV)
+    st = RandKStep(d, M, K, scales, device=DEV)
+    out = st.run(g, seed=42)
+    torch.cuda.synchronize()
+    W = np.float32(st.inner.w[0].item())
+    ref = O.randk_pipeline(host, K, scales, seed=42, d=d, W=W)
+    assert abs(int(W.view(np.int32)) - int(ref["W_oracle"].view(np.int32))) <= 1
+    assert np.array_equal(st.sel[:K].cpu().numpy().view(np.uint32), ref["sel"])
+    assert np.array_equal(st.inner.codes[:, :K].cpu().numpy(), ref["codes"])
+    assert np.array_equal(st.inner.sum[:K].cpu().numpy(), ref["sum"])
+    assert np.array_equal(out.cpu().numpy().view(np.int32), ref["full"].view(np.int32))
+
+
+def test_randk_workload_full_size():
+    """The ResNet-18-shaped workload with the paper's K = 10000."""
+    g, cfg = synth.make_gradients("resnet18", device=DEV)
+    d, M = cfg["d"], cfg["M"]
+    st = RandKStep(d, M, 10_000, [127.0], device=DEV)
+    out = st.run(g, seed=2)
+    torch.cuda.synchronize()
+    sel = O.randk_select(d, 10_000, 2)
+    assert np.array_equal(st.sel[:10_000].cpu().numpy().view(np.uint32), sel)
+    host_sub = g[:, torch.from_numpy(sel.astype(np.int64)).to(DEV)].cpu().numpy()
+    W = np.float32(st.inner.w[0].item())
+    ref = O.pipeline(host_sub, [127.0], 2, W=W)
+    full = np.zeros(d, dtype=np.float32)
+    full[sel.astype(np.int64)] = ref["out"]
+    assert np.array_equal(out.cpu().numpy().view(np.int32), full.view(np.int32))

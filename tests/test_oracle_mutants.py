@@ -11,7 +11,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "uq_oracle.c")
 PIN_TESTS = [os.path.join(ROOT, "tests", f) for f in (
     "test_oracle_philox.py", "test_oracle_scale.py", "test_oracle_index.py",
-    "test_oracle_quantize.py", "test_oracle_aggregate.py")]
+    "test_oracle_quantize.py", "test_oracle_aggregate.py", "test_oracle_randk.py")]
 
 MUTANTS = {
     "philox multiplier": ("0xD2511F53u * (uint64_t)x0", "0xD2511F55u * (uint64_t)x0"),
@@ -27,6 +27,9 @@ MUTANTS = {
     "truncated level": ("float p = x - lf;", "float p = x - lf; p = p * 0.5f;"),
     "dequant ignores index": ("out[i] = (float)sum[i] * deq[k];", "out[i] = (float)sum[i] * deq[0];"),
     "worker not in counter": ("(uint32_t)(block >> 32), worker, 0u", "(uint32_t)(block >> 32), 0u, 0u"),
+    "randk largest keys": ("out[j] = keys[j].idx;", "out[j] = keys[d - 1 - j].idx;"),
+    "randk low word reused": ("        ctr[3] = 3u;\n        orc_philox4x32_10(ctr, key, out);\n        lo[j]",
+                              "        ctr[3] = 2u;\n        orc_philox4x32_10(ctr, key, out);\n        lo[j]"),
 }
 
 
