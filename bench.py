@@ -29,19 +29,25 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCES = ["paper_2109_12497_amd/csrc/uq_kernels.hip", "paper_2109_12497_amd/csrc/uq_device.hpp"]
 
 
-def quantize_bytes_per_launch(d: int, rows: int, K: int) -> int:
+def code_bytes(d: int, bits: int) -> int:
+    return (d * bits + 7) // 8
+
+
+def quantize_bytes_per_launch(d: int, rows: int, K: int, bits: int = 8) -> int:
     """One quantiser launch over `rows` workers: their gradients in, their
     codes out, and (several scales) the shared index, needed once."""
-    return rows * d * (4 + 1) + (d if K > 1 else 0)
+    return rows * (4 * d + code_bytes(d, bits)) + (d if K > 1 else 0)
 
 
-def algorithmic_bytes(d: int, M: int, K: int, streamed: bool) -> dict:
+def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> dict:
     """Bytes each stage must move at minimum (reads + writes), per step."""
     multi = K > 1
+    cb = code_bytes(d, bits)
     b = {
         "shared_scale": 4 * M * d + (4 * M * d + d if multi else 0),
-        "quantize": (M * quantize_bytes_per_launch(d, 1, K)) if streamed else quantize_bytes_per_launch(d, M, K),
-        "sum": (M * d + 4 * d) if not streamed else (d + 4 * d) + (M - 1) * (d + 8 * d),
+        "quantize": ((M * quantize_bytes_per_launch(d, 1, K, bits)) if streamed
+                     else quantize_bytes_per_launch(d, M, K, bits)),
+        "sum": (M * cb + 4 * d) if not streamed else (cb + 4 * d) + (M - 1) * (cb + 8 * d),
         "dequantize": d * (4 + 4 + (1 if multi else 0)),
     }
     b["total"] = sum(b.values())
@@ -188,7 +194,8 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     if cfg.get("randk"):
         return bench_randk(args, g, cfg)
-    step = Step(d, M, scales, device="cuda", streamed=streamed)
+    bits = int(cfg.get("bits", 8))
+    step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits)
     torch.cuda.synchronize()
 
     for _ in range(args.warmup):
@@ -242,7 +249,7 @@ def main() -> int:
         ev["dequantize"].append((a, b))
     torch.cuda.synchronize()
     stage_ms = {s: sum(x.elapsed_time(y) for x, y in ev[s]) / args.steps for s in stages}
-    nbytes = algorithmic_bytes(d, M, K, streamed)
+    nbytes = algorithmic_bytes(d, M, K, streamed, bits)
 
     # -- dominant kernel (the quantiser): launches back to back between two
     # events on the stream it runs on, so the average is the kernel's own
@@ -256,9 +263,9 @@ def main() -> int:
     b = mark()
     torch.cuda.synchronize()
     q_launch_ms = a.elapsed_time(b) / reps
-    q_bytes_launch = quantize_bytes_per_launch(d, rows_per_launch, K)
+    q_bytes_launch = quantize_bytes_per_launch(d, rows_per_launch, K, bits)
     achieved = q_bytes_launch / (q_launch_ms * 1e-3) / 1e9
-    kernel_name = "k_quantise_multi" if K > 1 else "k_quantise_single"
+    kernel_name = ("k_quantise_multi" if K > 1 else "k_quantise_single") + ("" if bits == 8 else f"_{bits}bit")
     traffic = measured_traffic(kernel_name, args.workload)
 
     result = {
@@ -275,7 +282,7 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed,
-                   "quantizer": "multi" if K > 1 else "single", "streamed": streamed,
+                   "quantizer": "multi" if K > 1 else "single", "streamed": streamed, "code_bits": bits,
                    "parallelism": "one GPU, M workers simulated"},
         "pct_hbm_peak": round(100 * nbytes["total"] / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},

@@ -147,6 +147,32 @@ int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w,
                   const float* scales, int32_t K, const uint8_t* idx, float* out, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Sub-byte codes.  The paper stores every code in 8 bits because its
+ * framework had no narrower type, and found bit-packing too slow (Sec. 5,
+ * Appendix A).  Here the quantiser packs while it stores and the sum
+ * unpacks while it adds: the codes are the same as those of
+ * uq_quantize_single / uq_quantize_multi, held as `bits`-bit two's
+ * complement fields, low bits first: the code of coordinate i occupies bits
+ * (i % (8/bits)) * bits .. + bits-1 of byte i / (8/bits).
+ * ------------------------------------------------------------------------ */
+
+/*
+ * Quantise to packed codes.  bits = 4 needs s_0 <= 7, bits = 2 needs s_0 <= 1.
+ *   scales, K, idx  as for uq_quantize_multi (K = 1: one scale, idx may be NULL)
+ *   packed          [rows][ldp] bytes, ldp >= ceil(d * bits / 8), ldp % 16 == 0
+ * Other arguments as for uq_quantize_single.
+ */
+int uq_quantize_packed(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                       const float* w, const float* scales, int32_t K, const uint8_t* idx,
+                       uint64_t seed, int32_t bits, uint8_t* packed, int64_t ldp, void* stream);
+
+/*
+ * uq_sum_codes for packed rows: sum_i (=, or +=) the rows' unpacked codes.
+ */
+int uq_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, int32_t bits,
+                  int32_t accumulate, int32_t* sum, void* stream);
+
+/* ------------------------------------------------------------------------
  * GlobalRandK sparsification (Sec. 3.3 GlobalRandKMaxNorm, Sec. 3.4
  * GlobalRandKMaxNormMultiScale): K coordinates chosen uniformly at random,
  * the same for every worker, are quantised as a K-dimensional problem with

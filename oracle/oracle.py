@@ -62,6 +62,12 @@ def lib():
         L.orc_sum_codes.restype = None
         L.orc_dequantize.argtypes = [P, i64, i32, f32, P, i32, P, P]
         L.orc_dequantize.restype = None
+        L.orc_pack_codes.argtypes = [P, i64, i32, P]
+        L.orc_pack_codes.restype = None
+        L.orc_unpack_codes.argtypes = [P, i64, i32, P]
+        L.orc_unpack_codes.restype = None
+        L.orc_sum_packed.argtypes = [P, i64, i32, i64, i32, P]
+        L.orc_sum_packed.restype = None
         L.orc_randk_keys.argtypes = [u64, i64, i64, P, P]
         L.orc_randk_keys.restype = None
         L.orc_randk_select.argtypes = [i64, i64, u64, P, P]
@@ -197,6 +203,36 @@ def pipeline(g: np.ndarray, scales, seed: int, d: int | None = None, W=None,
     out = dequantize(sums, M, W, s, idx)
     return {"W": W, "W_oracle": W_own, "sumsq": S, "idx": idx, "codes": codes,
             "sum": sums, "out": out}
+
+
+# ---------------------------------------------------------------------------
+# Sub-byte codes
+# ---------------------------------------------------------------------------
+
+def pack_codes(codes: np.ndarray, bits: int) -> np.ndarray:
+    codes = np.ascontiguousarray(codes, dtype=np.int8).reshape(-1)
+    per = 8 // bits
+    out = np.zeros((codes.size + per - 1) // per, dtype=np.uint8)
+    lib().orc_pack_codes(_ptr(codes), codes.size, bits, _ptr(out))
+    return out
+
+
+def unpack_codes(packed: np.ndarray, n: int, bits: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8).reshape(-1)
+    out = np.zeros(n, dtype=np.int8)
+    lib().orc_unpack_codes(_ptr(packed), n, bits, _ptr(out))
+    return out
+
+
+def sum_packed(packed: np.ndarray, n: int, bits: int) -> np.ndarray:
+    """packed: [rows, ldp] uint8; the int32 sum of the rows' first n codes."""
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    if packed.ndim == 1:
+        packed = packed.reshape(1, -1)
+    rows, ldp = packed.shape
+    out = np.zeros(n, dtype=np.int32)
+    lib().orc_sum_packed(_ptr(packed), n, rows, ldp, bits, _ptr(out))
+    return out
 
 
 # ---------------------------------------------------------------------------

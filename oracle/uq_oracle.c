@@ -39,6 +39,11 @@
  *   - the all-reduce of the codes is an exact int32 sum; 1/M is folded into
  *     the reconstruction factor fl32(W / (M * s_k)).
  *
+ * Sub-byte codes (the bit-packing the paper discusses in Sec. 5 and
+ * Appendix A): with `bits` = 4 (s_min <= 7) or 2 (s_min <= 1) the code of
+ * coordinate i is stored two's complement in bits (i % (8/bits)) * bits ..
+ * +bits-1 of byte i / (8/bits), low bits first.
+ *
  * GlobalRandK (Sec. 3.3-3.4): the K coordinates are a uniformly random
  * K-subset shared by all workers: coordinate i gets the 64-bit key
  * (hi, lo) = (word i%4 of Philox block (i/4, 0, purpose 2),
@@ -340,4 +345,51 @@ void orc_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* out, void* 
     for (int64_t j = 0; j < K; ++j)
         out[j] = keys[j].idx;
     qsort(out, (size_t)K, sizeof(uint32_t), orc_u32_cmp);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sub-byte codes: packing, unpacking and the integer sum of packed rows.    */
+/* ------------------------------------------------------------------------ */
+
+void orc_pack_codes(const int8_t* codes, int64_t n, int32_t bits, uint8_t* out)
+{
+    int per = 8 / bits;
+    uint32_t field = (1u << bits) - 1u;
+    for (int64_t b = 0; b < (n + per - 1) / per; ++b)
+        out[b] = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t v = (uint32_t)(int32_t)codes[i] & field;
+        out[i / per] = (uint8_t)(out[i / per] | (v << ((i % per) * bits)));
+    }
+}
+
+void orc_unpack_codes(const uint8_t* packed, int64_t n, int32_t bits, int8_t* out)
+{
+    int per = 8 / bits;
+    uint32_t field = (1u << bits) - 1u;
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t v = ((uint32_t)packed[i / per] >> ((i % per) * bits)) & field;
+        int32_t x = (int32_t)v;
+        if (x >= (1 << (bits - 1)))
+            x -= 1 << bits; /* sign extension */
+        out[i] = (int8_t)x;
+    }
+}
+
+/* sum_i = sum over rows of the unpacked code of coordinate i (row stride ldp bytes). */
+void orc_sum_packed(const uint8_t* packed, int64_t n, int32_t rows, int64_t ldp, int32_t bits, int32_t* sum)
+{
+    for (int64_t i = 0; i < n; ++i)
+        sum[i] = 0;
+    int8_t one;
+    for (int32_t m = 0; m < rows; ++m) {
+        const uint8_t* row = packed + (int64_t)m * ldp;
+        for (int64_t i = 0; i < n; ++i) {
+            int per = 8 / bits;
+            uint8_t byte = row[i / per];
+            uint8_t sub[1] = { (uint8_t)(byte >> ((i % per) * bits)) };
+            orc_unpack_codes(sub, 1, bits, &one);
+            sum[i] += one;
+        }
+    }
 }

@@ -195,18 +195,19 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const flo
 
 static int quantise_common(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
                            const float* w, const uq::ScaleSet& S, const uint8_t* idx, uint64_t seed,
-                           int8_t* codes, int64_t ldc, void* stream)
+                           void* codes, int64_t ldc, int32_t bits, void* stream)
 {
     UQ_TRY(check_dims(d, rows, "rows"));
     UQ_TRY(check_rows(g, d, rows, ldg, 4, "g"));
-    UQ_TRY(check_rows(codes, d, rows, ldc, 16, "codes"));
+    const int64_t row_bytes = (d * bits + 7) / 8;
+    UQ_TRY(check_rows(codes, row_bytes, rows, ldc, 16, "codes"));
     UQ_TRY(check_w(w));
     if (worker0 < 0 || static_cast<int64_t>(worker0) + rows > (int64_t(1) << 31))
         return fail(UQ_ERANGE, "worker ids %d .. %lld exceed [0, 2^31)", worker0,
                     (long long)worker0 + rows - 1);
     if (S.K > 1)
         UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
-    return launched(uq::launch_quantise(g, d, rows, ldg, worker0, w, S, idx, seed, codes, ldc,
+    return launched(uq::launch_quantise(g, d, rows, ldg, worker0, w, S, idx, seed, codes, ldc, bits,
                                         static_cast<hipStream_t>(stream)));
 }
 
@@ -219,7 +220,7 @@ int uq_quantize_single(const float* g, int64_t d, int32_t rows, int64_t ldg, int
     std::memset(&S, 0, sizeof S);
     S.s[0] = static_cast<float>(s);
     S.K = 1;
-    return quantise_common(g, d, rows, ldg, worker0, w, S, nullptr, seed, codes, ldc, stream);
+    return quantise_common(g, d, rows, ldg, worker0, w, S, nullptr, seed, codes, ldc, 8, stream);
 }
 
 int uq_quantize_multi(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
@@ -230,7 +231,41 @@ int uq_quantize_multi(const float* g, int64_t d, int32_t rows, int64_t ldg, int3
     UQ_TRY(check_scales(scales, K, &S));
     if (K > 1 && idx == nullptr && d > 0)
         return fail(UQ_EINVAL, "idx is NULL");
-    return quantise_common(g, d, rows, ldg, worker0, w, S, idx, seed, codes, ldc, stream);
+    return quantise_common(g, d, rows, ldg, worker0, w, S, idx, seed, codes, ldc, 8, stream);
+}
+
+int uq_quantize_packed(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                       const float* scales, int32_t K, const uint8_t* idx, uint64_t seed, int32_t bits,
+                       uint8_t* packed, int64_t ldp, void* stream)
+{
+    if (bits != 4 && bits != 2)
+        return fail(UQ_ERANGE, "bits = %d is not 4 or 2", bits);
+    uq::ScaleSet S;
+    UQ_TRY(check_scales(scales, K, &S));
+    if (S.s[0] > static_cast<float>((1 << (bits - 1)) - 1))
+        return fail(UQ_ERANGE, "smallest scale %g does not fit a %d-bit code", (double)S.s[0], bits);
+    if (K > 1 && idx == nullptr && d > 0)
+        return fail(UQ_EINVAL, "idx is NULL");
+    return quantise_common(g, d, rows, ldg, worker0, w, S, idx, seed, packed, ldp, bits, stream);
+}
+
+int uq_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, int32_t bits, int32_t accumulate,
+                  int32_t* sum, void* stream)
+{
+    if (bits != 4 && bits != 2)
+        return fail(UQ_ERANGE, "bits = %d is not 4 or 2", bits);
+    if (d < 0 || d > kMaxElems)
+        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
+    if (rows < 1)
+        return fail(UQ_EINVAL, "rows = %d is smaller than 1", rows);
+    if (rows > (1 << 24))
+        return fail(UQ_ERANGE, "rows = %d exceeds 2^24 (int32 sums could overflow)", rows);
+    if (accumulate != 0 && accumulate != 1)
+        return fail(UQ_EINVAL, "accumulate must be 0 or 1");
+    UQ_TRY(check_rows(packed, (d * bits + 7) / 8, rows, ldp, 16, "packed"));
+    UQ_TRY(check_vec(sum, d, "sum"));
+    return launched(uq::launch_sum_packed(packed, d, rows, ldp, bits, accumulate, sum,
+                                          static_cast<hipStream_t>(stream)));
 }
 
 int uq_sum_codes(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate, int32_t* sum,

@@ -278,12 +278,37 @@ __device__ __forceinline__ uint32_t half16(uint32_t packed01, uint32_t packed23,
     return (j & 1) ? (w >> 16) : (w & 0xFFFFu);
 }
 
-template <bool MULTI>
+// BITS = 8: int8 codes.  BITS = 4 or 2: codes packed low bits first, two or
+// four to a byte (every |code| <= s_0 fits the field; checked on the host).
+template <int BITS>
+__device__ __forceinline__ uint32_t pack_field(const float c[4])
+{
+    constexpr uint32_t mask = (1u << BITS) - 1u;
+    uint32_t w = 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        w |= (static_cast<uint32_t>(static_cast<int32_t>(c[j])) & mask) << (BITS * j);
+    return w;
+}
+
+template <int BITS>
+__device__ __forceinline__ void store_codes4(uint8_t* row, int64_t coord, const float c[4])
+{
+    if (BITS == 8)
+        *reinterpret_cast<uint32_t*>(row + coord) = pack4(static_cast<int32_t>(c[0]), static_cast<int32_t>(c[1]),
+                                                          static_cast<int32_t>(c[2]), static_cast<int32_t>(c[3]));
+    else if (BITS == 4)
+        *reinterpret_cast<uint16_t*>(row + coord / 2) = static_cast<uint16_t>(pack_field<4>(c));
+    else
+        row[coord / 4] = static_cast<uint8_t>(pack_field<2>(c));
+}
+
+template <bool MULTI, int BITS>
 __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g, int64_t d, int64_t ldg,
                                                      int32_t worker0, const float* __restrict__ wptr,
                                                      ScaleSet S, const uint8_t* __restrict__ idx,
                                                      uint32_t key0, uint32_t key1,
-                                                     int8_t* __restrict__ codes, int64_t ldc, int32_t tpw)
+                                                     uint8_t* __restrict__ codes, int64_t ldc, int32_t tpw)
 {
     __shared__ float inv_s[kMaxScales];
     const float W = *wptr;
@@ -304,7 +329,7 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
     const int32_t r = blockIdx.y;
     const uint32_t worker = static_cast<uint32_t>(worker0) + static_cast<uint32_t>(r);
     const float* row = g + static_cast<int64_t>(r) * ldg;
-    int8_t* out = codes + static_cast<int64_t>(r) * ldc;
+    uint8_t* out = codes + static_cast<int64_t>(r) * ldc;
 
     const int lane = threadIdx.x & 63;
     const bool odd = (lane & 1) != 0;
@@ -362,10 +387,8 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
                     c[j] = copysignf(lf[j] + (h < (t[j] & 0xFFFFu) ? 1.0f : 0.0f), v[j]);
             }
         }
-        *reinterpret_cast<uint32_t*>(out + a_off) = pack4(static_cast<int32_t>(c[0]), static_cast<int32_t>(c[1]),
-                                                          static_cast<int32_t>(c[2]), static_cast<int32_t>(c[3]));
-        *reinterpret_cast<uint32_t*>(out + b_off) = pack4(static_cast<int32_t>(c[4]), static_cast<int32_t>(c[5]),
-                                                          static_cast<int32_t>(c[6]), static_cast<int32_t>(c[7]));
+        store_codes4<BITS>(out, a_off, c);
+        store_codes4<BITS>(out, b_off, c + 4);
       }
     }
 
@@ -384,10 +407,24 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
                 inv[j] = MULTI ? inv_s[min(static_cast<uint32_t>(in ? idx[base + j] : 0), kmax)] : inv0;
             }
             quantise_group(v, inv, s0, static_cast<uint64_t>(q), worker, key0, key1, code);
+            if (BITS == 8) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (base + j < d)
-                    out[base + j] = static_cast<int8_t>(code[j]);
+                for (int j = 0; j < 8; ++j)
+                    if (base + j < d)
+                        out[base + j] = static_cast<uint8_t>(code[j]);
+            } else {
+                // the group's 8 codes fill whole bytes of its own (coordinates
+                // past d have code 0); the packed row holds them
+                float c[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    c[j] = static_cast<float>(code[j]);
+                if (BITS == 4)
+                    *reinterpret_cast<uint32_t*>(out + base / 2) = pack_field<4>(c) | (pack_field<4>(c + 4) << 16);
+                else
+                    *reinterpret_cast<uint16_t*>(out + base / 4) =
+                        static_cast<uint16_t>(pack_field<2>(c) | (pack_field<2>(c + 4) << 8));
+            }
         }
     }
 }
@@ -471,6 +508,57 @@ __global__ __launch_bounds__(kBlock) void k_sum(const int8_t* __restrict__ codes
         for (int32_t r = 0; r < rows; ++r)
             acc += codes[static_cast<int64_t>(r) * ldc + t];
         sum[t] = acc;
+    }
+}
+
+// Sum of packed rows (BITS = 4 or 2): a block tile of 4096 coordinates,
+// thread t unpacks coordinates 16t .. 16t+15 of the tile from one 8-byte
+// (4-bit) or 4-byte (2-bit) load per row with signed bit-field extracts.
+template <int BITS>
+__global__ __launch_bounds__(kBlock) void k_sum_packed(const uint8_t* __restrict__ packed, int64_t d, int32_t rows,
+                                                       int64_t ldp, int32_t accumulate, int32_t* __restrict__ sum)
+{
+    for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
+         tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
+        const int64_t c0 = tile0 + 16 * threadIdx.x;
+        if (c0 >= d)
+            continue;
+        const int64_t byte0 = c0 * BITS / 8;
+        int32_t acc[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            acc[j] = 0;
+        for (int32_t r = 0; r < rows; ++r) {
+            const uint8_t* p = packed + static_cast<int64_t>(r) * ldp + byte0;
+            uint32_t w[2];
+            if (BITS == 4) {
+                const uint2 x = *reinterpret_cast<const uint2*>(p);
+                w[0] = x.x;
+                w[1] = x.y;
+            } else {
+                w[0] = load_nt_u32(p);
+                w[1] = 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const uint32_t word = w[(j * BITS) / 32];
+                acc[j] += __builtin_amdgcn_sbfe(static_cast<int32_t>(word), (j * BITS) % 32, BITS);
+            }
+        }
+        if (c0 + 16 <= d) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                int4 a = make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
+                if (accumulate) {
+                    const int4 o = *reinterpret_cast<const int4*>(sum + c0 + 4 * c);
+                    a.x += o.x; a.y += o.y; a.z += o.z; a.w += o.w;
+                }
+                *reinterpret_cast<int4*>(sum + c0 + 4 * c) = a;
+            }
+        } else {
+            for (int j = 0; j < 16 && c0 + j < d; ++j)
+                sum[c0 + j] = acc[j] + (accumulate ? sum[c0 + j] : 0);
+        }
     }
 }
 
@@ -581,7 +669,7 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
 
 hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
                            const float* w, const ScaleSet& S, const uint8_t* idx, uint64_t seed,
-                           int8_t* codes, int64_t ldc, hipStream_t stream)
+                           void* codes, int64_t ldc, int32_t bits, hipStream_t stream)
 {
     if (d == 0)
         return hipSuccess;
@@ -595,12 +683,19 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
     if (static_cast<int64_t>(tile_blocks) > per_row)
         tile_blocks = static_cast<unsigned>(per_row < 8 ? 8 : per_row);
     dim3 grid(tile_blocks, static_cast<unsigned>(rows));
-    if (S.K > 1)
-        hipLaunchKernelGGL(k_quantise<true>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx, key0,
-                           key1, codes, ldc, tpw);
-    else
-        hipLaunchKernelGGL(k_quantise<false>, grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx, key0,
-                           key1, codes, ldc, tpw);
+    uint8_t* out = reinterpret_cast<uint8_t*>(codes);
+#define UQ_LAUNCH_QUANTISE(MULTI, BITS)                                                                        \
+    hipLaunchKernelGGL((k_quantise<MULTI, BITS>), grid, dim3(kBlock), 0, stream, g, d, ldg, worker0, w, S, idx, \
+                       key0, key1, out, ldc, tpw)
+    const bool multi = S.K > 1;
+    if (bits == 8) {
+        if (multi) UQ_LAUNCH_QUANTISE(true, 8); else UQ_LAUNCH_QUANTISE(false, 8);
+    } else if (bits == 4) {
+        if (multi) UQ_LAUNCH_QUANTISE(true, 4); else UQ_LAUNCH_QUANTISE(false, 4);
+    } else {
+        if (multi) UQ_LAUNCH_QUANTISE(true, 2); else UQ_LAUNCH_QUANTISE(false, 2);
+    }
+#undef UQ_LAUNCH_QUANTISE
     return hipGetLastError();
 }
 
@@ -611,6 +706,19 @@ hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc,
         return hipSuccess;
     const unsigned gx = one_shot(d, kSumTile);
     hipLaunchKernelGGL(k_sum, dim3(gx), dim3(kBlock), 0, stream, codes, d, rows, ldc, accumulate, sum);
+    return hipGetLastError();
+}
+
+hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, int32_t bits,
+                             int32_t accumulate, int32_t* sum, hipStream_t stream)
+{
+    if (d == 0)
+        return hipSuccess;
+    const unsigned gx = one_shot(d, kSumTile);
+    if (bits == 4)
+        hipLaunchKernelGGL(k_sum_packed<4>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
+    else
+        hipLaunchKernelGGL(k_sum_packed<2>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
     return hipGetLastError();
 }
 

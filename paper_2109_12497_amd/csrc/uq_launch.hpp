@@ -34,9 +34,12 @@ int64_t grid_cap();
 
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
                                float* w, uint8_t* idx, double* part, hipStream_t stream);
+// bits = 8: int8 codes [rows][ldc]; bits = 4 or 2: packed codes, ldc in bytes
 hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
                            const float* w, const ScaleSet& S, const uint8_t* idx, uint64_t seed,
-                           int8_t* codes, int64_t ldc, hipStream_t stream);
+                           void* codes, int64_t ldc, int32_t bits, hipStream_t stream);
+hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, int32_t bits,
+                             int32_t accumulate, int32_t* sum, hipStream_t stream);
 hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,
                       int32_t* sum, hipStream_t stream);
 // GlobalRandK: at most kRandkCandidates keys sharing the threshold's 24-bit

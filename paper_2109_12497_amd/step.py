@@ -9,8 +9,9 @@ from __future__ import annotations
 
 import torch
 
-from . import (uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_single, uq_randk_select,
-               uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes, uq_workspace_bytes)
+from . import (uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_packed, uq_quantize_single,
+               uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes, uq_sum_packed,
+               uq_workspace_bytes)
 
 
 def round_up(x: int, m: int) -> int:
@@ -23,14 +24,18 @@ class Step:
     streamed=False: every worker's codes are materialised ([M, ldc] int8) and
     summed by one call.  streamed=True: one code row is reused; each worker is
     quantised and accumulated into the int32 sum in turn.
+    bits = 4 or 2: the codes are held packed ([M, ldc] bytes, ldc >= d*bits/8).
     """
 
-    def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None):
+    def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None,
+                 bits: int = 8):
         self.d, self.M = d, M
         self.scales = [float(s) for s in scales]
         self.K = len(self.scales)
         self.streamed = streamed
-        self.ldc = round_up(max(d, 1), 256) if ldc is None else ldc
+        self.bits = bits
+        row_bytes = (max(d, 1) * bits + 7) // 8
+        self.ldc = round_up(row_bytes, 256) if ldc is None else ldc
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
@@ -51,7 +56,10 @@ class Step:
     def quantize(self, g, seed: int, rows: int | None = None, worker0: int = 0, codes=None, stream=None):
         rows = self.M if rows is None else rows
         codes = self.codes if codes is None else codes
-        if self.K == 1:
+        if self.bits != 8:
+            uq_quantize_packed(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed,
+                               self.bits, codes, codes.stride(0), stream)
+        elif self.K == 1:
             uq_quantize_single(g, self.d, rows, g.stride(0), worker0, self.w, int(self.scales[0]), seed, codes,
                                codes.stride(0), stream)
         else:
@@ -61,7 +69,10 @@ class Step:
     def sum_codes(self, rows: int | None = None, accumulate: int = 0, codes=None, stream=None):
         rows = self.M if rows is None else rows
         codes = self.codes if codes is None else codes
-        uq_sum_codes(codes, self.d, rows, codes.stride(0), accumulate, self.sum, stream)
+        if self.bits != 8:
+            uq_sum_packed(codes, self.d, rows, codes.stride(0), self.bits, accumulate, self.sum, stream)
+        else:
+            uq_sum_codes(codes, self.d, rows, codes.stride(0), accumulate, self.sum, stream)
 
     def dequantize(self, stream=None):
         uq_dequantize(self.sum, self.d, self.M, self.w, self.scales, self.K, self.idx, self.out, stream)

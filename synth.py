@@ -17,6 +17,8 @@ Workloads (flat fp32 gradients of M simulated workers, row-major [M][ldg]):
                      N(0, 1e-3^2); one scale s = 7, or K = 4 scales 7 * 16^k.
   * student-t      : d = 2^30, M = 16, 1e-4 * t_3; K = 8 scales 127 * 16^k,
                      workers streamed through an int32 accumulator.
+  * *-4bit, *-2bit : the same gradients with the codes held packed (s = 7
+                     in 4 bits, s = 1 in 2 bits).
   * *-grandk*      : the same gradients with GlobalRandK sparsification of
                      10000 coordinates (one scale, or two scales 127, 2032).
 
@@ -92,6 +94,10 @@ WORKLOADS = {
     "vgg16-multi": dict(d=138_357_544, M=16, scales=scales_for(4, 4), seed=4, kind="vgg16"),
     "student-t": dict(d=2 ** 30, M=16, scales=scales_for(8, 8), seed=5, kind="student-t",
                       streamed=True),
+    # the same codes held as 4-bit / 2-bit fields
+    "vgg16-single-4bit": dict(d=138_357_544, M=16, scales=scales_for(4, 1), seed=4, kind="vgg16", bits=4),
+    "vgg16-multi-4bit": dict(d=138_357_544, M=16, scales=scales_for(4, 4), seed=4, kind="vgg16", bits=4),
+    "resnet18-2bit": dict(d=11_173_962, M=8, scales=scales_for(2, 1), seed=2, kind="resnet18", bits=2),
     # GlobalRandK (Sec. 3.3-3.4) with the paper's K = 10000 sampled coordinates
     "resnet18-grandk": dict(d=11_173_962, M=8, scales=scales_for(8, 1), seed=2, kind="resnet18", randk=10_000),
     "resnet50-grandk-ts": dict(d=25_557_032, M=8, scales=scales_for(8, 2), seed=3, kind="resnet50",

@@ -183,3 +183,30 @@ def test_scatter_rejects(kw, want):
 def test_randk_workspace_fixed_and_aligned():
     b = uq.uq_randk_workspace_bytes(10 ** 6, 10_000)
     assert b % 256 == 0 and 32 * 1024 < b < 1024 * 1024
+
+
+# Packed codes ---------------------------------------------------------------
+
+def status_qp(g=A, d=100, rows=2, ldg=128, worker0=0, w=A, scales=[7.0], K=1, idx=None, bits=4, packed=A, ldp=64):
+    hs = uq._HostScales(scales)
+    return L.uq_quantize_packed(g, d, rows, ldg, worker0, w, hs.ptr, K, idx, 1, bits, packed, ldp, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(bits=8), "range"), (dict(bits=3), "range"), (dict(scales=[15.0]), "range"),
+    (dict(bits=2, scales=[3.0]), "range"), (dict(ldp=48), "inval"), (dict(ldp=72), "align"),
+    (dict(packed=None), "inval"), (dict(K=2, scales=[7.0, 112.0], idx=None), "inval"), (dict(rows=0), "inval"),
+])
+def test_quantize_packed_rejects(kw, want):
+    assert status_qp(**kw) == E[want]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(bits=8), "range"), (dict(ldp=16), "inval"), (dict(ldp=56), "align"), (dict(sum_=None), "inval"),
+    (dict(acc=3), "inval"), (dict(rows=0), "inval"),
+])
+def test_sum_packed_rejects(kw, want):
+    args = dict(packed=A, d=100, rows=2, ldp=64, bits=4, acc=0, sum_=A)
+    args.update(kw)
+    assert L.uq_sum_packed(args["packed"], args["d"], args["rows"], args["ldp"], args["bits"], args["acc"],
+                           args["sum_"], None) == E[want]

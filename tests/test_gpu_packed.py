@@ -1,0 +1,79 @@
+"""GPU parity for sub-byte codes: the packed codes unpack to exactly the
+codes of the int8 path and of the oracle, and the packed sum equals the
+int8 sum."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import synth  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+from paper_2109_12497_amd.step import Step  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def run(host, d, scales, bits, seed, streamed=False):
+    g = torch.from_numpy(host).to(DEV)
+    st = Step(d, host.shape[0], scales, device=DEV, bits=bits, streamed=streamed)
+    st.run(g, seed)
+    torch.cuda.synchronize()
+    return st
+
+
+@pytest.mark.parametrize("d", [1, 7, 8, 9, 31, 511, 512, 513, 1000, 4097, 10_007, 65_539])
+@pytest.mark.parametrize("scales,bits", [([7.0], 4), ([7.0, 112.0, 1792.0], 4), ([1.0], 2), ([1.0, 16.0], 2)],
+                         ids=["s7-4bit", "K3-4bit", "s1-2bit", "K2-2bit"])
+def test_packed_matches_oracle(d, scales, bits):
+    M = 3
+    host = synth.mixed_rows(M, d, seed=d + bits, ldg=synth.round_up(d, 64))
+    st = run(host, d, scales, bits, seed=99)
+    W = np.float32(st.w[0].item())
+    ref = O.pipeline(host, scales, 99, d=d, W=W)
+    nbytes = (d * bits + 7) // 8
+    packed = st.codes[:, :nbytes].cpu().numpy()
+    for m in range(M):
+        assert np.array_equal(O.unpack_codes(packed[m], d, bits), ref["codes"][m]), m
+    assert np.array_equal(st.sum[:d].cpu().numpy(), ref["sum"])
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
+@pytest.mark.parametrize("bits,scales", [(4, [7.0]), (2, [1.0])])
+def test_packed_equals_int8_path(bits, scales):
+    d, M = 300_001, 5
+    host = synth.gaussian_rows(M, d, seed=4, ldg=synth.round_up(d, 64))
+    a = run(host, d, scales, 8, seed=5)
+    b = run(host, d, scales, bits, seed=5)
+    c = run(host, d, scales, bits, seed=5, streamed=True)
+    codes8 = a.codes[:, :d].cpu().numpy()
+    packed = b.codes[:, :(d * bits + 7) // 8].cpu().numpy()
+    for m in range(M):
+        assert np.array_equal(O.unpack_codes(packed[m], d, bits), codes8[m])
+    for st in (b, c):
+        assert torch.equal(a.sum[:d], st.sum[:d])
+        assert torch.equal(a.out[:d], st.out[:d])
+
+
+def test_packed_vgg16_full_size():
+    """The VGG-16-shaped workload with s = 7 held as 4-bit codes: identical
+    sums and outputs to the int8 path at full size."""
+    g, cfg = synth.make_gradients("vgg16-single", device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    a = Step(d, M, scales, device=DEV)
+    a.run(g, seed)
+    b = Step(d, M, scales, device=DEV, bits=4)
+    b.run(g, seed)
+    torch.cuda.synchronize()
+    assert torch.equal(a.sum[:d], b.sum[:d])
+    assert torch.equal(a.out[:d], b.out[:d])
+    # a window of packed codes against the int8 codes
+    i0, n = 77_000_000, 1 << 16
+    packed = b.codes[:, i0 // 2:(i0 + n) // 2].cpu().numpy()
+    codes8 = a.codes[:, i0:i0 + n].cpu().numpy()
+    for m in range(M):
+        assert np.array_equal(O.unpack_codes(packed[m], n, 4), codes8[m])
