@@ -10,6 +10,7 @@ the 8 TB/s HBM peak the step's algorithmic bytes reach.
 
 Prints one JSON line.  Extra modes:
   --workload NAME       another workload of synth.WORKLOADS (default resnet18)
+  --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
 """
@@ -122,12 +123,15 @@ def bench_randk(args, g, cfg) -> int:
     d, M, scales, seed, k = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"], cfg["randk"]
     st = RandKStep(d, M, k, scales, device="cuda")
     stream = torch.cuda.current_stream()
+    from paper_2109_12497_amd.step import capture
+
+    replay = capture(st, g, seed).replay if args.graph else (lambda: st.run(g, seed))
     for _ in range(args.warmup):
-        st.run(g, seed)
+        replay()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        st.run(g, seed)
+        replay()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     stages = ["select", "gather", "aggregate", "scatter"]
@@ -152,6 +156,7 @@ def bench_randk(args, g, cfg) -> int:
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed, "randk": k,
                    "quantizer": "multi" if len(scales) > 1 else "single",
+                   "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
         "stage_ms": stage_ms, "roofline": None, "cpu_baseline": None}))
     return 0
@@ -166,6 +171,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work to aim for")
     ap.add_argument("--copy-probe", type=int, default=0)
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step captured in a HIP graph instead of host launches")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -202,11 +209,20 @@ def main() -> int:
         step.run(g, seed)
     torch.cuda.synchronize()
 
-    # -- timed region: K whole steps, nothing else on the stream ------------
+    # -- timed region: K whole steps (host launches, or with --graph replays
+    # of the step's kernels captured once in a HIP graph)
+    from paper_2109_12497_amd.step import capture
+
+    if args.graph:
+        replay = capture(step, g, seed).replay
+    else:
+        replay = lambda: step.run(g, seed)  # noqa: E731
+    for _ in range(args.warmup):
+        replay()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step.run(g, seed)
+        replay()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed / args.steps * 1e3
@@ -283,6 +299,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed,
                    "quantizer": "multi" if K > 1 else "single", "streamed": streamed, "code_bits": bits,
+                   "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
         "pct_hbm_peak": round(100 * nbytes["total"] / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},

@@ -74,8 +74,8 @@ enum uq_status {
 #define UQ_MAX_SCALES 16
 
 /*
- * Shared scale of Sec. 3.1/3.2: W = max_m ||g^m||_2 (the "MaxAllReduce Norm"
- * of Algorithm 1 and Algorithm 2), and for K > 1 also the shared scale index
+ * Shared scale of Sec. 3.1/3.2: W = max_m ||g^m||_2 (the all-reduce of the
+ * norms by maximum in Algorithm 1 and Algorithm 2), and for K > 1 also the shared scale index
  * of Sec. 3.2 (the per-coordinate rule Eq. (11) followed by scale sharing,
  * s*_i = min_m s*^m_i).
  *   g        [M][ldg] fp32, the M workers' gradients (read)

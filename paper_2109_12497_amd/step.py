@@ -125,3 +125,20 @@ class RandKStep:
         self.inner.run(self.sub, seed, stream)
         self.scatter(stream)
         return self.out[:self.d]
+
+
+def capture(step, g, seed: int):
+    """Record step.run(g, seed) into a HIP graph (torch's graph API over the
+    stream the library launches on).  Replaying it redoes the whole step on
+    the same buffers; the library's kernels issue no memsets or allocations."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step.run(g, seed)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step.run(g, seed)
+    torch.cuda.synchronize()
+    return graph
