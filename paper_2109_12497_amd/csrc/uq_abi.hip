@@ -41,6 +41,16 @@ bool integral(float s)
     return std::isfinite(s) && std::floor(s) == s;
 }
 
+uq::ScaleSet one_scale(float s)
+{
+    uq::ScaleSet S;
+    std::memset(&S, 0, sizeof S);
+    S.s[0] = s;
+    S.K = 1;
+    S.s_last = s;
+    return S;
+}
+
 int check_scales(const float* scales, int32_t K, uq::ScaleSet* S)
 {
     if (K < 1 || K > UQ_MAX_SCALES)
@@ -59,6 +69,7 @@ int check_scales(const float* scales, int32_t K, uq::ScaleSet* S)
     if (scales[0] > 127.0f)
         return fail(UQ_ERANGE, "smallest scale %g exceeds 127 (codes are int8)", (double)scales[0]);
     S->K = K;
+    S->s_last = scales[K - 1];
     return UQ_OK;
 }
 
@@ -174,9 +185,7 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const flo
     UQ_TRY(check_w(w));
     uq::ScaleSet S;
     if (K == 1 && scales == nullptr) {
-        std::memset(&S, 0, sizeof S);
-        S.s[0] = 1.0f;
-        S.K = 1;
+        S = one_scale(1.0f);
     } else {
         UQ_TRY(check_scales(scales, K, &S));
     }
@@ -216,10 +225,7 @@ int uq_quantize_single(const float* g, int64_t d, int32_t rows, int64_t ldg, int
 {
     if (s < 1 || s > 127)
         return fail(UQ_ERANGE, "s = %d is outside [1, 127]", s);
-    uq::ScaleSet S;
-    std::memset(&S, 0, sizeof S);
-    S.s[0] = static_cast<float>(s);
-    S.K = 1;
+    const uq::ScaleSet S = one_scale(static_cast<float>(s));
     return quantise_common(g, d, rows, ldg, worker0, w, S, nullptr, seed, codes, ldc, 8, stream);
 }
 

@@ -216,13 +216,12 @@ __device__ __forceinline__ void quantise_group(const float v[8], const float inv
     const uint4 hi = philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 0u,
                                    key0, key1);
     const uint32_t hw[4] = {hi.x, hi.y, hi.z, hi.w};
-    float c[8], lf[8];
-    uint32_t t[8];
+    float x[8];
     bool tie[8];
     bool any_tie = false;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        c[j] = quantise_hi(v[j], inv[j], s0, half_of(hw, j), &tie[j], &t[j], &lf[j]);
+        code[j] = quantise_hi(v[j], inv[j], s0, half_of(hw, j), &tie[j], &x[j]);
         any_tie = any_tie || tie[j];
     }
     if (__builtin_expect(any_tie, 0)) {
@@ -232,11 +231,8 @@ __device__ __forceinline__ void quantise_group(const float v[8], const float inv
 #pragma unroll
         for (int j = 0; j < 8; ++j)
             if (tie[j])
-                c[j] = copysignf(lf[j] + (half_of(lw, j) < (t[j] & 0xFFFFu) ? 1.0f : 0.0f), v[j]);
+                code[j] = quantise_tie(v[j], x[j], half_of(lw, j));
     }
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-        code[j] = static_cast<int32_t>(c[j]);
 }
 
 // Wave tiles.  A wave quantises 512 consecutive coordinates (64 Philox blocks)
@@ -281,78 +277,99 @@ __device__ __forceinline__ uint32_t half16(uint32_t packed01, uint32_t packed23,
 // BITS = 8: int8 codes.  BITS = 4 or 2: codes packed low bits first, two or
 // four to a byte (every |code| <= s_0 fits the field; checked on the host).
 template <int BITS>
-__device__ __forceinline__ uint32_t pack_field(const float c[4])
+__device__ __forceinline__ uint32_t pack_field(const int32_t c[4])
 {
     constexpr uint32_t mask = (1u << BITS) - 1u;
     uint32_t w = 0u;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-        w |= (static_cast<uint32_t>(static_cast<int32_t>(c[j])) & mask) << (BITS * j);
+        w |= (static_cast<uint32_t>(c[j]) & mask) << (BITS * j);
     return w;
 }
 
+// Stores four consecutive codes held as 16-bit lanes of p01 (codes 0, 1) and
+// p23 (codes 2, 3) at coordinate `coord` of a code row.
 template <int BITS>
-__device__ __forceinline__ void store_codes4(uint8_t* row, int64_t coord, const float c[4])
+__device__ __forceinline__ void store_pairs(uint8_t* row, int64_t coord, uint32_t p01, uint32_t p23)
 {
-    if (BITS == 8)
-        *reinterpret_cast<uint32_t*>(row + coord) = pack4(static_cast<int32_t>(c[0]), static_cast<int32_t>(c[1]),
-                                                          static_cast<int32_t>(c[2]), static_cast<int32_t>(c[3]));
-    else if (BITS == 4)
-        *reinterpret_cast<uint16_t*>(row + coord / 2) = static_cast<uint16_t>(pack_field<4>(c));
-    else
-        row[coord / 4] = static_cast<uint8_t>(pack_field<2>(c));
+    // the low byte of each lane: codes 0..3 in bytes 0..3
+    const uint32_t w = __builtin_amdgcn_perm(p23, p01, 0x06040200u);
+    if (BITS == 8) {
+        *reinterpret_cast<uint32_t*>(row + coord) = w;
+    } else if (BITS == 4) {
+        const uint32_t x = w & 0x0F0F0F0Fu;
+        const uint32_t y = x | (x >> 4);  // byte 0: codes 0, 1; byte 2: codes 2, 3
+        *reinterpret_cast<uint16_t*>(row + coord / 2) =
+            static_cast<uint16_t>(__builtin_amdgcn_perm(0u, y, 0x0C0C0200u));
+    } else {
+        const uint32_t x = w & 0x03030303u;
+        const uint32_t y = x | (x >> 6);  // byte 0: codes 0, 1; byte 2: codes 2, 3
+        row[coord / 4] = static_cast<uint8_t>(y | (y >> 12));
+    }
 }
 
-template <bool MULTI, int BITS>
-__global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g, int64_t d, int64_t ldg,
-                                                     int32_t worker0, const float* __restrict__ wptr,
-                                                     ScaleSet S, const uint8_t* __restrict__ idx,
-                                                     uint32_t key0, uint32_t key1,
-                                                     uint8_t* __restrict__ codes, int64_t ldc, int32_t tpw)
+// Replaces 16-bit lane (j & 1) of *p with code c.
+__device__ __forceinline__ void set_lane16(uint32_t* p, int j, int32_t c)
 {
-    __shared__ float inv_s[kMaxScales];
-    const float W = *wptr;
-    // tables; on the zero path every entry is 0, which makes every code 0
-    const bool zero = zero_path(W, div_rn32(S.s[0], W));
-    float inv0 = 0.0f;
-    if (MULTI) {
-        if (threadIdx.x < S.K)
-            inv_s[threadIdx.x] = zero ? 0.0f : div_rn32(S.s[threadIdx.x], W);
-        __syncthreads();
-    } else {
-        inv0 = zero ? 0.0f : div_rn32(S.s[0], W);
-    }
-    const float s0 = S.s[0];
-    const uint32_t kmax = static_cast<uint32_t>(S.K - 1);
+    const uint32_t u = static_cast<uint32_t>(c) & 0xFFFFu;
+    *p = (j & 1) ? ((*p & 0xFFFFu) | (u << 16)) : ((*p & 0xFFFF0000u) | u);
+}
 
-    // 2-D grid: tile blocks in x, worker rows in y
-    const int32_t r = blockIdx.y;
-    const uint32_t worker = static_cast<uint32_t>(worker0) + static_cast<uint32_t>(r);
-    const float* row = g + static_cast<int64_t>(r) * ldg;
-    uint8_t* out = codes + static_cast<int64_t>(r) * ldc;
+// One tile's inputs for one lane: its A and B gradient quads and, with
+// several scales, their four scale indices each.
+struct TileIn {
+    f32x4 A, B;
+    uint32_t ka, kb;
+};
 
+template <bool MULTI>
+__device__ __forceinline__ TileIn load_tile(const float* __restrict__ row, const uint8_t* __restrict__ idx,
+                                            int64_t a_off)
+{
+    TileIn in;
+    in.A = load_nt(row + a_off);
+    in.B = load_nt(row + a_off + 256);
+    in.ka = MULTI ? *reinterpret_cast<const uint32_t*>(idx + a_off) : 0u;
+    in.kb = MULTI ? *reinterpret_cast<const uint32_t*>(idx + a_off + 256) : 0u;
+    return in;
+}
+
+// The whole tiles of one code row.  inv_t / inv0 hold s_k / W, multiplied by
+// 2^16 when PRE (then s0x = s0 * 2^16 too), so that xs = x * 2^16 comes out of
+// one multiply and one min; without PRE (an entry is above 2^100, or
+// infinite) the 2^16 is applied after the min.  Both give
+// xs = RN(|v| s_k / W) * 2^16 exactly whenever |v| s_k / W is a normal
+// number, and T = floor(xs) = 0 with a zero threshold low half otherwise, so
+// the codes do not depend on PRE.  With one scale the wave's first tile
+// (`first`, if below ntiles) arrives already loaded in `in0`.
+template <bool MULTI, int BITS, bool PRE>
+__device__ __forceinline__ void quantise_tiles(const float* __restrict__ row, uint8_t* __restrict__ out,
+                                               const uint8_t* __restrict__ idx, int64_t ntiles, int64_t first,
+                                               int64_t stride, const TileIn& in0, const float* inv_t, float inv0,
+                                               float s0x, uint32_t kmax, uint32_t worker, uint32_t key0,
+                                               uint32_t key1, int32_t tpw)
+{
     const int lane = threadIdx.x & 63;
     const bool odd = (lane & 1) != 0;
-    // each wave takes `tpw` consecutive tiles, then strides by the grid
-    const int64_t ntiles = d >> 9;
-    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
-    const int64_t wave_id = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + (threadIdx.x >> 6);
-    for (int64_t c0 = wave_id * tpw; c0 < ntiles; c0 += nwaves * tpw) {
+    uint32_t one2 = 0x00010001u;
+    asm("" : "+s"(one2));
+    for (int64_t c0 = first; c0 < ntiles; c0 += stride) {
       const int64_t c1 = c0 + tpw < ntiles ? c0 + tpw : ntiles;
       for (int64_t T = c0; T < c1; ++T) {
         const int64_t a_off = (T << 9) + 4 * lane;
         const int64_t b_off = a_off + 256;
-        const f32x4 A = load_nt(row + a_off);
-        const f32x4 B = load_nt(row + b_off);
-        float v[8] = {A.x, A.y, A.z, A.w, B.x, B.y, B.z, B.w};
+        TileIn in;
+        if (!MULTI && T == first)
+            in = in0;
+        else
+            in = load_tile<MULTI>(row, idx, a_off);
+        float v[8] = {in.A.x, in.A.y, in.A.z, in.A.w, in.B.x, in.B.y, in.B.z, in.B.w};
         float inv[8];
         if (MULTI) {
-            const uint32_t ka = *reinterpret_cast<const uint32_t*>(idx + a_off);
-            const uint32_t kb = *reinterpret_cast<const uint32_t*>(idx + b_off);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                inv[j] = inv_s[min((ka >> (8 * j)) & 0xFFu, kmax)];
-                inv[j + 4] = inv_s[min((kb >> (8 * j)) & 0xFFu, kmax)];
+                inv[j] = inv_t[min((in.ka >> (8 * j)) & 0xFFu, kmax)];
+                inv[j + 4] = inv_t[min((in.kb >> (8 * j)) & 0xFFu, kmax)];
             }
         } else {
 #pragma unroll
@@ -364,16 +381,41 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
         tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 0u, key0,
                                   key1),
                     odd, &a01, &a23, &b01, &b23);
-        float c[8], lf[8];
-        uint32_t t[8];
+        float xs[8];
+        if (PRE) {
+            // every table entry is finite, so |v| * inv is NaN or infinite only
+            // for NaN or infinite v, which quantise to 0 (wave-uniform, rare)
+            bool bad = false;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                xs[j] = fminf(fabsf(v[j]) * inv[j], s0x);
+                bad = bad || __builtin_amdgcn_classf(v[j], kNonFinite);
+            }
+            if (__builtin_expect(__ballot(bad) != 0, 0)) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    xs[j] = __builtin_amdgcn_classf(v[j], kNonFinite) ? 0.0f : xs[j];
+            }
+        } else {
+            // entries may be infinite (0 * inf is NaN): select by class
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                xs[j] = scaled_magnitude(v[j], inv[j], s0x) * 65536.0f;
+        }
+        uint32_t Tw[8];
         bool tie[8];
         bool any_tie = false;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
+            Tw[j] = static_cast<uint32_t>(xs[j]);
             const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
-            c[j] = quantise_hi(v[j], inv[j], s0, h, &tie[j], &t[j], &lf[j]);
+            tie[j] = (Tw[j] & 0xFFFFu) == h;
             any_tie = any_tie || tie[j];
         }
+        uint32_t p[4] = {pair_codes(Tw[0], Tw[1], v[0], v[1], a01, one2),
+                         pair_codes(Tw[2], Tw[3], v[2], v[3], a23, one2),
+                         pair_codes(Tw[4], Tw[5], v[4], v[5], b01, one2),
+                         pair_codes(Tw[6], Tw[7], v[6], v[7], b23, one2)};
         // wave-uniform branch (the DPP exchange needs every lane): draw the
         // low halves from the purpose-1 blocks when any lane has a tie
         if (__builtin_expect(__ballot(any_tie) != 0, 0)) {
@@ -384,13 +426,69 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
             for (int j = 0; j < 8; ++j) {
                 const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
                 if (tie[j])
-                    c[j] = copysignf(lf[j] + (h < (t[j] & 0xFFFFu) ? 1.0f : 0.0f), v[j]);
+                    set_lane16(&p[j >> 1], j, quantise_tie_scaled(v[j], xs[j], Tw[j], h));
             }
         }
-        store_codes4<BITS>(out, a_off, c);
-        store_codes4<BITS>(out, b_off, c + 4);
+        store_pairs<BITS>(out, a_off, p[0], p[1]);
+        store_pairs<BITS>(out, b_off, p[2], p[3]);
       }
     }
+}
+
+template <bool MULTI, int BITS>
+__global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g, int64_t d, int64_t ldg,
+                                                     int32_t worker0, const float* __restrict__ wptr,
+                                                     ScaleSet S, const uint8_t* __restrict__ idx,
+                                                     uint32_t key0, uint32_t key1,
+                                                     uint8_t* __restrict__ codes, int64_t ldc, int32_t tpw)
+{
+    __shared__ float inv_s[kMaxScales];   // s_k / W
+    __shared__ float inv_p[kMaxScales];   // s_k / W * 2^16 when pre
+
+    // 2-D grid: tile blocks in x, worker rows in y; each wave takes `tpw`
+    // consecutive tiles, then strides by the grid
+    const int32_t r = blockIdx.y;
+    const uint32_t worker = static_cast<uint32_t>(worker0) + static_cast<uint32_t>(r);
+    const float* row = g + static_cast<int64_t>(r) * ldg;
+    uint8_t* out = codes + static_cast<int64_t>(r) * ldc;
+    const int64_t ntiles = d >> 9;
+    const int32_t wave_in_block = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t first = (static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave_in_block) * tpw;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (kBlock / 64) * tpw;
+
+    // with one scale the first tile's loads go out before the tables are
+    // formed, so that their latency covers the load of W and the division
+    // (with several scales this measured slower, so there they stay in the
+    // tile loop)
+    TileIn in0 = {};
+    if (!MULTI && first < ntiles)
+        in0 = load_tile<MULTI>(row, idx, (first << 9) + 4 * (threadIdx.x & 63));
+
+    const float W = *wptr;
+    // tables; on the zero path every entry is 0, which makes every code 0
+    const bool zero = zero_path(W, div_rn32(S.s[0], W));
+    // the largest entry is the last scale's; 2^16 times it stays finite
+    const bool pre = zero || div_rn32(S.s_last, W) <= 0x1p100f;
+    float inv0 = 0.0f;
+    if (MULTI) {
+        if (threadIdx.x < S.K) {
+            const float inv = zero ? 0.0f : div_rn32(S.s[threadIdx.x], W);
+            inv_s[threadIdx.x] = inv;
+            inv_p[threadIdx.x] = pre ? inv * 65536.0f : inv;
+        }
+        __syncthreads();
+    } else {
+        inv0 = zero ? 0.0f : div_rn32(S.s[0], W);
+    }
+    const float s0 = S.s[0];
+    const uint32_t kmax = static_cast<uint32_t>(S.K - 1);
+
+    if (pre)
+        quantise_tiles<MULTI, BITS, true>(row, out, idx, ntiles, first, stride, in0, inv_p, inv0 * 65536.0f,
+                                          s0 * 65536.0f, kmax, worker, key0, key1, tpw);
+    else
+        quantise_tiles<MULTI, BITS, false>(row, out, idx, ntiles, first, stride, in0, inv_p, inv0, s0, kmax,
+                                           worker, key0, key1, tpw);
 
     // Coordinates past the last whole tile (fewer than 512): groups of 8
     // contiguous coordinates, one per lane of the first wave of block x = 0.
@@ -415,15 +513,12 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
             } else {
                 // the group's 8 codes fill whole bytes of its own (coordinates
                 // past d have code 0); the packed row holds them
-                float c[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    c[j] = static_cast<float>(code[j]);
                 if (BITS == 4)
-                    *reinterpret_cast<uint32_t*>(out + base / 2) = pack_field<4>(c) | (pack_field<4>(c + 4) << 16);
+                    *reinterpret_cast<uint32_t*>(out + base / 2) =
+                        pack_field<4>(code) | (pack_field<4>(code + 4) << 16);
                 else
                     *reinterpret_cast<uint16_t*>(out + base / 4) =
-                        static_cast<uint16_t>(pack_field<2>(c) | (pack_field<2>(c + 4) << 8));
+                        static_cast<uint16_t>(pack_field<2>(code) | (pack_field<2>(code + 4) << 8));
             }
         }
     }

@@ -160,7 +160,7 @@ def test_non_finite_inputs_take_zero_path(bad):
         assert_matches_oracle(res, host, d, scales, seed=1)
 
 
-@pytest.mark.parametrize("W", [0.0, -1.0, np.inf, np.nan, 1e-45, 3e-38])
+@pytest.mark.parametrize("W", [0.0, -1.0, np.inf, np.nan, 1e-45, 3e-38, 1e-33, 5e-30])
 def test_forced_scale_values(W):
     """Stages after the norm with a caller-chosen W, including the zero path
     and W small enough that the larger scales' reciprocals overflow."""
@@ -180,6 +180,47 @@ def test_forced_scale_values(W):
         ref = O.pipeline(host, scales, 3, d=d, W=np.float32(W))
         assert np.array_equal(step.codes[:, :d].cpu().numpy(), ref["codes"])
         assert np.array_equal(step.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
+@pytest.mark.parametrize("tiny", [1e-32, 1e-36])
+def test_tiny_norms(tiny):
+    """Rows so small that s_k / W exceeds 2^100: the quantiser then applies
+    its 2^16 scaling after the clamp instead of folding it into the tables."""
+    d, M = 5000, 3
+    host = synth.mixed_rows(M, d, seed=9, ldg=5056) * np.float32(tiny)
+    for scales in (S_SINGLE, [7.0], S_MULTI4):
+        res, _, _ = gpu_step(host, d, scales, seed=4)
+        assert np.isfinite(res["W"]) and scales[-1] / float(res["W"]) > 2.0 ** 100
+        assert_matches_oracle(res, host, d, scales, seed=4)
+
+
+@pytest.mark.parametrize("W", [1.0, 1e-33])
+def test_non_finite_values_with_given_scale(W):
+    """With a caller-given finite W, NaN and infinite coordinates get code 0
+    and the others their usual codes (a tile with and one without them)."""
+    d, M = 3000, 2
+    host = synth.gaussian_rows(M, d, seed=11, ldg=3008)
+    host[0, [5, 700, 2999]] = [np.inf, np.nan, -np.inf]
+    host[1, [0, 511, 1500]] = [-np.nan, np.inf, np.nan]
+    g = torch.from_numpy(host).to(DEV)
+    for scales in (S_SINGLE, S_MULTI4):
+        step = Step(d, M, scales, device=DEV)
+        step.w.fill_(float(W))
+        idx_host = None
+        if len(scales) > 1:
+            idx_host = O.scale_index_shared(np.nan_to_num(host, nan=0.0, posinf=0.0, neginf=0.0), np.float32(W),
+                                            scales, d=d)
+            step.idx[:d].copy_(torch.from_numpy(idx_host))
+        step.quantize(g, seed=5)
+        step.sum_codes()
+        step.dequantize()
+        torch.cuda.synchronize()
+        codes = np.stack([O.quantize(host[m, :d], np.float32(W), scales, 5, worker=m, idx=idx_host)
+                          for m in range(M)])
+        assert codes[0, 700] == 0 and codes[1, 511] == 0
+        assert np.array_equal(step.codes[:, :d].cpu().numpy(), codes)
+        out = O.dequantize(O.sum_codes(codes), M, np.float32(W), scales, idx_host)
+        assert np.array_equal(step.out[:d].cpu().numpy().view(np.int32), out.view(np.int32))
 
 
 def test_index_entries_beyond_K_read_as_last():
