@@ -149,11 +149,35 @@ __device__ __forceinline__ float usable_or_zero(float v)
     return a <= kFloatMax ? a : 0.0f;  // NaN compares false -> 0
 }
 
+// Largest usable |g| over the M rows at quad q.
+__device__ __forceinline__ f32x4 rows_amax(const float* __restrict__ g, int64_t q, int32_t M, int64_t ldg)
+{
+    f32x4 amax = {0.0f, 0.0f, 0.0f, 0.0f};
+    const float* p = g + (q << 2);
+    for (int32_t m = 0; m < M; ++m) {
+        const f32x4 v = load_nt(p + static_cast<int64_t>(m) * ldg);
+        amax.x = fmaxf(amax.x, usable_or_zero(v.x));
+        amax.y = fmaxf(amax.y, usable_or_zero(v.y));
+        amax.z = fmaxf(amax.z, usable_or_zero(v.z));
+        amax.w = fmaxf(amax.w, usable_or_zero(v.w));
+    }
+    return amax;
+}
+
 __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, int64_t d, int32_t M,
                                                   int64_t ldg, const float* __restrict__ wptr,
                                                   ScaleSet S, uint8_t* __restrict__ idx)
 {
     __shared__ float inv_s[kMaxScales];
+    const int64_t nquad = d >> 2;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    // the maxima do not need W: the first quad's loads go out before the
+    // tables are formed
+    f32x4 amax0 = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (first < nquad)
+        amax0 = rows_amax(g, first, M, ldg);
+
     const float W = *wptr;
     if (threadIdx.x < S.K)
         inv_s[threadIdx.x] = div_rn32(S.s[threadIdx.x], W);
@@ -168,18 +192,8 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
     const float s0 = S.s[0];
     const int32_t K = S.K;
 
-    const int64_t nquad = d >> 2;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nquad; q += stride) {
-        float4 amax = make_float4(0.f, 0.f, 0.f, 0.f);
-        const float* p = g + (q << 2);
-        for (int32_t m = 0; m < M; ++m) {
-            const f32x4 v = load_nt(p + static_cast<int64_t>(m) * ldg);
-            amax.x = fmaxf(amax.x, usable_or_zero(v.x));
-            amax.y = fmaxf(amax.y, usable_or_zero(v.y));
-            amax.z = fmaxf(amax.z, usable_or_zero(v.z));
-            amax.w = fmaxf(amax.w, usable_or_zero(v.w));
-        }
+    for (int64_t q = first; q < nquad; q += stride) {
+        const f32x4 amax = q == first ? amax0 : rows_amax(g, q, M, ldg);
         const uint32_t packed = index_of(amax.x, inv, K, s0, zero) |
                                 (index_of(amax.y, inv, K, s0, zero) << 8) |
                                 (index_of(amax.z, inv, K, s0, zero) << 16) |
@@ -666,6 +680,18 @@ __global__ __launch_bounds__(kBlock) void k_dequant(const int32_t* __restrict__ 
                                                     const uint8_t* __restrict__ idx, float* __restrict__ out)
 {
     __shared__ float deq_s[kMaxScales];
+    const int64_t nquad = d >> 2;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    // the first quad's loads go out before the tables are formed
+    i32x4 s_first = {0, 0, 0, 0};
+    uint32_t k_first = 0u;
+    if (first < nquad) {
+        s_first = load_nt(sum + (first << 2));
+        if (MULTI)
+            k_first = *reinterpret_cast<const uint32_t*>(idx + (first << 2));
+    }
+
     const float W = *wptr;
     const float inv0 = div_rn32(S.s[0], W);
     const bool zero = zero_path(W, inv0);
@@ -678,13 +704,19 @@ __global__ __launch_bounds__(kBlock) void k_dequant(const int32_t* __restrict__ 
     const int32_t kmax = S.K - 1;
     const float deq0 = deq_s[0];
 
-    const int64_t nquad = d >> 2;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nquad; q += stride) {
-        const i32x4 s = load_nt(sum + (q << 2));
+    for (int64_t q = first; q < nquad; q += stride) {
+        i32x4 s;
+        uint32_t kk = 0u;
+        if (q == first) {
+            s = s_first;
+            kk = k_first;
+        } else {
+            s = load_nt(sum + (q << 2));
+            if (MULTI)
+                kk = *reinterpret_cast<const uint32_t*>(idx + (q << 2));
+        }
         f32x4 o;
         if (MULTI) {
-            const uint32_t kk = *reinterpret_cast<const uint32_t*>(idx + (q << 2));
             const int32_t k0 = min(static_cast<int32_t>(kk & 0xFFu), kmax);
             const int32_t k1 = min(static_cast<int32_t>((kk >> 8) & 0xFFu), kmax);
             const int32_t k2 = min(static_cast<int32_t>((kk >> 16) & 0xFFu), kmax);
