@@ -13,6 +13,8 @@ Prints one JSON line.  Extra modes:
   --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
+  --stream-probe        achievable bandwidth of the hot path's access patterns
+                        with no work, on the workload's gradients
 """
 import argparse
 import hashlib
@@ -77,6 +79,49 @@ def measured_traffic(kernel: str, workload: str):
     return float(m.group(1))
 
 
+def stream_probe(workload: str, reps: int) -> None:
+    """Achievable bandwidth of the hot path's two access patterns with no work,
+    on the workload's gradient buffer: the norm pass (read M*d floats) and the
+    quantiser (read M*d floats, write M*d bytes).  Kernels from libuq_probe.so,
+    timed back to back between events."""
+    import ctypes
+
+    import torch
+
+    import synth
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2109_12497_amd", "libuq_probe.so"))
+    P, i64 = ctypes.c_void_p, ctypes.c_int64
+    lib.uqp_read.argtypes = [P, i64, P, P]
+    lib.uqp_read_write8.argtypes = [P, i64, P, P]
+    lib.uqp_read_out_floats.argtypes = [i64]
+    lib.uqp_read_out_floats.restype = i64
+    g, cfg = synth.make_gradients(workload, device="cuda")
+    n = g.numel() // 512 * 512
+    codes = torch.empty(n, dtype=torch.uint8, device="cuda")
+    out = torch.empty(int(lib.uqp_read_out_floats(n)), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    h = stream.cuda_stream
+
+    def timed(fn):
+        for _ in range(max(20, reps // 4)):
+            assert fn() == 0
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+
+    t_r = timed(lambda: lib.uqp_read(g.data_ptr(), n, out.data_ptr(), h))
+    t_rw = timed(lambda: lib.uqp_read_write8(g.data_ptr(), n, codes.data_ptr(), h))
+    print(json.dumps({"stream_probe": workload, "elements": n,
+                      "read_GBps": round(4 * n / t_r / 1e9, 1), "read_us": round(t_r * 1e6, 2),
+                      "read4_write1_GBps": round(5 * n / t_rw / 1e9, 1), "read4_write1_us": round(t_rw * 1e6, 2)}))
+
+
 def copy_probe(nbytes: int) -> None:
     import torch
 
@@ -134,21 +179,27 @@ def bench_randk(args, g, cfg) -> int:
         replay()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    stages = ["select", "gather", "aggregate", "scatter"]
-    ev = {s: [] for s in stages}
-
+    # per-stage times: each stage repeated back to back between two events
     def mark():
         e = torch.cuda.Event(enable_timing=True)
         e.record(stream)
         return e
 
-    for _ in range(args.steps):
-        a = mark(); st.select(seed); b = mark(); st.gather(g); c = mark()
-        st.inner.run(st.sub, seed); e = mark(); st.scatter(); f = mark()
-        ev["select"].append((a, b)); ev["gather"].append((b, c)); ev["aggregate"].append((c, e))
-        ev["scatter"].append((e, f))
-    torch.cuda.synchronize()
-    stage_ms = {s: round(sum(x.elapsed_time(y) for x, y in ev[s]) / args.steps, 4) for s in stages}
+    def stage_time(fn, reps):
+        fn()
+        a = mark()
+        for _ in range(reps):
+            fn()
+        b = mark()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    reps = max(10, args.steps)
+    stage_ms = {"select": stage_time(lambda: st.select(seed), reps),
+                "gather": stage_time(lambda: st.gather(g), reps),
+                "aggregate": stage_time(lambda: st.inner.run(st.sub, seed), reps),
+                "scatter": stage_time(lambda: st.scatter(), reps)}
+    stage_ms = {k: round(v, 4) for k, v in stage_ms.items()}
     print(json.dumps({
         "metric": METRIC, "value": round(M * d * args.steps / elapsed / 1e9, 3), "unit": "G elements/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -173,6 +224,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work to aim for")
     ap.add_argument("--copy-probe", type=int, default=0)
+    ap.add_argument("--stream-probe", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of the step captured in a HIP graph instead of host launches")
     args = ap.parse_args()
@@ -191,6 +243,9 @@ def main() -> int:
         return 1
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return 0
+    if args.stream_probe:
+        stream_probe(args.workload, max(10, args.steps))
         return 0
 
     import synth
@@ -230,43 +285,33 @@ def main() -> int:
     ms_per_step = elapsed / args.steps * 1e3
     value = M * d * args.steps / elapsed / 1e9
 
-    # -- per-stage times: the same steps again with events between stages ---
-    stages = ["shared_scale", "quantize", "sum", "dequantize"]
-    ev = {s: [] for s in stages}
-
+    # -- per-stage times: each stage repeated back to back between two events
+    # on the stream (its inputs are the previous stage's outputs, already in
+    # place), so host launch overhead does not enter the figures
     def mark():
         e = torch.cuda.Event(enable_timing=True)
         e.record(stream)
         return e
 
-    for _ in range(args.steps):
+    def stage_time(fn, reps):
+        fn()
         a = mark()
-        step.shared_scale(g)
+        for _ in range(reps):
+            fn()
         b = mark()
-        ev["shared_scale"].append((a, b))
-        if streamed:
-            for m in range(M):
-                a = mark()
-                step.quantize(g[m:m + 1], seed, rows=1, worker0=m)
-                b = mark()
-                step.sum_codes(rows=1, accumulate=1 if m > 0 else 0)
-                c = mark()
-                ev["quantize"].append((a, b))
-                ev["sum"].append((b, c))
-        else:
-            a = mark()
-            step.quantize(g, seed)
-            b = mark()
-            step.sum_codes()
-            c = mark()
-            ev["quantize"].append((a, b))
-            ev["sum"].append((b, c))
-        a = mark()
-        step.dequantize()
-        b = mark()
-        ev["dequantize"].append((a, b))
-    torch.cuda.synchronize()
-    stage_ms = {s: sum(x.elapsed_time(y) for x, y in ev[s]) / args.steps for s in stages}
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    reps = max(10, args.steps)
+    stage_ms = {"shared_scale": stage_time(lambda: step.shared_scale(g), reps)}
+    if streamed:
+        # one worker row per call, M calls per step
+        stage_ms["quantize"] = M * stage_time(lambda: step.quantize(g[:1], seed, rows=1), reps)
+        stage_ms["sum"] = M * stage_time(lambda: step.sum_codes(rows=1, accumulate=1), reps)
+    else:
+        stage_ms["quantize"] = stage_time(lambda: step.quantize(g, seed), reps)
+        stage_ms["sum"] = stage_time(lambda: step.sum_codes(), reps)
+    stage_ms["dequantize"] = stage_time(lambda: step.dequantize(), reps)
     nbytes = algorithmic_bytes(d, M, K, streamed, bits)
 
     # -- dominant kernel (the quantiser): launches back to back between two
@@ -315,6 +360,8 @@ def main() -> int:
     if not args.no_cpu_baseline:
         base, ref, dn = cpu_baseline(g, cfg, args.cpu_budget)
         result["cpu_baseline"] = base
+        step.run(g, seed)  # one whole step, after the stage timings
+        torch.cuda.synchronize()
         # the oracle ran on the same inputs: compare what it covers (free parity check)
         W = np.float32(step.w[0].item())
         if dn == d and not streamed:

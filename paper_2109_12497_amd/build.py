@@ -13,6 +13,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, f) for f in ("uq_kernels.hip", "uq_randk.hip", "uq_abi.hip")]
 LIB_PATH = os.path.join(HERE, "libuq.so")
+# achievable-bandwidth references used by the benchmark (not part of libuq)
+PROBE_SOURCES = [os.path.join(CSRC, "uq_probe.hip")]
+PROBE_LIB_PATH = os.path.join(HERE, "libuq_probe.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",
@@ -31,10 +34,10 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
+def _hipcc(sources, out, verbose):
     hipcc = os.environ.get("HIPCC", "hipcc")
-    tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, *SOURCES, "-o", tmp]
+    tmp = out + ".tmp"
+    cmd = [hipcc, *HIPCC_FLAGS, *sources, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     log = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if noise not in l)
@@ -42,8 +45,14 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{' '.join(cmd)}\n{log}")
     if verbose and log.strip():
         print(log, file=sys.stderr)
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Builds libuq.so (the product library) and libuq_probe.so."""
+    _hipcc(PROBE_SOURCES, PROBE_LIB_PATH, verbose)
+    return _hipcc(SOURCES, LIB_PATH, verbose)
 
 
 if __name__ == "__main__":

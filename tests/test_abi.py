@@ -39,6 +39,23 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_probe_library_is_separate():
+    """The bandwidth-probe kernels live in their own library: libuq does not
+    export them, libuq_probe.so does, and its argument checks need no GPU."""
+    import os
+
+    lib = ctypes.CDLL(uq.LIB_PATH)
+    probe = ctypes.CDLL(os.path.join(os.path.dirname(uq.LIB_PATH), "libuq_probe.so"))
+    for name in ("uqp_read", "uqp_read_write8", "uqp_read_out_floats"):
+        assert hasattr(probe, name) and not hasattr(lib, name), name
+    probe.uqp_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    probe.uqp_read_out_floats.argtypes = [ctypes.c_int64]
+    probe.uqp_read_out_floats.restype = ctypes.c_int64
+    assert probe.uqp_read(None, 512, None, None) == -1
+    assert probe.uqp_read(16, 500, 16, None) == -1   # not a multiple of 512
+    assert probe.uqp_read_out_floats(512) == 256
+
+
 def test_strerror_and_workspace():
     assert uq.uq_strerror(0) == "success"
     for status in (-1, -2, -3, -4, -5):
