@@ -77,13 +77,24 @@ def test_small_shapes(d, scales):
     assert_matches_oracle(res, host, d, scales, seed=1000 + d)
 
 
-@pytest.mark.parametrize("M", [1, 2, 5, 16])
+@pytest.mark.parametrize("M", [1, 2, 5, 16, 300])
 def test_worker_counts(M):
     d = 12_345
     host = synth.gaussian_rows(M, d, seed=M, ldg=synth.round_up(d, 64))
     for scales in (S_SINGLE, S_MULTI4):
         res, _, _ = gpu_step(host, d, scales, seed=77)
         assert_matches_oracle(res, host, d, scales, seed=77)
+
+
+@pytest.mark.parametrize("d", [7, 600])
+def test_max_rows(d):
+    """The largest row count the ABI accepts (the grid's y extent): every
+    worker id up to 65534 enters the random stream."""
+    M = 65535
+    host = synth.gaussian_rows(M, d, seed=d, ldg=64 * ((d + 63) // 64))
+    for scales in (S_SINGLE, S_MULTI4):
+        res, _, _ = gpu_step(host, d, scales, seed=99)
+        assert_matches_oracle(res, host, d, scales, seed=99)
 
 
 def test_seed_high_word_and_worker_offset():
@@ -331,3 +342,32 @@ def test_student_t_streamed_sampled_parity():
     device_norm_check(g, d, np.float32(step.w[0].item()))
     check_windows(step, g, d, scales, seed, sample_windows(d, n_windows=8, seed=5), streamed=True)
     assert int(step.sum[:d].abs().max()) <= M * scales[0]
+
+
+def test_rows_longer_than_2_pow_31():
+    """d = 2^31 + 777 coordinates per row (64-bit indexing, grid caps, Philox
+    counters above 2^28): oracle windows around 2^31 and at the ragged end,
+    W against a float64 norm, and the integer sum over every coordinate."""
+    d, M = (1 << 31) + 777, 2
+    scales = S_MULTI4
+    ldg = synth.round_up(d, 64)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(31)
+    g = torch.zeros((M, ldg), dtype=torch.float32, device=DEV)
+    for m in range(M):
+        for c in range(0, d, 1 << 28):
+            n = min(1 << 28, d - c)
+            g[m, c:c + n].normal_(0.0, 1e-3, generator=gen)
+    g[1, (1 << 31) + 5] = 0.25  # a large coordinate past 2^31 sets the shared index there
+    step = Step(d, M, scales, device=DEV)
+    step.run(g, 4321)
+    torch.cuda.synchronize()
+    device_norm_check(g, d, np.float32(step.w[0].item()))
+    w = 1 << 14
+    windows = [(0, w), ((1 << 31) - w // 2, w), ((1 << 31) + 1, w), (d - w, w), ((1 << 30) + 12345, w)]
+    check_windows(step, g, d, scales, 4321, windows, streamed=False)
+    for c in range(0, d, 1 << 28):
+        e = min(d, c + (1 << 28))
+        assert torch.equal(step.codes[:, c:e].to(torch.int32).sum(dim=0), step.sum[c:e]), c
+    del g, step
+    torch.cuda.empty_cache()
