@@ -183,7 +183,7 @@ int uq_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, i
  * sampled coordinates (the paper's K), not a number of scales.
  * ------------------------------------------------------------------------ */
 
-/* Workspace bytes uq_randk_select needs (a fixed size, about 96 KiB). */
+/* Workspace bytes uq_randk_select needs (a fixed size, about 4.3 MiB). */
 size_t uq_randk_workspace_bytes(int64_t d, int64_t K);
 
 /*
@@ -196,9 +196,10 @@ size_t uq_randk_workspace_bytes(int64_t d, int64_t K);
  *   K      1 <= K <= d
  *   sel    [K] uint32 (written), 16-byte aligned
  *   ws     device workspace of uq_randk_workspace_bytes(d, K) bytes
- * The boundary search keeps at most 4096 keys that share the K-th key's top
- * 24 bits (about d / 2^24 are expected); more would make the result wrong,
- * which pseudo-random keys do not produce for any d < 2^32.
+ * The boundary search keeps at most 8192 keys that share the K-th key's top
+ * 20 bits (about d / 2^20 are expected, at most 4096 with a standard
+ * deviation of 64); more would make the result wrong, which pseudo-random
+ * keys do not produce for any d < 2^32.
  */
 int uq_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, size_t ws_bytes,
                     void* stream);

@@ -42,9 +42,10 @@ hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int
                              int32_t accumulate, int32_t* sum, hipStream_t stream);
 hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,
                       int32_t* sum, hipStream_t stream);
-// GlobalRandK: at most kRandkCandidates keys sharing the threshold's 24-bit
-// prefix are kept (expected d / 2^24; d < 2^32).
-constexpr int kRandkCandidates = 4096;
+// GlobalRandK: at most kRandkCandidates keys sharing the threshold's 20-bit
+// prefix are kept (expected d / 2^20 <= 4096 for d < 2^32, standard deviation
+// 64 at most).
+constexpr int kRandkCandidates = 8192;
 
 size_t randk_workspace_bytes();
 hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, hipStream_t stream);

@@ -7,18 +7,24 @@
 // Philox block (i/4, 0, purpose 2), lo the same word of block (i/4, 0,
 // purpose 3).  The K coordinates with the smallest (hi, lo, i) are chosen.
 // Keys are regenerated in every pass (no key array in memory):
-//   1. per-block LDS histograms of hi >> 20 (4096 bins), merged with atomics;
-//   2. one block finds the bin b1 holding the K-th key and how many keys of
-//      it are still needed;
-//   3. keys in bin b1 histogram (hi >> 8) & 0xFFF (sparse global atomics);
-//   4. one block finds the sub-bin b2;
-//   5. keys whose top 24 bits are (b1, b2) are collected with their low
-//      words (expected d / 2^24 of them, at most kRandkCandidates);
-//   6. one block ranks the candidates and takes the (key, index) threshold;
-//   7. the coordinates at or below the threshold (exactly K) are written in
-//      increasing order: contiguous per-block ranges are counted, the counts
-//      scanned, and each block then writes its selections at its offset,
-//      ordered inside the block by wave ballots.
+//   1. per-block LDS histograms of hi >> 24 (256 bins), merged with atomics;
+//   2. every block of the next pass finds the bin b1 holding the K-th key
+//      (and how many of its keys are still needed) from that histogram, and
+//      keys in bin b1 histogram (hi >> 12) & 0xFFF (global atomics);
+//   3. one block finds the sub-bin b2;
+//   4. keys whose top 20 bits are (b1, b2) are collected with their low
+//      words (expected d / 2^20 of them, at most kRandkCandidates);
+//   5. one block ranks the candidates and takes the (key, index) threshold;
+//   6. the coordinates at or below the threshold (exactly K) are output in
+//      increasing order.  For K <= kRkSortMax each wave appends its
+//      selections to one of kRkShards staging lists (one atomic per wave
+//      with selections, spread over the shards' counters: device-scope
+//      atomics on one address serialise) and one block sorts the lists by
+//      buckets of the index range; for larger K contiguous per-block ranges
+//      are counted, the counts scanned, and each block writes its
+//      selections at its offset, ordered by wave ballots.
+// The key passes run persistent grids, four independent Philox blocks per
+// thread and iteration.
 #include <stdint.h>
 
 #include "uq_device.hpp"
@@ -26,25 +32,36 @@
 
 namespace uq {
 
-constexpr int kRkBins = 4096;
+constexpr int kRkBins1 = 256;    // level 1: hi >> 24
+constexpr int kRkBins2 = 4096;   // level 2: (hi >> 12) & 0xFFF
 constexpr int kRkSortThreads = 1024;
+constexpr int kRkSortMax = 16384;  // largest K sorted by one block
+constexpr int kRkShards = 64;      // staging lists of the K <= kRkSortMax path
+constexpr int kRkUnroll = 4;       // Philox blocks per thread and iteration
+constexpr int kRkCopies = 16;      // level-1 histogram copies the blocks merge into
+constexpr int kRkLine = 64;        // uint32 per 256-byte line: one atomic counter per line
 
 struct RandkControl {
     uint32_t b1, need1, b2, need2;  // bins found by the two scans
-    uint32_t n_cand, n_sel;         // append counters
+    uint32_t n_cand, pad0;          // candidate append counter
     uint32_t thr_hi, thr_lo, thr_idx;
     uint32_t pad[7];
 };
 
 constexpr int kRkMaxBlocks = 2048;  // ordered-compaction blocks
 
+// Device-scope atomics execute at the memory side and serialise per cache
+// line, so counters that many waves hit live on lines of their own and the
+// level-1 histogram is merged into kRkCopies copies.
 struct RandkWorkspace {
-    uint32_t hist1[kRkBins];
-    uint32_t hist2[kRkBins];
+    uint32_t hist1[kRkCopies][kRkBins1];
+    uint32_t hist2[kRkBins2];
     RandkControl ctl;
     uint32_t cand[kRandkCandidates][3];  // (hi, lo, index)
     uint32_t block_count[kRkMaxBlocks];
     uint32_t block_offset[kRkMaxBlocks];
+    uint32_t n_stage[kRkShards][kRkLine];     // staging list lengths (element 0 of each line)
+    uint32_t stage[kRkShards][kRkSortMax];    // unordered selections (K <= kRkSortMax)
 };
 
 __device__ __forceinline__ uint4 selection_block(uint32_t q, uint32_t purpose, uint32_t key0, uint32_t key1)
@@ -57,107 +74,183 @@ __device__ __forceinline__ uint32_t word_of(uint4 w, int j)
     return j == 0 ? w.x : (j == 1 ? w.y : (j == 2 ? w.z : w.w));
 }
 
+// Inclusive scan of one value per thread over a block of kBlock threads
+// (scratch: kBlock / 64 words of LDS).
+__device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t x, uint32_t* scratch)
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, 64);
+        if (lane >= off)
+            x += y;
+    }
+    if (lane == 63)
+        scratch[wave] = x;
+    __syncthreads();
+    uint32_t before = 0u;
+    for (int v = 0; v < wave; ++v)
+        before += scratch[v];
+    __syncthreads();  // scratch may be reused by the caller
+    return x + before;
+}
+
+// The bin of hist[0 .. kBlock * PER) where the cumulative count first reaches
+// `need` (1 <= need <= the total), and how many keys of that bin are still
+// needed.  Thread t owns bins [t * PER, (t + 1) * PER); the owner of the
+// crossing writes *bin and *rest.
+template <int PER>
+__device__ __forceinline__ void find_bin(const uint32_t* hist, uint32_t need, uint32_t* scratch, uint32_t* bin,
+                                         uint32_t* rest)
+{
+    uint32_t v[PER];
+    uint32_t s = 0u;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        v[j] = hist[threadIdx.x * PER + j];
+        s += v[j];
+    }
+    const uint32_t incl = block_inclusive_scan(s, scratch);
+    uint32_t cum = incl - s;
+    if (cum < need && need <= incl) {
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            if (cum < need && need <= cum + v[j]) {
+                *bin = static_cast<uint32_t>(threadIdx.x * PER + j);
+                *rest = need - cum;
+            }
+            cum += v[j];
+        }
+    }
+}
+
+static_assert(kRkCopies * kRkBins1 == kRkBins2, "one zeroing loop covers both histograms");
 __global__ __launch_bounds__(kBlock) void k_rk_init(RandkWorkspace* __restrict__ ws)
 {
-    for (int b = threadIdx.x; b < kRkBins; b += kBlock) {
-        ws->hist1[b] = 0u;
+    for (int b = threadIdx.x; b < kRkBins2; b += kBlock) {
+        reinterpret_cast<uint32_t*>(ws->hist1)[b] = 0u;  // kRkCopies * kRkBins1 == kRkBins2
         ws->hist2[b] = 0u;
     }
     if (threadIdx.x < sizeof(RandkControl) / 4)
         reinterpret_cast<uint32_t*>(&ws->ctl)[threadIdx.x] = 0u;
+    if (threadIdx.x < kRkShards)
+        ws->n_stage[threadIdx.x][0] = 0u;
 }
 
-// Pass 1: histogram of the top 12 bits of hi.
+// The kRkUnroll key groups q0 + u * kBlock (u < kRkUnroll) of one thread and
+// iteration; groups at or past nq get an all-zero block and must be skipped.
+__device__ __forceinline__ void key_blocks(int64_t q0, int64_t nq, uint32_t purpose, uint32_t key0, uint32_t key1,
+                                           uint4 w[kRkUnroll])
+{
+#pragma unroll
+    for (int u = 0; u < kRkUnroll; ++u) {
+        const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
+        w[u] = q < nq ? selection_block(static_cast<uint32_t>(q), purpose, key0, key1) : make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+// Pass 1: histogram of the top 8 bits of hi.
+static_assert(kRkBins1 == kBlock, "one level-1 bin per thread");
 __global__ __launch_bounds__(kBlock) void k_rk_hist1(int64_t d, uint32_t key0, uint32_t key1,
                                                      RandkWorkspace* __restrict__ ws)
 {
-    __shared__ uint32_t h[kRkBins];
-    for (int b = threadIdx.x; b < kRkBins; b += kBlock)
-        h[b] = 0u;
+    __shared__ uint32_t h[kRkBins1];
+    h[threadIdx.x] = 0u;
     __syncthreads();
     const int64_t nq = (d + 3) >> 2;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nq;
-         q += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock * kRkUnroll;
+    for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kBlock * kRkUnroll + threadIdx.x; q0 < nq; q0 += step) {
+        uint4 w[kRkUnroll];
+        key_blocks(q0, nq, 2u, key0, key1, w);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if ((q << 2) + j < d)
-                atomicAdd(&h[word_of(w, j) >> 20], 1u);
-    }
-    __syncthreads();
-    for (int b = threadIdx.x; b < kRkBins; b += kBlock)
-        if (h[b] != 0u)
-            atomicAdd(&ws->hist1[b], h[b]);
-}
-
-// Scans (one block): the bin whose cumulative count first reaches `need`.
-__global__ __launch_bounds__(kBlock) void k_rk_scan(RandkWorkspace* __restrict__ ws, int level, uint32_t K)
-{
-    __shared__ uint32_t part[kBlock];
-    const uint32_t* hist = level == 1 ? ws->hist1 : ws->hist2;
-    const uint32_t need = level == 1 ? K : ws->ctl.need1;
-    constexpr int per = kRkBins / kBlock;  // 16 bins per thread
-    uint32_t local = 0u;
+        for (int u = 0; u < kRkUnroll; ++u) {
+            const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
 #pragma unroll
-    for (int j = 0; j < per; ++j)
-        local += hist[threadIdx.x * per + j];
-    part[threadIdx.x] = local;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t cum = 0u;
-        int t = 0;
-        while (t < kBlock - 1 && cum + part[t] < need)
-            cum += part[t++];
-        int b = t * per;
-        while (b < kRkBins - 1 && cum + hist[b] < need)
-            cum += hist[b++];
-        if (level == 1) {
-            ws->ctl.b1 = static_cast<uint32_t>(b);
-            ws->ctl.need1 = need - cum;
-        } else {
-            ws->ctl.b2 = static_cast<uint32_t>(b);
-            ws->ctl.need2 = need - cum;
+            for (int j = 0; j < 4; ++j)
+                if ((q << 2) + j < d)
+                    atomicAdd(&h[word_of(w[u], j) >> 24], 1u);
         }
     }
+    __syncthreads();
+    if (h[threadIdx.x] != 0u)
+        atomicAdd(&ws->hist1[blockIdx.x % kRkCopies][threadIdx.x], h[threadIdx.x]);
 }
 
-// Pass 2: keys in bin b1 histogram bits 19..8 of hi.
-__global__ __launch_bounds__(kBlock) void k_rk_hist2(int64_t d, uint32_t key0, uint32_t key1,
+// Pass 2: every block finds (b1, need1); keys in bin b1 histogram bits
+// 23..12 of hi.
+__global__ __launch_bounds__(kBlock) void k_rk_hist2(int64_t d, uint32_t K, uint32_t key0, uint32_t key1,
                                                      RandkWorkspace* __restrict__ ws)
 {
-    const uint32_t b1 = ws->ctl.b1;
-    const int64_t nq = (d + 3) >> 2;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nq;
-         q += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+    __shared__ uint32_t scratch[kBlock / 64];
+    __shared__ uint32_t found[2];
+    __shared__ uint32_t hist1[kRkBins1];
+    uint32_t c[kRkCopies];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint32_t hi = word_of(w, j);
-            if ((q << 2) + j < d && (hi >> 20) == b1)
-                atomicAdd(&ws->hist2[(hi >> 8) & 0xFFFu], 1u);
+    for (int k = 0; k < kRkCopies; ++k)
+        c[k] = ws->hist1[k][threadIdx.x];
+    uint32_t total = 0u;
+#pragma unroll
+    for (int k = 0; k < kRkCopies; ++k)
+        total += c[k];
+    hist1[threadIdx.x] = total;
+    __syncthreads();
+    find_bin<1>(hist1, K, scratch, &found[0], &found[1]);
+    __syncthreads();
+    const uint32_t b1 = found[0];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        ws->ctl.b1 = b1;
+        ws->ctl.need1 = found[1];
+    }
+    const int64_t nq = (d + 3) >> 2;
+    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock * kRkUnroll;
+    for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kBlock * kRkUnroll + threadIdx.x; q0 < nq; q0 += step) {
+        uint4 w[kRkUnroll];
+        key_blocks(q0, nq, 2u, key0, key1, w);
+#pragma unroll
+        for (int u = 0; u < kRkUnroll; ++u) {
+            const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t hi = word_of(w[u], j);
+                if ((q << 2) + j < d && (hi >> 24) == b1)
+                    atomicAdd(&ws->hist2[(hi >> 12) & 0xFFFu], 1u);
+            }
         }
     }
 }
 
-// Pass 3: collect the keys whose top 24 bits are (b1, b2), with low words.
+// One block: the level-2 sub-bin b2 holding the need1-th key of bin b1.
+__global__ __launch_bounds__(kBlock) void k_rk_scan2(RandkWorkspace* __restrict__ ws)
+{
+    __shared__ uint32_t scratch[kBlock / 64];
+    find_bin<kRkBins2 / kBlock>(ws->hist2, ws->ctl.need1, scratch, &ws->ctl.b2, &ws->ctl.need2);
+}
+
+// Pass 3: collect the keys whose top 20 bits are (b1, b2), with low words.
 __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0, uint32_t key1,
                                                        RandkWorkspace* __restrict__ ws)
 {
     const uint32_t prefix = (ws->ctl.b1 << 12) | ws->ctl.b2;
     const int64_t nq = (d + 3) >> 2;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nq;
-         q += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock * kRkUnroll;
+    for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kBlock * kRkUnroll + threadIdx.x; q0 < nq; q0 += step) {
+      uint4 wu[kRkUnroll];
+      key_blocks(q0, nq, 2u, key0, key1, wu);
+#pragma unroll
+      for (int u = 0; u < kRkUnroll; ++u) {
+        const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
+        const uint4 w = wu[u];
         bool any = false;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            any = any || (((q << 2) + j < d) && (word_of(w, j) >> 8) == prefix);
+            any = any || (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix);
         if (any) {
             const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int64_t i = (q << 2) + j;
-                if (i < d && (word_of(w, j) >> 8) == prefix) {
+                if (i < d && (word_of(w, j) >> 12) == prefix) {
                     const uint32_t slot = atomicAdd(&ws->ctl.n_cand, 1u);
                     if (slot < static_cast<uint32_t>(kRandkCandidates)) {
                         ws->cand[slot][0] = word_of(w, j);
@@ -167,6 +260,7 @@ __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0,
                 }
             }
         }
+      }
     }
 }
 
@@ -177,7 +271,7 @@ __device__ __forceinline__ bool key_less(uint32_t ah, uint32_t al, uint32_t ai, 
 }
 
 // One block: the candidate whose rank among the candidates (by hi, lo,
-// index; all distinct) is need2 - 1 is the threshold.  About d / 2^24
+// index; all distinct) is need2 - 1 is the threshold.  About d / 2^20
 // candidates are expected, so a direct count of smaller keys is cheapest.
 __global__ __launch_bounds__(kRkSortThreads) void k_rk_threshold(RandkWorkspace* __restrict__ ws)
 {
@@ -220,8 +314,204 @@ __device__ __forceinline__ uint32_t selected_mask(int64_t q, int64_t d, uint32_t
     return mask;
 }
 
-// Block b owns coordinates [b * chunk, (b + 1) * chunk): pass 4 counts its
-// selections, pass 5 writes them in order at the scanned offset.
+// Whether coordinate i = 4q + j is selected, from the hi words of its group
+// (the lo words are drawn only when a hi word equals the threshold's).
+__device__ __forceinline__ uint32_t selected_mask_hi(uint4 w, int64_t q, int64_t d, uint32_t key0, uint32_t key1,
+                                                     uint32_t th, uint32_t tl, uint32_t ti)
+{
+    bool tie = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        tie = tie || (((q << 2) + j < d) && word_of(w, j) == th);
+    uint4 l = make_uint4(0u, 0u, 0u, 0u);
+    if (tie)
+        l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
+    uint32_t mask = 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t i = (q << 2) + j;
+        const uint32_t hi = word_of(w, j);
+        const bool take = i < d && (hi < th || (hi == th && !key_less(th, tl, ti, hi, word_of(l, j),
+                                                                       static_cast<uint32_t>(i))));
+        mask |= take ? (1u << j) : 0u;
+    }
+    return mask;
+}
+
+// K <= kRkSortMax: every wave appends its selections (any order) to staging
+// list (wave id mod kRkShards) with one atomic on that list's length.  Each
+// list has room for all K selections, so none can overflow.
+__global__ __launch_bounds__(kBlock) void k_rk_pick(int64_t d, uint32_t key0, uint32_t key1,
+                                                    RandkWorkspace* __restrict__ ws, uint32_t K)
+{
+    const uint32_t th = ws->ctl.thr_hi, tl = ws->ctl.thr_lo, ti = ws->ctl.thr_idx;
+    const int lane = threadIdx.x & 63;
+    const uint64_t below = (uint64_t(1) << lane) - 1u;
+    const uint32_t shard = (blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) % kRkShards;
+    uint32_t* list = ws->stage[shard];
+    const int64_t nq = (d + 3) >> 2;
+    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock * kRkUnroll;
+    for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kBlock * kRkUnroll + threadIdx.x; q0 < nq; q0 += step) {
+        uint4 w[kRkUnroll];
+        key_blocks(q0, nq, 2u, key0, key1, w);
+#pragma unroll
+        for (int u = 0; u < kRkUnroll; ++u) {
+            const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
+            const uint32_t mask = q < nq ? selected_mask_hi(w[u], q, d, key0, key1, th, tl, ti) : 0u;
+            uint32_t before = 0u, total = 0u;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint64_t b = __ballot((mask >> j) & 1u);
+                before += __popcll(b & below);
+                total += __popcll(b);
+            }
+            if (total == 0u)
+                continue;  // wave-uniform
+            uint32_t base = 0u;
+            if (lane == 0)
+                base = atomicAdd(&ws->n_stage[shard][0], total);
+            base = __shfl(base, 0, 64);
+            uint32_t pos = base + before;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if ((mask >> j) & 1u) {
+                    if (pos < K)  // at most K in all lists together; the guard keeps writes in bounds
+                        list[pos] = static_cast<uint32_t>((q << 2) + j);
+                    ++pos;
+                }
+        }
+    }
+}
+
+constexpr int kRkBuckets = 4 * kRkSortThreads;  // buckets of the index range in the sort
+
+// Bucket of index i < d among kRkBuckets equal parts of [0, d): a monotone
+// map, clamped so that no index can address outside the counters.
+__device__ __forceinline__ uint32_t bucket_of(uint32_t i, double scale)
+{
+    const uint32_t b = static_cast<uint32_t>(static_cast<double>(i) * scale);
+    return b < kRkBuckets ? b : kRkBuckets - 1u;
+}
+
+// One block: the K staged indices in increasing order.  The staging lists
+// are concatenated (thread t holds positions t, t + 1024, ...), the indices
+// binned into kRkBuckets buckets of the index range through LDS counters
+// (about K / kRkBuckets indices each), and every index is written at its
+// bucket's start plus its rank inside the bucket.
+__global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace* __restrict__ ws,
+                                                            uint32_t* __restrict__ sel, uint32_t K, int64_t d)
+{
+    constexpr int kPer = kRkSortMax / kRkSortThreads;  // 16 items per thread
+    constexpr int kBPer = kRkBuckets / kRkSortThreads;  // 4 buckets per thread
+    __shared__ uint32_t buf[kRkSortMax];
+    __shared__ uint32_t count[kRkBuckets];
+    __shared__ uint32_t start[kRkBuckets];
+    __shared__ uint32_t scratch[kRkSortThreads / 64];
+    __shared__ uint32_t list_start[kRkShards + 1];
+    const uint32_t t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+#pragma unroll
+    for (int k = 0; k < kBPer; ++k)
+        count[t * kBPer + k] = 0u;
+    static_assert(kRkShards == 64, "one wave scans the list lengths");
+    if (wave == 0) {
+        const uint32_t len = ws->n_stage[lane][0];
+        uint32_t x = len;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(x, off, 64);
+            if (lane >= off)
+                x += y;
+        }
+        list_start[lane] = x - len;
+        if (lane == 63)
+            list_start[kRkShards] = x;
+    }
+    __syncthreads();
+    // this thread's items, all loads issued before any is used
+    uint32_t item[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+        const uint32_t j = t + r * kRkSortThreads;
+        uint32_t v = 0u;
+        if (j < K) {
+            // the list holding concatenated position j
+            int lo = 0, hi = kRkShards;  // list_start[lo] <= j < list_start[hi]
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (list_start[mid] <= j)
+                    lo = mid;
+                else
+                    hi = mid;
+            }
+            v = ws->stage[lo][j - list_start[lo]];
+        }
+        item[r] = v;
+    }
+    const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
+    uint32_t bucket[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+        bucket[r] = bucket_of(item[r], scale);
+        if (t + r * kRkSortThreads < K)
+            atomicAdd(&count[bucket[r]], 1u);
+    }
+    __syncthreads();
+    // exclusive scan of the bucket counts (thread t owns buckets 4t .. 4t+3)
+    uint32_t c[kBPer];
+    uint32_t own = 0u;
+#pragma unroll
+    for (int k = 0; k < kBPer; ++k) {
+        c[k] = count[t * kBPer + k];
+        own += c[k];
+    }
+    uint32_t x = own;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, 64);
+        if (lane >= off)
+            x += y;
+    }
+    if (lane == 63)
+        scratch[wave] = x;
+    __syncthreads();
+    uint32_t run = x - own;
+    for (int v = 0; v < wave; ++v)
+        run += scratch[v];
+#pragma unroll
+    for (int k = 0; k < kBPer; ++k) {
+        start[t * kBPer + k] = run;
+        run += c[k];
+        count[t * kBPer + k] = 0u;  // reused as the bucket's fill cursor
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kPer; ++r)
+        if (t + r * kRkSortThreads < K) {
+            const uint32_t p = start[bucket[r]] + atomicAdd(&count[bucket[r]], 1u);
+            if (p < static_cast<uint32_t>(kRkSortMax))
+                buf[p] = item[r];
+        }
+    __syncthreads();
+    // each index goes to its bucket's start plus the number of smaller
+    // indices in its bucket (the indices are distinct)
+#pragma unroll
+    for (int r = 0; r < kPer; ++r)
+        if (t + r * kRkSortThreads < K) {
+            const uint32_t b = bucket[r], s0 = start[b];
+            const uint32_t room = static_cast<uint32_t>(kRkSortMax) - min(s0, static_cast<uint32_t>(kRkSortMax));
+            const uint32_t n = min(count[b], room);
+            uint32_t rank = 0u;
+            for (uint32_t a = 0; a < n; ++a)
+                rank += buf[s0 + a] < item[r] ? 1u : 0u;
+            if (s0 + rank < K)
+                sel[s0 + rank] = item[r];
+        }
+}
+
+// K > kRkSortMax: block b owns coordinates [b * chunk, (b + 1) * chunk); one
+// pass counts its selections, the next writes them in order at the scanned
+// offset.
 __global__ __launch_bounds__(kBlock) void k_rk_count(int64_t d, int64_t chunk, uint32_t key0, uint32_t key1,
                                                      RandkWorkspace* __restrict__ ws)
 {
@@ -242,31 +532,27 @@ __global__ __launch_bounds__(kBlock) void k_rk_count(int64_t d, int64_t chunk, u
         ws->block_count[blockIdx.x] = wave_count[0] + wave_count[1] + wave_count[2] + wave_count[3];
 }
 
-// One block: exclusive scan of the per-block counts.
+// One block: exclusive scan of the per-block counts (thread t owns blocks
+// [t * PER, (t + 1) * PER)).
 __global__ __launch_bounds__(kBlock) void k_rk_offsets(RandkWorkspace* __restrict__ ws, int32_t nblocks)
 {
-    __shared__ uint32_t part[kBlock];
-    const int per = (nblocks + kBlock - 1) / kBlock;
-    const int b0 = threadIdx.x * per;
-    uint32_t local = 0u;
-    for (int b = b0; b < b0 + per && b < nblocks; ++b)
-        local += ws->block_count[b];
-    part[threadIdx.x] = local;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t run = 0u;
-        for (int t = 0; t < kBlock; ++t) {
-            const uint32_t x = part[t];
-            part[t] = run;
-            run += x;
-        }
+    constexpr int PER = kRkMaxBlocks / kBlock;
+    __shared__ uint32_t scratch[kBlock / 64];
+    uint32_t v[PER];
+    uint32_t s = 0u;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int b = threadIdx.x * PER + j;
+        v[j] = b < nblocks ? ws->block_count[b] : 0u;
+        s += v[j];
     }
-    __syncthreads();
-    uint32_t run = part[threadIdx.x];
-    for (int b = b0; b < b0 + per && b < nblocks; ++b) {
-        const uint32_t x = ws->block_count[b];
-        ws->block_offset[b] = run;
-        run += x;
+    uint32_t run = block_inclusive_scan(s, scratch) - s;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int b = threadIdx.x * PER + j;
+        if (b < nblocks)
+            ws->block_offset[b] = run;
+        run += v[j];
     }
 }
 
@@ -355,11 +641,13 @@ size_t randk_workspace_bytes()
     return (sizeof(RandkWorkspace) + 255) / 256 * 256;
 }
 
+// Persistent grid for the key passes: kBlock * kRkUnroll key groups per block
+// and iteration, at most eight blocks per compute unit.
 static unsigned key_grid(int64_t d)
 {
     const int64_t groups = (d + 3) >> 2;
-    int64_t blocks = (groups + kBlock - 1) / kBlock;
-    const int64_t cap = grid_cap();
+    int64_t blocks = (groups + kBlock * kRkUnroll - 1) / (kBlock * kRkUnroll);
+    const int64_t cap = grid_cap() / 8;
     blocks = blocks < 1 ? 1 : (blocks > cap ? cap : blocks);
     return static_cast<unsigned>(blocks);
 }
@@ -369,19 +657,23 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
     RandkWorkspace* ws = static_cast<RandkWorkspace*>(ws_raw);
     const uint32_t key0 = static_cast<uint32_t>(seed);
     const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
-    const unsigned gx = key_grid(d);
+    const unsigned gx = key_grid(d);  // persistent grid for the key passes
     hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws);
-    // the first histogram merges 4096 LDS bins per block into global memory:
-    // few, long-lived blocks keep those atomics to a few per bin
+    // the first histogram merges its LDS bins into global memory: few,
+    // long-lived blocks keep those atomics to a few per bin
     int64_t hist_blocks = grid_cap() / 32;  // two blocks per compute unit
     hist_blocks = hist_blocks > static_cast<int64_t>(gx) ? static_cast<int64_t>(gx) : hist_blocks;
     hipLaunchKernelGGL(k_rk_hist1, dim3(static_cast<unsigned>(hist_blocks)), dim3(kBlock), 0, stream, d, key0, key1,
                        ws);
-    hipLaunchKernelGGL(k_rk_scan, dim3(1), dim3(kBlock), 0, stream, ws, 1, static_cast<uint32_t>(K));
-    hipLaunchKernelGGL(k_rk_hist2, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws);
-    hipLaunchKernelGGL(k_rk_scan, dim3(1), dim3(kBlock), 0, stream, ws, 2, static_cast<uint32_t>(K));
+    hipLaunchKernelGGL(k_rk_hist2, dim3(gx), dim3(kBlock), 0, stream, d, static_cast<uint32_t>(K), key0, key1, ws);
+    hipLaunchKernelGGL(k_rk_scan2, dim3(1), dim3(kBlock), 0, stream, ws);
     hipLaunchKernelGGL(k_rk_collect, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws);
     hipLaunchKernelGGL(k_rk_threshold, dim3(1), dim3(kRkSortThreads), 0, stream, ws);
+    if (K <= kRkSortMax) {
+        hipLaunchKernelGGL(k_rk_pick, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws, static_cast<uint32_t>(K));
+        hipLaunchKernelGGL(k_rk_sort, dim3(1), dim3(kRkSortThreads), 0, stream, ws, sel, static_cast<uint32_t>(K), d);
+        return hipGetLastError();
+    }
     // ordered compaction over contiguous chunks (a multiple of 1024 coordinates)
     const int64_t per_block = 1024;
     int64_t chunk = (d + kRkMaxBlocks - 1) / kRkMaxBlocks;

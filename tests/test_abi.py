@@ -199,7 +199,8 @@ def test_scatter_rejects(kw, want):
 
 def test_randk_workspace_fixed_and_aligned():
     b = uq.uq_randk_workspace_bytes(10 ** 6, 10_000)
-    assert b % 256 == 0 and 32 * 1024 < b < 1024 * 1024
+    assert b % 256 == 0 and 32 * 1024 < b < 8 * 1024 * 1024
+    assert uq.uq_randk_workspace_bytes(2 ** 32 - 1, 2 ** 31) == b
 
 
 # Packed codes ---------------------------------------------------------------

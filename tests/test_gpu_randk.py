@@ -29,6 +29,8 @@ def gpu_select(d, K, seed):
     (1, 1, 0), (2, 1, 5), (5, 5, 1), (7, 3, 2), (100, 99, 3), (1000, 1, 4), (4097, 4096, 5),
     (65_539, 10_000, 6), (1 << 20, 32_768, 7), (1 << 20, 10_000, (1 << 63) + 12345), (300_000, 250_000, 10),
     (3_000_001, 10_000, 8), (11_173_962, 10_000, 9),
+    # both sides of the largest K that one block sorts
+    (100_000, 16_384, 11), (100_000, 16_385, 12),
 ])
 def test_selection_matches_oracle(d, K, seed):
     got = gpu_select(d, K, seed)
