@@ -1,6 +1,7 @@
 // C ABI of libuq: argument checks on the host, then asynchronous launches.
 // Every check completes before the first HIP runtime call, so an invalid
 // call returns its status without touching the device or the runtime.
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -149,19 +150,21 @@ int launched(hipError_t e)
 
 namespace uq {
 
+// 64 blocks per compute unit of the current device (the count is cached per
+// device; concurrent first calls may both query it and store the same value).
 int64_t grid_cap()
 {
-    static int cus_by_device[64] = {0};
+    static std::atomic<int> cus_by_device[64] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
         return 256 * 64;
-    if (cus_by_device[dev] == 0) {
-        int cus = 0;
+    int cus = cus_by_device[dev].load(std::memory_order_relaxed);
+    if (cus == 0) {
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        cus_by_device[dev] = cus;
+        cus_by_device[dev].store(cus, std::memory_order_relaxed);
     }
-    return static_cast<int64_t>(cus_by_device[dev]) * 64;
+    return static_cast<int64_t>(cus) * 64;
 }
 
 }  // namespace uq
