@@ -356,6 +356,78 @@ __device__ __forceinline__ TileIn load_tile(const float* __restrict__ row, const
 // number, and T = floor(xs) = 0 with a zero threshold low half otherwise, so
 // the codes do not depend on PRE.  With one scale the wave's first tile
 // (`first`, if below ntiles) arrives already loaded in `in0`.
+// The eight codes of one lane for tile T of worker `worker`, as four 16-bit
+// lane pairs (A0 A1, A2 A3, B0 B1, B2 B3).  v: the lane's coordinates;
+// inv: their s_k / W, times 2^16 when PRE (then s0x = s0 * 2^16).  Every lane
+// of the wave must call it (DPP exchange, wave-uniform branches).
+template <bool PRE>
+__device__ __forceinline__ void tile_codes(const float v[8], const float inv[8], float s0x, int64_t T,
+                                           uint32_t worker, uint32_t key0, uint32_t key1, uint32_t one2,
+                                           uint32_t p[4])
+{
+    const int lane = threadIdx.x & 63;
+    const bool odd = (lane & 1) != 0;
+    const uint64_t q = static_cast<uint64_t>(T << 6) + static_cast<uint64_t>(lane >> 1) + (odd ? 32u : 0u);
+    uint32_t a01, a23, b01, b23;
+    tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 0u, key0, key1),
+                odd, &a01, &a23, &b01, &b23);
+    float xs[8];
+    if (PRE) {
+        // every table entry is finite, so |v| * inv is NaN or infinite only
+        // for NaN or infinite v, which quantise to 0 (wave-uniform, rare)
+        bool bad = false;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            xs[j] = fminf(fabsf(v[j]) * inv[j], s0x);
+            bad = bad || __builtin_amdgcn_classf(v[j], kNonFinite);
+        }
+        if (__builtin_expect(__ballot(bad) != 0, 0)) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                xs[j] = __builtin_amdgcn_classf(v[j], kNonFinite) ? 0.0f : xs[j];
+        }
+    } else {
+        // entries may be infinite (0 * inf is NaN): select by class
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            xs[j] = scaled_magnitude(v[j], inv[j], s0x) * 65536.0f;
+    }
+    uint32_t Tw[8];
+    bool tie[8];
+    bool any_tie = false;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        Tw[j] = static_cast<uint32_t>(xs[j]);
+        const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
+        tie[j] = (Tw[j] & 0xFFFFu) == h;
+        any_tie = any_tie || tie[j];
+    }
+    p[0] = pair_codes(Tw[0], Tw[1], v[0], v[1], a01, one2);
+    p[1] = pair_codes(Tw[2], Tw[3], v[2], v[3], a23, one2);
+    p[2] = pair_codes(Tw[4], Tw[5], v[4], v[5], b01, one2);
+    p[3] = pair_codes(Tw[6], Tw[7], v[6], v[7], b23, one2);
+    // wave-uniform branch (the DPP exchange needs every lane): draw the low
+    // halves from the purpose-1 blocks when any lane has a tie
+    if (__builtin_expect(__ballot(any_tie) != 0, 0)) {
+        tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 1u, key0, key1),
+                    odd, &a01, &a23, &b01, &b23);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
+            if (tie[j])
+                set_lane16(&p[j >> 1], j, quantise_tie_scaled(v[j], xs[j], Tw[j], h));
+        }
+    }
+}
+
+// The whole tiles of one code row.  inv_t / inv0 hold s_k / W, multiplied by
+// 2^16 when PRE (then s0x = s0 * 2^16 too), so that xs = x * 2^16 comes out of
+// one multiply and one min; without PRE (an entry is above 2^100, or
+// infinite) the 2^16 is applied after the min.  Both give
+// xs = RN(|v| s_k / W) * 2^16 exactly whenever |v| s_k / W is a normal
+// number, and T = floor(xs) = 0 with a zero threshold low half otherwise, so
+// the codes do not depend on PRE.  With one scale the wave's first tile
+// (`first`, if below ntiles) arrives already loaded in `in0`.
 template <bool MULTI, int BITS, bool PRE>
 __device__ __forceinline__ void quantise_tiles(const float* __restrict__ row, uint8_t* __restrict__ out,
                                                const uint8_t* __restrict__ idx, int64_t ntiles, int64_t first,
@@ -364,20 +436,18 @@ __device__ __forceinline__ void quantise_tiles(const float* __restrict__ row, ui
                                                uint32_t key1, int32_t tpw)
 {
     const int lane = threadIdx.x & 63;
-    const bool odd = (lane & 1) != 0;
     uint32_t one2 = 0x00010001u;
     asm("" : "+s"(one2));
     for (int64_t c0 = first; c0 < ntiles; c0 += stride) {
       const int64_t c1 = c0 + tpw < ntiles ? c0 + tpw : ntiles;
       for (int64_t T = c0; T < c1; ++T) {
         const int64_t a_off = (T << 9) + 4 * lane;
-        const int64_t b_off = a_off + 256;
         TileIn in;
         if (!MULTI && T == first)
             in = in0;
         else
             in = load_tile<MULTI>(row, idx, a_off);
-        float v[8] = {in.A.x, in.A.y, in.A.z, in.A.w, in.B.x, in.B.y, in.B.z, in.B.w};
+        const float v[8] = {in.A.x, in.A.y, in.A.z, in.A.w, in.B.x, in.B.y, in.B.z, in.B.w};
         float inv[8];
         if (MULTI) {
 #pragma unroll
@@ -390,62 +460,49 @@ __device__ __forceinline__ void quantise_tiles(const float* __restrict__ row, ui
             for (int j = 0; j < 8; ++j)
                 inv[j] = inv0;
         }
-        const uint64_t q = static_cast<uint64_t>(T << 6) + static_cast<uint64_t>(lane >> 1) + (odd ? 32u : 0u);
-        uint32_t a01, a23, b01, b23;
-        tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 0u, key0,
-                                  key1),
-                    odd, &a01, &a23, &b01, &b23);
-        float xs[8];
-        if (PRE) {
-            // every table entry is finite, so |v| * inv is NaN or infinite only
-            // for NaN or infinite v, which quantise to 0 (wave-uniform, rare)
-            bool bad = false;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                xs[j] = fminf(fabsf(v[j]) * inv[j], s0x);
-                bad = bad || __builtin_amdgcn_classf(v[j], kNonFinite);
-            }
-            if (__builtin_expect(__ballot(bad) != 0, 0)) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    xs[j] = __builtin_amdgcn_classf(v[j], kNonFinite) ? 0.0f : xs[j];
-            }
-        } else {
-            // entries may be infinite (0 * inf is NaN): select by class
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                xs[j] = scaled_magnitude(v[j], inv[j], s0x) * 65536.0f;
-        }
-        uint32_t Tw[8];
-        bool tie[8];
-        bool any_tie = false;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            Tw[j] = static_cast<uint32_t>(xs[j]);
-            const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
-            tie[j] = (Tw[j] & 0xFFFFu) == h;
-            any_tie = any_tie || tie[j];
-        }
-        uint32_t p[4] = {pair_codes(Tw[0], Tw[1], v[0], v[1], a01, one2),
-                         pair_codes(Tw[2], Tw[3], v[2], v[3], a23, one2),
-                         pair_codes(Tw[4], Tw[5], v[4], v[5], b01, one2),
-                         pair_codes(Tw[6], Tw[7], v[6], v[7], b23, one2)};
-        // wave-uniform branch (the DPP exchange needs every lane): draw the
-        // low halves from the purpose-1 blocks when any lane has a tie
-        if (__builtin_expect(__ballot(any_tie) != 0, 0)) {
-            tile_halves(philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), worker, 1u, key0,
-                                      key1),
-                        odd, &a01, &a23, &b01, &b23);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t h = j < 4 ? half16(a01, a23, j) : half16(b01, b23, j - 4);
-                if (tie[j])
-                    set_lane16(&p[j >> 1], j, quantise_tie_scaled(v[j], xs[j], Tw[j], h));
-            }
-        }
+        uint32_t p[4];
+        tile_codes<PRE>(v, inv, s0x, T, worker, key0, key1, one2, p);
         store_pairs<BITS>(out, a_off, p[0], p[1]);
-        store_pairs<BITS>(out, b_off, p[2], p[3]);
+        store_pairs<BITS>(out, a_off + 256, p[2], p[3]);
       }
+    }
+}
+
+// The coordinates of one row past its last whole tile (fewer than 512), in
+// groups of 8 contiguous coordinates, one per lane of one wave.  inv_s holds
+// s_k / W (not scaled).
+template <bool MULTI, int BITS>
+__device__ __forceinline__ void quantise_tail(const float* __restrict__ row, uint8_t* __restrict__ out,
+                                              const uint8_t* __restrict__ idx, int64_t d, int64_t ntiles,
+                                              const float* inv_s, float inv0, float s0, uint32_t kmax,
+                                              uint32_t worker, uint32_t key0, uint32_t key1)
+{
+    const int64_t q = (ntiles << 6) + (threadIdx.x & 63);
+    const int64_t base = q << 3;
+    if (base >= d)
+        return;
+    float v[8], inv[8];
+    int32_t code[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const bool in = base + j < d;
+        v[j] = in ? row[base + j] : 0.0f;
+        inv[j] = MULTI ? inv_s[min(static_cast<uint32_t>(in ? idx[base + j] : 0), kmax)] : inv0;
+    }
+    quantise_group(v, inv, s0, static_cast<uint64_t>(q), worker, key0, key1, code);
+    if (BITS == 8) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (base + j < d)
+                out[base + j] = static_cast<uint8_t>(code[j]);
+    } else {
+        // the group's 8 codes fill whole bytes of its own (coordinates past d
+        // have code 0); the packed row holds them
+        if (BITS == 4)
+            *reinterpret_cast<uint32_t*>(out + base / 2) = pack_field<4>(code) | (pack_field<4>(code + 4) << 16);
+        else
+            *reinterpret_cast<uint16_t*>(out + base / 4) =
+                static_cast<uint16_t>(pack_field<2>(code) | (pack_field<2>(code + 4) << 8));
     }
 }
 
@@ -506,36 +563,8 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
 
     // Coordinates past the last whole tile (fewer than 512): groups of 8
     // contiguous coordinates, one per lane of the first wave of block x = 0.
-    if (blockIdx.x == 0 && threadIdx.x < 64) {
-        const int64_t q = (ntiles << 6) + threadIdx.x;
-        const int64_t base = q << 3;
-        if (base < d) {
-            float v[8], inv[8];
-            int32_t code[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const bool in = base + j < d;
-                v[j] = in ? row[base + j] : 0.0f;
-                inv[j] = MULTI ? inv_s[min(static_cast<uint32_t>(in ? idx[base + j] : 0), kmax)] : inv0;
-            }
-            quantise_group(v, inv, s0, static_cast<uint64_t>(q), worker, key0, key1, code);
-            if (BITS == 8) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (base + j < d)
-                        out[base + j] = static_cast<uint8_t>(code[j]);
-            } else {
-                // the group's 8 codes fill whole bytes of its own (coordinates
-                // past d have code 0); the packed row holds them
-                if (BITS == 4)
-                    *reinterpret_cast<uint32_t*>(out + base / 2) =
-                        pack_field<4>(code) | (pack_field<4>(code + 4) << 16);
-                else
-                    *reinterpret_cast<uint16_t*>(out + base / 4) =
-                        static_cast<uint16_t>(pack_field<2>(code) | (pack_field<2>(code + 4) << 8));
-            }
-        }
-    }
+    if (blockIdx.x == 0 && threadIdx.x < 64)
+        quantise_tail<MULTI, BITS>(row, out, idx, d, ntiles, inv_s, inv0, s0, kmax, worker, key0, key1);
 }
 
 // ---------------------------------------------------------------------------
