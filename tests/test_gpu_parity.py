@@ -371,3 +371,56 @@ def test_rows_longer_than_2_pow_31():
         assert torch.equal(step.codes[:, c:e].to(torch.int32).sum(dim=0), step.sum[c:e]), c
     del g, step
     torch.cuda.empty_cache()
+
+
+def _long_rows(d, M, seed):
+    ldg = synth.round_up(d, 64)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(seed)
+    g = torch.zeros((M, ldg), dtype=torch.float32, device=DEV)
+    for m in range(M):
+        for c in range(0, d, 1 << 28):
+            n = min(1 << 28, d - c)
+            g[m, c:c + n].normal_(0.0, 1e-3, generator=gen)
+    return g
+
+
+def test_packed_rows_longer_than_2_pow_31():
+    """4-bit packed codes over 2^31 + 777 coordinates: oracle windows (the
+    packed row unpacked) around 2^31 and at the ragged end."""
+    d, M, scales, seed = (1 << 31) + 777, 2, [7.0, 112.0], 77
+    g = _long_rows(d, M, 32)
+    step = Step(d, M, scales, device=DEV, bits=4)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    W = np.float32(step.w[0].item())
+    w = 1 << 14
+    # even window starts: a window begins on a byte of the packed row
+    for i0 in ((1 << 31) - w // 2, (1 << 31) + 2, (d - w) & ~1):
+        i1 = min(d, i0 + w)
+        host = g[:, i0:i1].cpu().numpy()
+        idx = O.scale_index_shared(host, W, scales)
+        assert np.array_equal(step.idx[i0:i1].cpu().numpy(), idx), i0
+        codes = np.stack([O.quantize(host[m], W, scales, seed, worker=m, i0=i0, idx=idx) for m in range(M)])
+        packed = step.codes[:, i0 // 2:(i1 + 1) // 2].cpu().numpy()
+        for m in range(M):
+            assert np.array_equal(O.unpack_codes(packed[m], i1 - i0, 4), codes[m]), (i0, m)
+        assert np.array_equal(step.sum[i0:i1].cpu().numpy(), O.sum_codes(codes)), i0
+    del g, step
+    torch.cuda.empty_cache()
+
+
+def test_streamed_rows_longer_than_2_pow_31():
+    """The streamed accumulator (one code row reused, sum += per worker) over
+    2^31 + 777 coordinates: windows against the oracle, and the sum bounded."""
+    d, M, scales, seed = (1 << 31) + 777, 2, synth.scales_for(8, 3), 78
+    g = _long_rows(d, M, 33)
+    step = Step(d, M, scales, device=DEV, streamed=True)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    device_norm_check(g, d, np.float32(step.w[0].item()))
+    w = 1 << 14
+    check_windows(step, g, d, scales, seed, [((1 << 31) - w // 2, w), (d - w, w)], streamed=True)
+    assert int(step.sum[:d].abs().max()) <= M * scales[0]
+    del g, step
+    torch.cuda.empty_cache()
