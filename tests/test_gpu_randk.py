@@ -96,3 +96,36 @@ def test_randk_workload_full_size():
     full = np.zeros(d, dtype=np.float32)
     full[sel.astype(np.int64)] = ref["out"]
     assert np.array_equal(out.cpu().numpy().view(np.int32), full.view(np.int32))
+
+
+def _key(hi, lo, i):
+    return (int(hi) << 64) | (int(lo) << 32) | int(i)
+
+
+@pytest.mark.parametrize("d,K", [(2 ** 32 - 1, 10_000), (3_000_000_007, 16_385)])
+def test_selection_at_the_largest_d(d, K):
+    """d up to 2^32 - 1 (about 4096 boundary candidates, uint32 indices near
+    their limit), on both selection paths.  The oracle cannot sort 4e9 keys,
+    so the rule is checked exactly inside windows: a coordinate there is
+    selected iff its (hi, lo, i) is at most the largest selected one."""
+    import paper_2109_12497_amd as uq
+
+    seed = 21
+    sel = torch.zeros(K + 64, dtype=torch.int32, device=DEV)
+    wsb = uq.uq_randk_workspace_bytes(d, K)
+    ws = torch.zeros(wsb // 4 + 64, dtype=torch.int32, device=DEV)
+    uq.uq_randk_select(d, K, seed, sel, ws, wsb)
+    torch.cuda.synchronize()
+    got = sel[:K].cpu().numpy().view(np.uint32).astype(np.int64)
+    assert np.all(np.diff(got) > 0) and got[0] >= 0 and got[-1] < d
+    keys = [O.randk_keys(seed, int(i), 1) for i in got]
+    top = max(_key(h[0], l[0], i) for (h, l), i in zip(keys, got))
+    chosen = set(got.tolist())
+    n = 1 << 20
+    for i0 in (0, (1 << 31) - n // 2, d - n):
+        hi, lo = O.randk_keys(seed, i0, n)
+        # candidates by the high word first (cheap), then the exact rule
+        near = np.nonzero(hi.astype(np.uint64) <= (top >> 64))[0]
+        below = {i0 + int(j) for j in near if _key(hi[j], lo[j], i0 + int(j)) <= top}
+        inside = {i for i in chosen if i0 <= i < i0 + n}
+        assert below == inside, (i0, len(below), len(inside))
