@@ -153,22 +153,39 @@ def brute_force_moments(v, scale_per_coord, W: Fraction, laws):
     """Exact E[Q(v)] and E||Q(v) - v||^2 over all 2^n outcomes.
 
     Q_i = W * sign(v_i) * mag_i / s*_i  (Eq. (7)/(10) with xi = mag / s*).
+    Every joint outcome is enumerated; its probability is carried as an
+    integer numerator over 2^(32 n) (each p_i is a multiple of 2^-32), and
+    each coordinate accumulates the probability mass of its upper level.
     """
     v = [frac(x) for x in v]
     n = len(v)
-    mean = [Fraction(0)] * n
-    second = Fraction(0)
-    total = Fraction(0)
-    for mags, prob in enumerate_outcomes(laws):
+    one = 1 << 32
+    weights = []
+    for _, p in laws:
+        a = p * one
+        assert a.denominator == 1 and 0 <= a <= one
+        weights.append((one - int(a), int(a)))
+    total = 0
+    upper = [0] * n  # sum of the probabilities of the outcomes with mag_i = l_i + 1
+    for ups in itertools.product((0, 1), repeat=n):
+        prob = 1
+        for (w0, w1), u in zip(weights, ups):
+            prob *= w1 if u else w0
         total += prob
-        err2 = Fraction(0)
-        for i in range(n):
-            sgn = (v[i] > 0) - (v[i] < 0)
-            q = W * sgn * Fraction(mags[i]) / scale_per_coord[i]
-            mean[i] += prob * q
-            err2 += (q - v[i]) ** 2
-        second += prob * err2
-    assert total == 1
+        for i, u in enumerate(ups):
+            if u:
+                upper[i] += prob
+    denom = one ** n
+    assert total == denom
+    mean = []
+    second = Fraction(0)
+    for i, (l, _) in enumerate(laws):
+        sgn = (v[i] > 0) - (v[i] < 0)
+        q0 = W * sgn * Fraction(l) / scale_per_coord[i]
+        q1 = W * sgn * Fraction(l + 1) / scale_per_coord[i]
+        m0, m1 = Fraction(denom - upper[i], denom), Fraction(upper[i], denom)
+        mean.append(m0 * q0 + m1 * q1)
+        second += m0 * (q0 - v[i]) ** 2 + m1 * (q1 - v[i]) ** 2
     return mean, second
 
 
