@@ -161,12 +161,6 @@ __device__ __forceinline__ int32_t quantise_tie_scaled(float v, float xs, uint32
     return apply_sign((T >> 16) + (lo16 < t_lo ? 1u : 0u), v);
 }
 
-__device__ __forceinline__ uint32_t pack4(int32_t a, int32_t b, int32_t c, int32_t d)
-{
-    return (static_cast<uint32_t>(a) & 0xFFu) | ((static_cast<uint32_t>(b) & 0xFFu) << 8) |
-           ((static_cast<uint32_t>(c) & 0xFFu) << 16) | (static_cast<uint32_t>(d) << 24);
-}
-
 // Deterministic wave64 sum of a double (fixed butterfly order).
 __device__ __forceinline__ double wave_sum(double x)
 {
