@@ -153,8 +153,19 @@ def cpu_baseline(g, cfg, budget_s: float):
     t0 = time.perf_counter()
     ref = oracle.pipeline(host, scales, seed, d=dn)
     dt = time.perf_counter() - t0
+    # a sample that finishes well inside the budget is run again (same input,
+    # same result) until about the budget is spent, so the rate is not one
+    # short run's
+    runs = 1
+    while dt < 0.75 * budget_s and runs < 64 and dt / runs * (runs + 1) <= budget_s:
+        t1 = time.perf_counter()
+        oracle.pipeline(host, scales, seed, d=dn)
+        dt += time.perf_counter() - t1
+        runs += 1
     sample = "full workload" if dn == d else f"all {M} workers, coordinates [0, {dn}) of {d}"
-    return {"value": round(M * dn / dt / 1e9, 6), "unit": "G elements/s", "cores": 1, "kind": "oracle",
+    if runs > 1:
+        sample += f", {runs} runs"
+    return {"value": round(M * dn * runs / dt / 1e9, 6), "unit": "G elements/s", "cores": 1, "kind": "oracle",
             "sample": sample, "seconds": round(dt, 2)}, ref, dn
 
 
