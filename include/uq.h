@@ -160,6 +160,9 @@ int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w,
  * Quantise to packed codes.  bits = 4 needs s_0 <= 7, bits = 2 needs s_0 <= 1.
  *   scales, K, idx  as for uq_quantize_multi (K = 1: one scale, idx may be NULL)
  *   packed          [rows][ldp] bytes, ldp >= ceil(d * bits / 8), ldp % 16 == 0
+ *                   (written: the bytes of every 8-coordinate group that
+ *                   starts below d, ceil(d / 8) * bits bytes per row, which
+ *                   ldp always covers; fields past d hold 0)
  * Other arguments as for uq_quantize_single.
  */
 int uq_quantize_packed(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,

@@ -348,14 +348,6 @@ __device__ __forceinline__ TileIn load_tile(const float* __restrict__ row, const
     return in;
 }
 
-// The whole tiles of one code row.  inv_t / inv0 hold s_k / W, multiplied by
-// 2^16 when PRE (then s0x = s0 * 2^16 too), so that xs = x * 2^16 comes out of
-// one multiply and one min; without PRE (an entry is above 2^100, or
-// infinite) the 2^16 is applied after the min.  Both give
-// xs = RN(|v| s_k / W) * 2^16 exactly whenever |v| s_k / W is a normal
-// number, and T = floor(xs) = 0 with a zero threshold low half otherwise, so
-// the codes do not depend on PRE.  With one scale the wave's first tile
-// (`first`, if below ntiles) arrives already loaded in `in0`.
 // The eight codes of one lane for tile T of worker `worker`, as four 16-bit
 // lane pairs (A0 A1, A2 A3, B0 B1, B2 B3).  v: the lane's coordinates;
 // inv: their s_k / W, times 2^16 when PRE (then s0x = s0 * 2^16).  Every lane
