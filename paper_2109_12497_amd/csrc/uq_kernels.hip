@@ -8,7 +8,7 @@
 //   k_index     shared scale index from the largest |g| over    (Eq. (11) +
 //               the workers at each coordinate                    sharing)
 //   k_quantise  Philox draws + stochastic rounding + int8 pack  (Eq. (8)/(12))
-//   k_sum       int8 rows -> int32                               (all-reduce)
+//   k_sum       int8 (or 4-/2-bit) code rows -> int32           (all-reduce)
 //   k_dequant   int32 (+ index) -> fp32                          (Eq. (9)/(13))
 //
 // Every per-coordinate result is a pure function of its inputs and the
@@ -560,135 +560,103 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
 }
 
 // ---------------------------------------------------------------------------
-// Integer sum of the rows' codes (the all-reduce), four coordinates per
-// thread per step.
+// Integer sum of the rows' codes (the all-reduce), for int8 codes and for
+// codes packed as 4- or 2-bit fields.  A block tile of 4096 coordinates:
+// thread t unpacks coordinates 16t .. 16t+15 of the tile from one 16-, 8- or
+// 4-byte load per row with signed bit-field extracts, eight rows' loads in
+// flight at a time.  The tile's sums are then staged through LDS so that the
+// int32 stores (and, when accumulating, the loads of the old sums) are
+// coalesced: thread t writes quads t, t+256, t+512 and t+768 of the tile.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int32_t sbyte(uint32_t w, int j)
-{
-    return static_cast<int32_t>(static_cast<int8_t>(w >> (8 * j)));
-}
-
-// Block tiles of 4096 coordinates: thread t sums quads t, t+256, t+512 and
-// t+768 of the tile, so every row load and every store of a wave covers
-// 256 or 1024 contiguous bytes; rows are read four at a time.  Quads past d
-// (in the last tile) are skipped and the last d % 4 coordinates are summed
-// one by one.
 constexpr int64_t kSumTile = 4096;
 
-__device__ __forceinline__ void sum_rows(const int8_t* __restrict__ codes, int32_t rows, int64_t ldc,
-                                         int64_t base, const bool live[4], int32_t acc[16])
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// The 16 BITS-bit fields starting at p (16-byte aligned for BITS = 8, 8-byte
+// for 4, 4-byte for 2).
+template <int BITS>
+__device__ __forceinline__ u32x4 load_fields(const uint8_t* p)
 {
-    int32_t r = 0;
-    for (; r + 4 <= rows; r += 4) {
-        uint32_t w[4][4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                w[u][c] = live[c] ? load_nt_u32(codes + static_cast<int64_t>(r + u) * ldc + base + 1024 * c) : 0u;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[4 * c + j] += sbyte(w[u][c], j);
+    u32x4 w = {0u, 0u, 0u, 0u};
+    if (BITS == 8) {
+        w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    } else if (BITS == 4) {
+        const u32x2 h = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+        w.x = h.x;
+        w.y = h.y;
+    } else {
+        w.x = load_nt_u32(p);
     }
-    for (; r < rows; ++r) {
+    return w;
+}
+
+template <int BITS>
+__device__ __forceinline__ void add_fields(u32x4 w, int32_t acc[16])
+{
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const uint32_t w = live[c] ? load_nt_u32(codes + static_cast<int64_t>(r) * ldc + base + 1024 * c) : 0u;
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                acc[4 * c + j] += sbyte(w, j);
-        }
+    for (int j = 0; j < 16; ++j) {
+        const int k = (j * BITS) / 32;
+        const uint32_t word = k == 0 ? w.x : k == 1 ? w.y : k == 2 ? w.z : w.w;
+        acc[j] += __builtin_amdgcn_sbfe(static_cast<int32_t>(word), (j * BITS) % 32, BITS);
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_sum(const int8_t* __restrict__ codes, int64_t d, int32_t rows,
+template <int BITS>
+__global__ __launch_bounds__(kBlock) void k_sum(const uint8_t* __restrict__ codes, int64_t d, int32_t rows,
                                                 int64_t ldc, int32_t accumulate, int32_t* __restrict__ sum)
 {
-    const int64_t dq = d & ~int64_t(3);  // coordinates covered by whole quads
+    constexpr int kRowsInFlight = 8;
+    // the tile's sums with one padding word after every 16, so that both the
+    // row-of-16 writes and the quad reads are free of bank conflicts
+    __shared__ int32_t stage[kSumTile + kSumTile / 16];
+    const int t = threadIdx.x;
     for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
          tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
-        const int64_t base = tile0 + 4 * threadIdx.x;
-        bool live[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            live[c] = base + 1024 * c + 4 <= dq;
-        int32_t acc[16];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            int4 a = make_int4(0, 0, 0, 0);
-            if (accumulate && live[c])
-                a = *reinterpret_cast<const int4*>(sum + base + 1024 * c);
-            acc[4 * c] = a.x; acc[4 * c + 1] = a.y; acc[4 * c + 2] = a.z; acc[4 * c + 3] = a.w;
-        }
-        sum_rows(codes, rows, ldc, base, live, acc);
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            if (live[c])
-                *reinterpret_cast<int4*>(sum + base + 1024 * c) =
-                    make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
-    }
-    // the last d % 4 coordinates
-    const int64_t t = dq + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (blockIdx.x == 0 && t < d) {
-        int32_t acc = accumulate ? sum[t] : 0;
-        for (int32_t r = 0; r < rows; ++r)
-            acc += codes[static_cast<int64_t>(r) * ldc + t];
-        sum[t] = acc;
-    }
-}
-
-// Sum of packed rows (BITS = 4 or 2): a block tile of 4096 coordinates,
-// thread t unpacks coordinates 16t .. 16t+15 of the tile from one 8-byte
-// (4-bit) or 4-byte (2-bit) load per row with signed bit-field extracts.
-template <int BITS>
-__global__ __launch_bounds__(kBlock) void k_sum_packed(const uint8_t* __restrict__ packed, int64_t d, int32_t rows,
-                                                       int64_t ldp, int32_t accumulate, int32_t* __restrict__ sum)
-{
-    for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
-         tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
-        const int64_t c0 = tile0 + 16 * threadIdx.x;
-        if (c0 >= d)
-            continue;
-        const int64_t byte0 = c0 * BITS / 8;
+        const int64_t c0 = tile0 + 16 * t;
         int32_t acc[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j)
             acc[j] = 0;
-        for (int32_t r = 0; r < rows; ++r) {
-            const uint8_t* p = packed + static_cast<int64_t>(r) * ldp + byte0;
-            uint32_t w[2];
-            if (BITS == 4) {
-                const uint2 x = *reinterpret_cast<const uint2*>(p);
-                w[0] = x.x;
-                w[1] = x.y;
-            } else {
-                w[0] = load_nt_u32(p);
-                w[1] = 0u;
-            }
+        if (c0 < d) {
+            // fields past d in the last group are read (they lie inside the
+            // row's ldc bytes) and dropped below
+            const uint8_t* p = codes + c0 * BITS / 8;
+            int32_t r = 0;
+            for (; r + kRowsInFlight <= rows; r += kRowsInFlight) {
+                u32x4 w[kRowsInFlight];
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const uint32_t word = w[(j * BITS) / 32];
-                acc[j] += __builtin_amdgcn_sbfe(static_cast<int32_t>(word), (j * BITS) % 32, BITS);
+                for (int u = 0; u < kRowsInFlight; ++u)
+                    w[u] = load_fields<BITS>(p + static_cast<int64_t>(r + u) * ldc);
+#pragma unroll
+                for (int u = 0; u < kRowsInFlight; ++u)
+                    add_fields<BITS>(w[u], acc);
             }
+            for (; r < rows; ++r)
+                add_fields<BITS>(load_fields<BITS>(p + static_cast<int64_t>(r) * ldc), acc);
         }
-        if (c0 + 16 <= d) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                int4 a = make_int4(acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]);
+        for (int j = 0; j < 16; ++j)
+            stage[17 * t + j] = acc[j];
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int L = 1024 * c + 4 * t;  // tile coordinate of the quad
+            const int S = L + (L >> 4);      // its padded LDS index
+            const int64_t q0 = tile0 + L;
+            if (q0 + 4 <= d) {
+                int4 a = make_int4(stage[S], stage[S + 1], stage[S + 2], stage[S + 3]);
                 if (accumulate) {
-                    const int4 o = *reinterpret_cast<const int4*>(sum + c0 + 4 * c);
+                    const int4 o = *reinterpret_cast<const int4*>(sum + q0);
                     a.x += o.x; a.y += o.y; a.z += o.z; a.w += o.w;
                 }
-                *reinterpret_cast<int4*>(sum + c0 + 4 * c) = a;
+                *reinterpret_cast<int4*>(sum + q0) = a;
+            } else {
+                for (int j = 0; j < 4 && q0 + j < d; ++j)
+                    sum[q0 + j] = stage[S + j] + (accumulate ? sum[q0 + j] : 0);
             }
-        } else {
-            for (int j = 0; j < 16 && c0 + j < d; ++j)
-                sum[c0 + j] = acc[j] + (accumulate ? sum[c0 + j] : 0);
         }
+        __syncthreads();  // the next tile reuses stage
     }
 }
 
@@ -853,7 +821,8 @@ hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc,
     if (d == 0)
         return hipSuccess;
     const unsigned gx = one_shot(d, kSumTile);
-    hipLaunchKernelGGL(k_sum, dim3(gx), dim3(kBlock), 0, stream, codes, d, rows, ldc, accumulate, sum);
+    hipLaunchKernelGGL(k_sum<8>, dim3(gx), dim3(kBlock), 0, stream, reinterpret_cast<const uint8_t*>(codes), d,
+                       rows, ldc, accumulate, sum);
     return hipGetLastError();
 }
 
@@ -864,9 +833,9 @@ hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int
         return hipSuccess;
     const unsigned gx = one_shot(d, kSumTile);
     if (bits == 4)
-        hipLaunchKernelGGL(k_sum_packed<4>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
+        hipLaunchKernelGGL(k_sum<4>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
     else
-        hipLaunchKernelGGL(k_sum_packed<2>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
+        hipLaunchKernelGGL(k_sum<2>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
     return hipGetLastError();
 }
 

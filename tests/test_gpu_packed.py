@@ -43,6 +43,19 @@ def test_packed_matches_oracle(d, scales, bits):
     assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
 
 
+@pytest.mark.parametrize("M", [8, 11, 17])
+@pytest.mark.parametrize("d", [4095, 4096, 12_291])
+@pytest.mark.parametrize("bits,scales", [(8, [127.0]), (4, [7.0]), (2, [1.0])])
+def test_sum_row_groups(M, d, bits, scales):
+    """The sum reads rows in groups of eight: whole groups, a group plus a
+    remainder, and ragged tiles, against the oracle."""
+    host = synth.mixed_rows(M, d, seed=M * 7 + d, ldg=synth.round_up(d, 64))
+    st = run(host, d, scales, bits, seed=11)
+    ref = O.pipeline(host, scales, 11, d=d, W=np.float32(st.w[0].item()))
+    assert np.array_equal(st.sum[:d].cpu().numpy(), ref["sum"])
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
 @pytest.mark.parametrize("bits,scales", [(4, [7.0]), (2, [1.0])])
 def test_packed_equals_int8_path(bits, scales):
     d, M = 300_001, 5
