@@ -756,14 +756,6 @@ static unsigned one_shot(int64_t units, int64_t per_block)
     return static_cast<unsigned>(blocks);
 }
 
-static unsigned grid_for(int64_t units, int64_t cap)
-{
-    int64_t blocks = (units + kBlock - 1) / kBlock;
-    if (blocks > cap)
-        blocks = cap;
-    return static_cast<unsigned>(blocks < 1 ? 1 : blocks);
-}
-
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
                                float* w, uint8_t* idx, double* part, hipStream_t stream)
 {
@@ -844,7 +836,7 @@ hipError_t launch_dequant(const int32_t* sum, int64_t d, int32_t M, const float*
 {
     if (d == 0)
         return hipSuccess;
-    const unsigned gx = grid_for((d + 3) / 4, grid_cap());
+    const unsigned gx = one_shot((d + 3) / 4, kBlock);
     if (S.K > 1)
         hipLaunchKernelGGL(k_dequant<true>, dim3(gx), dim3(kBlock), 0, stream, sum, d, M, w, S, idx, out);
     else
