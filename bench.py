@@ -140,6 +140,32 @@ def copy_probe(nbytes: int) -> None:
     print(json.dumps({"copy_probe_bytes": nbytes, "read_plus_write_GBps": 2 * nbytes / dt / 1e9}))
 
 
+def stage_ms_per_call(torch, stream, fn, reps: int, rounds: int = 3) -> float:
+    """GPU time per call (ms) of fn repeated back to back between two events
+    on `stream`, its inputs already in place.  Best of `rounds` rounds: a
+    round in which the host fell behind the GPU (a stall in the runtime's
+    launch path) reads high, so the lowest round is the stage's own time."""
+    best = float("inf")
+    for _ in range(rounds):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b) / reps)
+    return best
+
+
+def stage_reps(steps: int, step_s: float) -> int:
+    """Calls per timing round of one stage: the bench's step count, fewer for
+    long steps (a round of about 0.1 s), at least 10."""
+    return max(10, min(steps, int(0.1 / max(step_s, 1e-9))))
+
+
 def cpu_baseline(g, cfg, budget_s: float):
     """The oracle on the host cores over a bounded sample of the workload."""
     import numpy as np
@@ -191,21 +217,10 @@ def bench_randk(args, g, cfg) -> int:
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     # per-stage times: each stage repeated back to back between two events
-    def mark():
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        return e
-
     def stage_time(fn, reps):
-        fn()
-        a = mark()
-        for _ in range(reps):
-            fn()
-        b = mark()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps
+        return stage_ms_per_call(torch, stream, fn, reps)
 
-    reps = max(10, args.steps)
+    reps = stage_reps(args.steps, elapsed / args.steps)
     stage_ms = {"select": stage_time(lambda: st.select(seed), reps),
                 "gather": stage_time(lambda: st.gather(g), reps),
                 "aggregate": stage_time(lambda: st.inner.run(st.sub, seed), reps),
@@ -305,15 +320,9 @@ def main() -> int:
         return e
 
     def stage_time(fn, reps):
-        fn()
-        a = mark()
-        for _ in range(reps):
-            fn()
-        b = mark()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps
+        return stage_ms_per_call(torch, stream, fn, reps)
 
-    reps = max(10, args.steps)
+    reps = stage_reps(args.steps, elapsed / args.steps)
     stage_ms = {"shared_scale": stage_time(lambda: step.shared_scale(g), reps)}
     if streamed:
         # one worker row per call, M calls per step
