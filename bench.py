@@ -29,6 +29,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "G gradient elements/s quantize+sum+dequantize; % of HBM peak GB/s"
 HBM_PEAK_GBS = 8000.0
+# workers up to which the shared scale takes the fused norm + row-maximum pass
+FUSED_MAX_ROWS = 16
 KERNEL_SOURCES = ["paper_2109_12497_amd/csrc/uq_kernels.hip", "paper_2109_12497_amd/csrc/uq_device.hpp"]
 
 
@@ -43,11 +45,21 @@ def quantize_bytes_per_launch(d: int, rows: int, K: int, bits: int = 8) -> int:
 
 
 def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> dict:
-    """Bytes each stage must move at minimum (reads + writes), per step."""
+    """Bytes each stage must move at minimum (reads + writes), per step.  With
+    several scales and at most 16 workers the norm pass also writes the
+    largest |g| over the workers (4 bytes per coordinate), which the index
+    pass reads instead of the gradients; with more workers the index pass
+    reads every gradient again."""
     multi = K > 1
     cb = code_bytes(d, bits)
+    if not multi:
+        scale_bytes = 4 * M * d
+    elif M <= FUSED_MAX_ROWS:
+        scale_bytes = 4 * M * d + 4 * d + 4 * d + d
+    else:
+        scale_bytes = 4 * M * d + 4 * M * d + d
     b = {
-        "shared_scale": 4 * M * d + (4 * M * d + d if multi else 0),
+        "shared_scale": scale_bytes,
         "quantize": ((M * quantize_bytes_per_launch(d, 1, K, bits)) if streamed
                      else quantize_bytes_per_launch(d, M, K, bits)),
         "sum": (M * cb + 4 * d) if not streamed else (cb + 4 * d) + (M - 1) * (cb + 8 * d),

@@ -173,11 +173,18 @@ extern "C" {
 
 size_t uq_workspace_bytes(int64_t d, int32_t M)
 {
-    const uq::NormPlan p = uq::norm_plan(d < 0 ? 0 : d);
+    const int64_t dd = d < 0 ? 0 : d;
+    const uq::NormPlan p = uq::norm_plan(dd);
     const int64_t rows = M < 1 ? 1 : M;
     const int64_t chunks = p.nchunks < 1 ? 1 : p.nchunks;
-    const size_t bytes = static_cast<size_t>(rows) * static_cast<size_t>(chunks) * sizeof(double);
-    return (bytes + 255) / 256 * 256;
+    size_t bytes = uq::align256(static_cast<size_t>(rows) * static_cast<size_t>(chunks) * sizeof(double));
+    // enough for any K: with several scales and few rows the fused pass
+    // also keeps the rows' maxima
+    if (uq::use_fused(dd, static_cast<int32_t>(rows), 2)) {
+        const size_t fused = uq::fused_layout(dd, static_cast<int32_t>(rows)).bytes;
+        bytes = fused > bytes ? fused : bytes;
+    }
+    return bytes;
 }
 
 int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
@@ -201,8 +208,7 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const flo
     if (ws_bytes < uq_workspace_bytes(d, M))
         return fail(UQ_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", ws_bytes,
                     uq_workspace_bytes(d, M));
-    return launched(uq::launch_shared_scale(g, d, M, ldg, S, w, idx, static_cast<double*>(ws),
-                                            static_cast<hipStream_t>(stream)));
+    return launched(uq::launch_shared_scale(g, d, M, ldg, S, w, idx, ws, static_cast<hipStream_t>(stream)));
 }
 
 static int quantise_common(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,

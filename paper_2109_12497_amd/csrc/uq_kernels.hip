@@ -211,6 +211,306 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 }
 
 // ---------------------------------------------------------------------------
+// Fused shared scale for several scales and at most kFuseRows rows: one pass
+// over the gradients forms the rows' chunk sums of squares and the largest
+// usable |g| over the rows at every coordinate (amax, fp32 [d] in the
+// workspace); the index pass then reads amax instead of the M rows.
+//   k_norm_max   block c: chunk c of every row (below)
+//   k_rowsum     block m: S_m = fixed-order sum of row m's chunk partials
+//   k_index_max  W from the S_m (the rule of k_finish; block 0 stores it),
+//                then the index of every coordinate from amax
+// Measured on MI355X, the amax stores cost far more than their bytes when
+// mixed into the sixteen concurrent row streams (the pass runs 25-30% slower
+// than without them); a variant that walked the rows one at a time and
+// stored each window's maxima once was slower still.
+// ---------------------------------------------------------------------------
+// Block c covers chunk c of every row in tiles of 1024 coordinates (256
+// quads).  Wave w owns rows w, w + 4, ... (ROWS / 4 of them; rows past M
+// re-read row M - 1, a cache hit, and are not accumulated): lane l loads quads
+// l, l + 64, l + 128, l + 192 of the tile from each of its rows, so each row
+// is read 4 KiB at a time per wave, and keeps one fp64 accumulator per row.
+// The waves' maxima meet in LDS and leave as one coalesced amax store, issued
+// after the next tile's loads: one counter tracks a wave's loads and stores in
+// issue order, so a store issued first would hold up the wait for the loads.
+// Barrier for LDS traffic only: the block's LDS writes are complete and
+// visible, while its global loads and stores stay in flight (__syncthreads
+// would also wait for those).
+__device__ __forceinline__ void sync_lds()
+{
+    __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Loads of one tile; quads past q_end re-read quad q_end - 1 (so that the
+// loads carry no branch) and are zeroed by the caller.
+template <int ROWS>
+__device__ __forceinline__ void norm_max_load(const float* const rowp[ROWS / 4], int64_t t0, int64_t q_end,
+                                              int lane, f32x4 v[ROWS / 4][4])
+{
+#pragma unroll
+    for (int r = 0; r < ROWS / 4; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t q = t0 + lane + 64 * j;
+            v[r][j] = load_nt(rowp[r] + ((q < q_end ? q : q_end - 1) << 2));
+        }
+}
+
+template <int ROWS>
+__global__ __launch_bounds__(kBlock) void k_norm_max(const float* __restrict__ g, int64_t d, int32_t M,
+                                                     int64_t ldg, int64_t chunk, int32_t nchunks,
+                                                     double* __restrict__ part, float* __restrict__ amax)
+{
+    constexpr int RPW = ROWS / 4;  // rows per wave
+    __shared__ f32x4 wave_max[4][kBlock];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int32_t c = blockIdx.x;
+    const int64_t begin = static_cast<int64_t>(c) * chunk;
+    const int64_t end = begin + chunk < d ? begin + chunk : d;
+    const int64_t q_end = end >> 2;  // chunk starts are multiples of 4: whole quads below end
+    const int64_t spare_quad = (d + 3) >> 2;
+    const float* rowp[RPW];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+        const int m = wave + 4 * r;
+        rowp[r] = g + static_cast<int64_t>(m < M ? m : M - 1) * ldg;
+    }
+    double acc[RPW];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r)
+        acc[r] = 0.0;
+    f32x4 v[RPW][4];
+    int64_t t0 = begin >> 2;
+    if (t0 < q_end) {
+        norm_max_load<ROWS>(rowp, t0, q_end, lane, v);
+        // a store after the first loads as after every later batch, so the
+        // loop entry and the back edge agree on the wait for the loads
+        __asm__ volatile("" ::: "memory");
+        *reinterpret_cast<f32x4*>(amax + (spare_quad << 2)) = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    for (; t0 < q_end; t0 += kBlock) {
+        f32x4 mx[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            mx[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            if (t0 + lane + 64 * j >= q_end) {
+#pragma unroll
+                for (int r = 0; r < RPW; ++r)
+                    v[r][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < RPW; ++r) {
+            double a = acc[r];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                a = fma((double)v[r][j].x, (double)v[r][j].x, a);
+                a = fma((double)v[r][j].y, (double)v[r][j].y, a);
+                a = fma((double)v[r][j].z, (double)v[r][j].z, a);
+                a = fma((double)v[r][j].w, (double)v[r][j].w, a);
+                mx[j].x = fmaxf(mx[j].x, usable_or_zero(v[r][j].x));
+                mx[j].y = fmaxf(mx[j].y, usable_or_zero(v[r][j].y));
+                mx[j].z = fmaxf(mx[j].z, usable_or_zero(v[r][j].z));
+                mx[j].w = fmaxf(mx[j].w, usable_or_zero(v[r][j].w));
+            }
+            acc[r] = wave + 4 * r < M ? a : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            wave_max[wave][lane + 64 * j] = mx[j];
+        sync_lds();
+        const f32x4 m0 = wave_max[0][threadIdx.x], m1 = wave_max[1][threadIdx.x];
+        const f32x4 m2 = wave_max[2][threadIdx.x], m3 = wave_max[3][threadIdx.x];
+        sync_lds();  // wave_max is reused by the next tile
+        // the next tile's loads go out before this tile's store
+        if (t0 + kBlock < q_end)
+            norm_max_load<ROWS>(rowp, t0 + kBlock, q_end, lane, v);
+        __asm__ volatile("" ::: "memory");
+        // quads past q_end go to the spare quad after amax (an unconditional
+        // store keeps the wait counts exact)
+        const int64_t q = t0 + threadIdx.x;
+        f32x4 o;
+        o.x = fmaxf(fmaxf(m0.x, m1.x), fmaxf(m2.x, m3.x));
+        o.y = fmaxf(fmaxf(m0.y, m1.y), fmaxf(m2.y, m3.y));
+        o.z = fmaxf(fmaxf(m0.z, m1.z), fmaxf(m2.z, m3.z));
+        o.w = fmaxf(fmaxf(m0.w, m1.w), fmaxf(m2.w, m3.w));
+        *reinterpret_cast<f32x4*>(amax + ((q < q_end ? q : spare_quad) << 2)) = o;
+    }
+    // the trailing d % 4 coordinates (last chunk only): each wave adds its own
+    // rows' squares; wave 0 forms the maximum over all rows
+    const int64_t tail = (q_end << 2) + lane;
+    if (tail < end) {
+#pragma unroll
+        for (int r = 0; r < RPW; ++r) {
+            const double x = rowp[r][tail];
+            acc[r] = wave + 4 * r < M ? fma(x, x, acc[r]) : 0.0;
+        }
+        if (wave == 0) {
+            float mx = 0.0f;
+            for (int32_t m = 0; m < M; ++m)
+                mx = fmaxf(mx, usable_or_zero(g[static_cast<int64_t>(m) * ldg + tail]));
+            amax[tail] = mx;
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+        const double s = wave_sum(acc[r]);
+        const int m = wave + 4 * r;
+        if (lane == 0 && m < M)
+            part[static_cast<int64_t>(m) * nchunks + c] = s;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ part, int32_t nchunks,
+                                                   double* __restrict__ rows)
+{
+    __shared__ double wave_part[kBlock / 64];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const double* p = part + static_cast<int64_t>(blockIdx.x) * nchunks;
+    // nchunks <= 8192: at most 32 partials per thread, 16 loads in flight at a time
+    double s = 0.0;
+    for (int32_t j0 = 0; j0 < nchunks; j0 += 16 * kBlock) {
+        double x[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int32_t c = j0 + static_cast<int32_t>(threadIdx.x) + kBlock * j;
+            x[j] = c < nchunks ? p[c] : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            s += x[j];
+    }
+    s = wave_sum(s);
+    if (lane == 0)
+        wave_part[wave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        rows[blockIdx.x] = (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
+}
+
+// k_index_max: a block covers kIndexTile quads (8 per thread: quads t,
+// t + 256, ..., so each load and store of a wave is contiguous), all loaded
+// before W is formed.  The per-coordinate rule compares thresholds instead of
+// forming products: a -> RN32(a * inv_k) is non-decreasing for inv_k > 0, so
+// RN32(a * inv_k) <= s_0 holds exactly for a <= T_k, the largest binary32
+// that passes; each block finds T_k once (a few ulp steps from s_0 / inv_k),
+// and a coordinate costs K compares.
+constexpr int kIndexQuads = 8;
+constexpr int64_t kIndexTile = kIndexQuads * kBlock;
+
+// Largest binary32 a >= 0 with RN32(a * inv) <= s0, for 0 < inv; 0 when inv
+// is infinite (then no positive a passes).
+__device__ float index_threshold(float inv, float s0)
+{
+    if (!(inv <= kFloatMax))
+        return 0.0f;
+    const double q = static_cast<double>(s0) / static_cast<double>(inv);
+    float a = q >= static_cast<double>(kFloatMax) ? kFloatMax : static_cast<float>(q);
+    // RN32(q) is within an ulp or two of the boundary; the loops are bounded
+    // for safety and take at most a few steps
+    for (int i = 0; i < 64 && a > 0.0f && a * inv > s0; ++i)
+        a = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a) - 1u);
+    for (int i = 0; i < 64 && a < kFloatMax; ++i) {
+        const float n = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a) + 1u);
+        if (!(n * inv <= s0))
+            break;
+        a = n;
+    }
+    return a;
+}
+
+// Scale index of amax from the thresholds: #{k < K : amax <= T_k} - 1 (the
+// rule of index_of), K - 1 for a zero amax or on the zero path.
+__device__ __forceinline__ uint32_t index_from_count(float amax, int32_t count, int32_t K, bool zero)
+{
+    if (zero || !(amax > 0.0f))
+        return static_cast<uint32_t>(K - 1);
+    return static_cast<uint32_t>(count > 0 ? count - 1 : 0);
+}
+
+__global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ amax, int64_t d, int32_t M,
+                                                      const double* __restrict__ rows, float* __restrict__ wptr,
+                                                      ScaleSet S, uint8_t* __restrict__ idx)
+{
+    __shared__ float thr_s[kMaxScales];
+    const int64_t nquad = d >> 2;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kIndexTile;
+    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kIndexTile;
+    f32x4 a[kIndexQuads];
+#pragma unroll
+    for (int j = 0; j < kIndexQuads; ++j) {
+        const int64_t q = tile0 + threadIdx.x + kBlock * j;
+        a[j] = q < nquad ? *reinterpret_cast<const f32x4*>(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+
+    // W = RN32(sqrt(max_m S_m)), NaN if any S_m is NaN (as k_finish): lane m
+    // of every wave loads S_m (M <= 64), then a butterfly maximum
+    const int lane = threadIdx.x & 63;
+    double r = lane < M ? rows[lane] : 0.0;
+    const bool any_nan = __ballot(r != r) != 0;
+    r = r != r ? 0.0 : r;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const double o = __shfl_xor(r, off, 64);
+        r = o > r ? o : r;
+    }
+    const float W = any_nan ? __builtin_nanf("") : static_cast<float>(sqrt(r));
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        *wptr = W;
+    const float s0 = S.s[0];
+    const int32_t K = S.K;
+    const bool zero = zero_path(W, div_rn32(s0, W));
+    if (threadIdx.x < K)
+        thr_s[threadIdx.x] = zero ? 0.0f : index_threshold(div_rn32(S.s[threadIdx.x], W), s0);
+    __syncthreads();
+
+    for (int64_t t0 = tile0; t0 < nquad; t0 += stride) {
+        if (t0 != tile0) {
+#pragma unroll
+            for (int j = 0; j < kIndexQuads; ++j) {
+                const int64_t q = t0 + threadIdx.x + kBlock * j;
+                a[j] = q < nquad ? *reinterpret_cast<const f32x4*>(amax + (q << 2))
+                                 : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+        }
+        int32_t cnt[kIndexQuads][4];
+#pragma unroll
+        for (int j = 0; j < kIndexQuads; ++j)
+            cnt[j][0] = cnt[j][1] = cnt[j][2] = cnt[j][3] = 0;
+        for (int k = 0; k < K; ++k) {
+            const float t = thr_s[k];
+#pragma unroll
+            for (int j = 0; j < kIndexQuads; ++j) {
+                cnt[j][0] += a[j].x <= t ? 1 : 0;
+                cnt[j][1] += a[j].y <= t ? 1 : 0;
+                cnt[j][2] += a[j].z <= t ? 1 : 0;
+                cnt[j][3] += a[j].w <= t ? 1 : 0;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kIndexQuads; ++j) {
+            const int64_t q = t0 + threadIdx.x + kBlock * j;
+            if (q < nquad) {
+                const uint32_t packed = index_from_count(a[j].x, cnt[j][0], K, zero) |
+                                        (index_from_count(a[j].y, cnt[j][1], K, zero) << 8) |
+                                        (index_from_count(a[j].z, cnt[j][2], K, zero) << 16) |
+                                        (index_from_count(a[j].w, cnt[j][3], K, zero) << 24);
+                *reinterpret_cast<uint32_t*>(idx + (q << 2)) = packed;
+            }
+        }
+    }
+    const int64_t t = (nquad << 2) + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (blockIdx.x == 0 && t < d) {
+        const float x = amax[t];
+        int32_t count = 0;
+        for (int k = 0; k < K; ++k)
+            count += x <= thr_s[k] ? 1 : 0;
+        idx[t] = static_cast<uint8_t>(index_from_count(x, count, K, zero));
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Quantisation.  One thread handles a group of 8 consecutive coordinates,
 // which is exactly one Philox block: its eight 16-bit halves are the high
 // halves of the coordinates' uniform words (coordinate j < 4 takes the low
@@ -757,8 +1057,31 @@ static unsigned one_shot(int64_t units, int64_t per_block)
 }
 
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
-                               float* w, uint8_t* idx, double* part, hipStream_t stream)
+                               float* w, uint8_t* idx, void* ws, hipStream_t stream)
 {
+    if (use_fused(d, M, S.K)) {
+        const NormPlan plan = fused_plan(d);
+        const FusedLayout L = fused_layout(d, M);
+        double* part = static_cast<double*>(ws);
+        double* rows = reinterpret_cast<double*>(static_cast<char*>(ws) + L.rows_off);
+        float* amax = reinterpret_cast<float*>(static_cast<char*>(ws) + L.amax_off);
+        const dim3 grid(static_cast<unsigned>(plan.nchunks));
+        if (M <= 4)
+            hipLaunchKernelGGL(k_norm_max<4>, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,
+                               plan.nchunks, part, amax);
+        else if (M <= 8)
+            hipLaunchKernelGGL(k_norm_max<8>, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,
+                               plan.nchunks, part, amax);
+        else
+            hipLaunchKernelGGL(k_norm_max<kFuseRows>, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,
+                               plan.nchunks, part, amax);
+        hipLaunchKernelGGL(k_rowsum, dim3(static_cast<unsigned>(M)), dim3(kBlock), 0, stream, part, plan.nchunks,
+                           rows);
+        const unsigned gx = one_shot((d + 3) / 4, kIndexTile);
+        hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, amax, d, M, rows, w, S, idx);
+        return hipGetLastError();
+    }
+    double* part = static_cast<double*>(ws);
     const NormPlan plan = norm_plan(d);
     if (plan.nchunks > 0) {
         // rows beyond kMaxBlocks / nchunks are taken in turn by the same blocks

@@ -28,12 +28,62 @@ inline NormPlan norm_plan(int64_t d)
     return p;
 }
 
+// Several scales and at most kFuseRows rows: one pass over the gradients
+// yields both the rows' sums of squares and the largest |g| over the rows at
+// every coordinate (the input of the scale index), so the gradients are read
+// once instead of twice.  Its reduction tree: chunks of 2048 * ceil(d / 2^24)
+// coordinates (a multiple of 2048, 16-byte aligned starts), at most 8192 per
+// row; it depends on d only.
+constexpr int32_t kFuseRows = 16;
+
+inline NormPlan fused_plan(int64_t d)
+{
+    const int64_t base = 2048;
+    const int64_t per = base * 8192;
+    const int64_t mult = d > 0 ? (d + per - 1) / per : 1;
+    NormPlan p;
+    p.chunk = base * mult;
+    p.nchunks = static_cast<int32_t>(d > 0 ? (d + p.chunk - 1) / p.chunk : 0);
+    return p;
+}
+
+// Workspace of the fused path, in bytes from the start of the workspace:
+// chunk partials [M][nchunks] fp64, row sums [M] fp64, row maxima [d] fp32
+// followed by one spare quad (a harmless target for masked-off stores).
+struct FusedLayout {
+    size_t rows_off;
+    size_t amax_off;
+    size_t bytes;
+};
+
+inline size_t align256(size_t n)
+{
+    return (n + 255) / 256 * 256;
+}
+
+inline FusedLayout fused_layout(int64_t d, int32_t M)
+{
+    const NormPlan p = fused_plan(d);
+    FusedLayout L;
+    L.rows_off = align256(static_cast<size_t>(M) * static_cast<size_t>(p.nchunks) * sizeof(double));
+    L.amax_off = L.rows_off + align256(static_cast<size_t>(M) * sizeof(double));
+    L.bytes = L.amax_off + align256(static_cast<size_t>((d + 3) / 4 * 4 + 4) * sizeof(float));
+    return L;
+}
+
+inline bool use_fused(int64_t d, int32_t M, int32_t K)
+{
+    return K > 1 && d > 0 && M <= kFuseRows;
+}
+
 // Upper bound on blocks for the grid-stride kernels: 64 blocks of 256
 // threads per compute unit of the current device.
 int64_t grid_cap();
 
+// ws: at least uq_workspace_bytes(d, M) bytes (norm partials, or the fused
+// path's layout)
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
-                               float* w, uint8_t* idx, double* part, hipStream_t stream);
+                               float* w, uint8_t* idx, void* ws, hipStream_t stream);
 // bits = 8: int8 codes [rows][ldc]; bits = 4 or 2: packed codes, ldc in bytes
 hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
                            const float* w, const ScaleSet& S, const uint8_t* idx, uint64_t seed,

@@ -62,10 +62,16 @@ def test_strerror_and_workspace():
         assert uq.uq_strerror(status) not in ("success", "unknown status")
     assert uq.uq_strerror(12345) == "unknown status"
     assert uq.uq_workspace_bytes(0, 1) >= 8
-    for d, M in ((1, 1), (2 ** 20, 4), (11_173_962, 8), (2 ** 30, 16)):
+    for d, M in ((1, 1), (2 ** 20, 4), (11_173_962, 8), (2 ** 30, 16), (2 ** 30, 17), (5, 300)):
         b = uq.uq_workspace_bytes(d, M)
         assert b % 256 == 0 and b >= 8 * M
-    assert uq.uq_workspace_bytes(2 ** 30, 16) <= 16 * 1024 * 8 + 256
+        if M <= 16:
+            # several scales with at most 16 rows: d fp32 row maxima, at most
+            # 8192 fp64 partials per row and M row sums
+            assert 4 * d <= b <= 4 * d + 8 * M * 8192 + 8 * M + 4 * 256
+        else:
+            assert b <= 8 * M * 1024 + 256
+    assert uq.uq_workspace_bytes(2 ** 30, 17) <= 17 * 1024 * 8 + 256
 
 
 def _hs(vals):
