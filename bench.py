@@ -46,7 +46,7 @@ def quantize_bytes_per_launch(d: int, rows: int, K: int, bits: int = 8) -> int:
 
 def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> dict:
     """Bytes each stage must move at minimum (reads + writes), per step.  With
-    several scales and at most 16 workers the norm pass also writes the
+    several scales and 2 to 16 workers the norm pass also writes the
     largest |g| over the workers (4 bytes per coordinate), which the index
     pass reads instead of the gradients; with more workers the index pass
     reads every gradient again."""
@@ -54,7 +54,7 @@ def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> 
     cb = code_bytes(d, bits)
     if not multi:
         scale_bytes = 4 * M * d
-    elif M <= FUSED_MAX_ROWS:
+    elif 2 <= M <= FUSED_MAX_ROWS:
         scale_bytes = 4 * M * d + 4 * d + 4 * d + d
     else:
         scale_bytes = 4 * M * d + 4 * M * d + d

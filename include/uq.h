@@ -50,7 +50,7 @@
  *   Reconstruction (Eq. (9) / Eq. (13) with 1/M): out_i = RN32(sum_i * deq_k).
  *   The norm is an fp64 sum of exact fp32 squares in a fixed order that
  *   depends only on d and on the pass that forms it (one scale or more than
- *   16 rows: the norm pass alone; several scales and at most 16 rows: the
+ *   16 rows or one row: the norm pass alone; several scales and 2 to 16 rows: the
  *   pass that also takes the rows' maxima), so W is deterministic; it can
  *   differ from a sequential fp64 sum by at most one binary32 ulp.
  */
@@ -93,7 +93,7 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg,
                     void* ws, size_t ws_bytes, void* stream);
 
 /* Workspace bytes uq_shared_scale needs for (d, M) and any K; 0 never
- * returned.  With M <= 16 this includes 4 * d bytes: with several scales the
+ * returned.  With 2 <= M <= 16 this includes 4 * d bytes: with several scales the
  * norm pass also keeps the largest |g| over the rows at every coordinate, so
  * that the index pass need not read the gradients again. */
 size_t uq_workspace_bytes(int64_t d, int32_t M);

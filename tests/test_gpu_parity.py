@@ -79,9 +79,10 @@ def test_small_shapes(d, scales):
 
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 8, 9, 16, 17, 300])
 def test_worker_counts(M):
-    """Up to 16 rows the shared scale with several scales takes the fused
+    """From 2 to 16 rows the shared scale with several scales takes the fused
     norm + row-maximum pass (4, 8 or 16 accumulators, exact or with rows to
-    spare); 17 and more take the separate norm and index passes."""
+    spare); one row, and 17 and more, take the separate norm and index
+    passes."""
     d = 12_345
     host = synth.gaussian_rows(M, d, seed=M, ldg=synth.round_up(d, 64))
     for scales in (S_SINGLE, S_MULTI4):
