@@ -368,7 +368,7 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const double* p = part + static_cast<int64_t>(blockIdx.x) * nchunks;
-    // nchunks <= 8192: at most 32 partials per thread, 16 loads in flight at a time
+    // nchunks <= 65536: at most 256 partials per thread, 16 loads in flight at a time
     double s = 0.0;
     for (int32_t j0 = 0; j0 < nchunks; j0 += 16 * kBlock) {
         double x[16];
