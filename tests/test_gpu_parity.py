@@ -163,6 +163,46 @@ def test_zero_gradients():
             assert np.all(res["idx"] == len(scales) - 1)
 
 
+def _largest_passing(inv: np.float32, s0: np.float32) -> np.float32:
+    """Largest binary32 a with RN32(a * inv) <= s0, by stepping ulps from s0 / inv."""
+    a = np.float32(np.float64(s0) / np.float64(inv))
+    while np.float32(a * inv) > s0:
+        a = np.nextafter(a, np.float32(0))
+    while np.float32(np.nextafter(a, np.float32(np.inf)) * inv) <= s0:
+        a = np.nextafter(a, np.float32(np.inf))
+    return a
+
+
+@pytest.mark.parametrize("M", [4, 17])
+def test_index_at_scale_boundaries(M):
+    """Coordinates exactly at, and one ulp either side of, the largest |g|
+    each scale k >= 1 admits (RN32(|g| inv_k) <= s_0), with W fixed by a
+    one-hot row at a value that is not a power of two: the shared index
+    (M = 4: from the row maxima of the fused pass; M = 17: from the rows)
+    and everything after it match the oracle."""
+    scales = S_MULTI4
+    Wv = np.float32(0.7)
+    d = 4096 + 37
+    host = np.zeros((M, synth.round_up(d, 64)), dtype=np.float32)
+    host[0, 0] = Wv
+    rng = np.random.default_rng(M)
+    host[1:, :d] = (rng.standard_normal((M - 1, d)) * 1e-6).astype(np.float32)
+    col = 100
+    for k in range(1, len(scales)):
+        inv = np.float32(np.float64(np.float32(scales[k])) / np.float64(Wv))
+        T = _largest_passing(inv, np.float32(scales[0]))
+        for v in (T, np.nextafter(T, np.float32(0)), np.nextafter(T, np.float32(np.inf))):
+            for sign in (1, -1):
+                host[1 + (col % (M - 1)), col] = sign * v
+                col += 7
+    assert np.sqrt((host.astype(np.float64) ** 2).sum(axis=1)).max() == np.float64(Wv)
+    res, _, _ = gpu_step(host, d, scales, seed=5)
+    assert res["W"] == Wv
+    ref = assert_matches_oracle(res, host, d, scales, seed=5)
+    # the boundary coordinates really do split between neighbouring indices
+    assert len(set(ref["idx"][100:col:7].tolist())) >= 3
+
+
 @pytest.mark.parametrize("bad", [np.inf, -np.inf, np.nan])
 def test_non_finite_inputs_take_zero_path(bad):
     d, M = 999, 2
