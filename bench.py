@@ -326,11 +326,6 @@ def main() -> int:
     # -- per-stage times: each stage repeated back to back between two events
     # on the stream (its inputs are the previous stage's outputs, already in
     # place), so host launch overhead does not enter the figures
-    def mark():
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        return e
-
     def stage_time(fn, reps):
         return stage_ms_per_call(torch, stream, fn, reps)
 
@@ -348,16 +343,14 @@ def main() -> int:
 
     # -- dominant kernel (the quantiser): launches back to back between two
     # events on the stream it runs on, so the average is the kernel's own
-    # duration (the figure rocprofv3 reports for k_quantise)
+    # duration (the figure rocprofv3 reports for k_quantise); best of three
+    # rounds, as for the stages, so that a round in which the host stalled
+    # does not count idle time as kernel time
     reps = max(10, args.steps)
     rows_per_launch = 1 if streamed else M
     step.shared_scale(g)
-    a = mark()
-    for _ in range(reps):
-        step.quantize(g[:rows_per_launch], seed, rows=rows_per_launch)
-    b = mark()
-    torch.cuda.synchronize()
-    q_launch_ms = a.elapsed_time(b) / reps
+    q_launch_ms = stage_ms_per_call(
+        torch, stream, lambda: step.quantize(g[:rows_per_launch], seed, rows=rows_per_launch), reps)
     q_bytes_launch = quantize_bytes_per_launch(d, rows_per_launch, K, bits)
     achieved = q_bytes_launch / (q_launch_ms * 1e-3) / 1e9
     kernel_name = ("k_quantise_multi" if K > 1 else "k_quantise_single") + ("" if bits == 8 else f"_{bits}bit")
