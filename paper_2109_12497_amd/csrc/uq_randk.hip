@@ -19,8 +19,8 @@
 //      increasing order.  For K <= kRkSortMax each wave appends its
 //      selections to one of kRkShards staging lists (one atomic per wave
 //      with selections, spread over the shards' counters: device-scope
-//      atomics on one address serialise) and one block sorts the lists by
-//      buckets of the index range; for larger K contiguous per-block ranges
+//      atomics on one address serialise) and 64 blocks sort the lists, each
+//      one slice of the index range; for larger K contiguous per-block ranges
 //      are counted, the counts scanned, and each block writes its
 //      selections at its offset, ordered by wave ballots.
 // The key passes run persistent grids, four independent Philox blocks per
@@ -393,26 +393,32 @@ __device__ __forceinline__ uint32_t bucket_of(uint32_t i, double scale)
     return b < kRkBuckets ? b : kRkBuckets - 1u;
 }
 
-// One block: the K staged indices in increasing order.  The staging lists
-// are concatenated (thread t holds positions t, t + 1024, ...), the indices
-// binned into kRkBuckets buckets of the index range through LDS counters
-// (about K / kRkBuckets indices each), and every index is written at its
-// bucket's start plus its rank inside the bucket.
+// The K staged indices in increasing order, by kRkSlices blocks.  The index
+// range is cut into kRkBuckets buckets (a monotone map) and block j owns the
+// contiguous run of buckets j * kRkSliceBuckets .. + kRkSliceBuckets - 1.
+// Every block reads all staged indices (concatenated lists; thread t holds
+// positions t, t + 1024, ...), counts those in earlier slices (its output
+// offset), bins its own through LDS counters (about K / kRkBuckets per bucket)
+// and writes each at the offset plus its bucket's start plus its rank inside
+// the bucket (the indices are distinct).
+constexpr int kRkSlices = 64;
+constexpr int kRkSliceBuckets = kRkBuckets / kRkSlices;
+static_assert(kRkSliceBuckets == 64, "one wave scans a slice's buckets");
+
 __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace* __restrict__ ws,
                                                             uint32_t* __restrict__ sel, uint32_t K, int64_t d)
 {
     constexpr int kPer = kRkSortMax / kRkSortThreads;  // 16 items per thread
-    constexpr int kBPer = kRkBuckets / kRkSortThreads;  // 4 buckets per thread
     __shared__ uint32_t buf[kRkSortMax];
-    __shared__ uint32_t count[kRkBuckets];
-    __shared__ uint32_t start[kRkBuckets];
-    __shared__ uint32_t scratch[kRkSortThreads / 64];
+    __shared__ uint32_t count[kRkSliceBuckets];
+    __shared__ uint32_t start[kRkSliceBuckets];
+    __shared__ uint32_t wave_below[kRkSortThreads / 64];
     __shared__ uint32_t list_start[kRkShards + 1];
     const uint32_t t = threadIdx.x;
+    const uint32_t slice = blockIdx.x;
     const int lane = t & 63, wave = t >> 6;
-#pragma unroll
-    for (int k = 0; k < kBPer; ++k)
-        count[t * kBPer + k] = 0u;
+    if (t < kRkSliceBuckets)
+        count[t] = 0u;
     static_assert(kRkShards == 64, "one wave scans the list lengths");
     if (wave == 0) {
         const uint32_t len = ws->n_stage[lane][0];
@@ -450,62 +456,66 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
     }
     const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
     uint32_t bucket[kPer];
+    uint32_t below = 0u;
 #pragma unroll
     for (int r = 0; r < kPer; ++r) {
         bucket[r] = bucket_of(item[r], scale);
-        if (t + r * kRkSortThreads < K)
-            atomicAdd(&count[bucket[r]], 1u);
+        if (t + r * kRkSortThreads < K) {
+            const uint32_t s = bucket[r] / kRkSliceBuckets;
+            if (s < slice)
+                ++below;
+            else if (s == slice)
+                atomicAdd(&count[bucket[r] % kRkSliceBuckets], 1u);
+        }
     }
+    // indices in earlier slices: the block's output offset
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        below += __shfl_xor(below, off, 64);
+    if (lane == 0)
+        wave_below[wave] = below;
     __syncthreads();
-    // exclusive scan of the bucket counts (thread t owns buckets 4t .. 4t+3)
-    uint32_t c[kBPer];
-    uint32_t own = 0u;
+    uint32_t offset = 0u;
 #pragma unroll
-    for (int k = 0; k < kBPer; ++k) {
-        c[k] = count[t * kBPer + k];
-        own += c[k];
-    }
-    uint32_t x = own;
+    for (int v = 0; v < kRkSortThreads / 64; ++v)
+        offset += wave_below[v];
+    // exclusive scan of the slice's bucket counts (one wave, a bucket per lane)
+    if (wave == 0) {
+        const uint32_t c = count[lane];
+        uint32_t x = c;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(x, off, 64);
-        if (lane >= off)
-            x += y;
-    }
-    if (lane == 63)
-        scratch[wave] = x;
-    __syncthreads();
-    uint32_t run = x - own;
-    for (int v = 0; v < wave; ++v)
-        run += scratch[v];
-#pragma unroll
-    for (int k = 0; k < kBPer; ++k) {
-        start[t * kBPer + k] = run;
-        run += c[k];
-        count[t * kBPer + k] = 0u;  // reused as the bucket's fill cursor
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(x, off, 64);
+            if (lane >= off)
+                x += y;
+        }
+        start[lane] = x - c;
+        count[lane] = 0u;  // reused as the bucket's fill cursor
     }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kPer; ++r)
-        if (t + r * kRkSortThreads < K) {
-            const uint32_t p = start[bucket[r]] + atomicAdd(&count[bucket[r]], 1u);
+        if (t + r * kRkSortThreads < K && bucket[r] / kRkSliceBuckets == slice) {
+            const uint32_t b = bucket[r] % kRkSliceBuckets;
+            const uint32_t p = start[b] + atomicAdd(&count[b], 1u);
             if (p < static_cast<uint32_t>(kRkSortMax))
                 buf[p] = item[r];
         }
     __syncthreads();
-    // each index goes to its bucket's start plus the number of smaller
-    // indices in its bucket (the indices are distinct)
+    // each index goes to the offset plus its bucket's start plus the number of
+    // smaller indices in its bucket
 #pragma unroll
     for (int r = 0; r < kPer; ++r)
-        if (t + r * kRkSortThreads < K) {
-            const uint32_t b = bucket[r], s0 = start[b];
+        if (t + r * kRkSortThreads < K && bucket[r] / kRkSliceBuckets == slice) {
+            const uint32_t b = bucket[r] % kRkSliceBuckets, s0 = start[b];
             const uint32_t room = static_cast<uint32_t>(kRkSortMax) - min(s0, static_cast<uint32_t>(kRkSortMax));
             const uint32_t n = min(count[b], room);
             uint32_t rank = 0u;
             for (uint32_t a = 0; a < n; ++a)
                 rank += buf[s0 + a] < item[r] ? 1u : 0u;
-            if (s0 + rank < K)
-                sel[s0 + rank] = item[r];
+            const uint32_t pos = offset + s0 + rank;
+            if (pos < K)
+                sel[pos] = item[r];
         }
 }
 
@@ -671,7 +681,8 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
     hipLaunchKernelGGL(k_rk_threshold, dim3(1), dim3(kRkSortThreads), 0, stream, ws);
     if (K <= kRkSortMax) {
         hipLaunchKernelGGL(k_rk_pick, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws, static_cast<uint32_t>(K));
-        hipLaunchKernelGGL(k_rk_sort, dim3(1), dim3(kRkSortThreads), 0, stream, ws, sel, static_cast<uint32_t>(K), d);
+        hipLaunchKernelGGL(k_rk_sort, dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
+                           static_cast<uint32_t>(K), d);
         return hipGetLastError();
     }
     // ordered compaction over contiguous chunks (a multiple of 1024 coordinates)
