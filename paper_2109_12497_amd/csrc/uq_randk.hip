@@ -16,13 +16,15 @@
 //      words (expected d / 2^20 of them, at most kRandkCandidates);
 //   5. one block ranks the candidates and takes the (key, index) threshold;
 //   6. the coordinates at or below the threshold (exactly K) are output in
-//      increasing order.  For K <= kRkSortMax each wave appends its
-//      selections to one of kRkShards staging lists (one atomic per wave
-//      with selections, spread over the shards' counters: device-scope
-//      atomics on one address serialise) and 64 blocks sort the lists, each
-//      one slice of the index range; for larger K contiguous per-block ranges
-//      are counted, the counts scanned, and each block writes its
-//      selections at its offset, ordered by wave ballots.
+//      increasing order.  For K <= kRkSortMax the keys below the boundary
+//      prefix are appended during pass 4 (each wave adds its selections to
+//      one of kRkShards staging lists with one atomic, spread over the
+//      shards' counters: device-scope atomics on one address serialise), the
+//      ranking block of step 5 appends the selected candidates, and 64
+//      blocks sort the lists, each one slice of the index range; for larger
+//      K contiguous per-block ranges are counted, the counts scanned, and
+//      each block writes its selections at its offset, ordered by wave
+//      ballots.
 // The key passes run persistent grids, four independent Philox blocks per
 // thread and iteration.
 #include <stdint.h>
@@ -228,10 +230,18 @@ __global__ __launch_bounds__(kBlock) void k_rk_scan2(RandkWorkspace* __restrict_
 }
 
 // Pass 3: collect the keys whose top 20 bits are (b1, b2), with low words.
+// With PICK (K <= kRkSortMax) the keys below that prefix, all selected, are
+// appended to the staging lists in the same pass: each wave adds its
+// selections of a key group to list (wave id mod kRkShards) with one atomic.
+template <bool PICK>
 __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0, uint32_t key1,
-                                                       RandkWorkspace* __restrict__ ws)
+                                                       RandkWorkspace* __restrict__ ws, uint32_t K)
 {
     const uint32_t prefix = (ws->ctl.b1 << 12) | ws->ctl.b2;
+    const int lane = threadIdx.x & 63;
+    const uint64_t below_lanes = (uint64_t(1) << lane) - 1u;
+    const uint32_t shard = (blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) % kRkShards;
+    uint32_t* list = ws->stage[shard];
     const int64_t nq = (d + 3) >> 2;
     const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock * kRkUnroll;
     for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kBlock * kRkUnroll + threadIdx.x; q0 < nq; q0 += step) {
@@ -242,9 +252,13 @@ __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0,
         const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
         const uint4 w = wu[u];
         bool any = false;
+        uint32_t take = 0u;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            any = any || (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix);
+        for (int j = 0; j < 4; ++j) {
+            const bool in = (q << 2) + j < d;
+            any = any || (in && (word_of(w, j) >> 12) == prefix);
+            take |= (PICK && in && (word_of(w, j) >> 12) < prefix) ? (1u << j) : 0u;
+        }
         if (any) {
             const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
 #pragma unroll
@@ -260,6 +274,29 @@ __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0,
                 }
             }
         }
+        if (PICK) {
+            uint32_t before = 0u, total = 0u;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint64_t bal = __ballot((take >> j) & 1u);
+                before += __popcll(bal & below_lanes);
+                total += __popcll(bal);
+            }
+            if (total != 0u) {  // wave-uniform
+                uint32_t base = 0u;
+                if (lane == 0)
+                    base = atomicAdd(&ws->n_stage[shard][0], total);
+                base = __shfl(base, 0, 64);
+                uint32_t pos = base + before;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if ((take >> j) & 1u) {
+                        if (pos < K)  // at most K in all lists together; the guard keeps writes in bounds
+                            list[pos] = static_cast<uint32_t>((q << 2) + j);
+                        ++pos;
+                    }
+            }
+        }
       }
     }
 }
@@ -273,7 +310,10 @@ __device__ __forceinline__ bool key_less(uint32_t ah, uint32_t al, uint32_t ai, 
 // One block: the candidate whose rank among the candidates (by hi, lo,
 // index; all distinct) is need2 - 1 is the threshold.  About d / 2^20
 // candidates are expected, so a direct count of smaller keys is cheapest.
-__global__ __launch_bounds__(kRkSortThreads) void k_rk_threshold(RandkWorkspace* __restrict__ ws)
+// With PICK the candidates of rank below need2 (the selected ones) are
+// appended to staging list 0.
+template <bool PICK>
+__global__ __launch_bounds__(kRkSortThreads) void k_rk_threshold(RandkWorkspace* __restrict__ ws, uint32_t K)
 {
     const uint32_t n = min(ws->ctl.n_cand, static_cast<uint32_t>(kRandkCandidates));
     const uint32_t want = ws->ctl.need2 - 1u;
@@ -286,6 +326,11 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_threshold(RandkWorkspace*
             ws->ctl.thr_hi = h;
             ws->ctl.thr_lo = l;
             ws->ctl.thr_idx = i;
+        }
+        if (PICK && rank <= want) {
+            const uint32_t pos = atomicAdd(&ws->n_stage[0][0], 1u);
+            if (pos < K)
+                ws->stage[0][pos] = i;
         }
     }
 }
@@ -312,75 +357,6 @@ __device__ __forceinline__ uint32_t selected_mask(int64_t q, int64_t d, uint32_t
         mask |= take ? (1u << j) : 0u;
     }
     return mask;
-}
-
-// Whether coordinate i = 4q + j is selected, from the hi words of its group
-// (the lo words are drawn only when a hi word equals the threshold's).
-__device__ __forceinline__ uint32_t selected_mask_hi(uint4 w, int64_t q, int64_t d, uint32_t key0, uint32_t key1,
-                                                     uint32_t th, uint32_t tl, uint32_t ti)
-{
-    bool tie = false;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        tie = tie || (((q << 2) + j < d) && word_of(w, j) == th);
-    uint4 l = make_uint4(0u, 0u, 0u, 0u);
-    if (tie)
-        l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
-    uint32_t mask = 0u;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int64_t i = (q << 2) + j;
-        const uint32_t hi = word_of(w, j);
-        const bool take = i < d && (hi < th || (hi == th && !key_less(th, tl, ti, hi, word_of(l, j),
-                                                                       static_cast<uint32_t>(i))));
-        mask |= take ? (1u << j) : 0u;
-    }
-    return mask;
-}
-
-// K <= kRkSortMax: every wave appends its selections (any order) to staging
-// list (wave id mod kRkShards) with one atomic on that list's length.  Each
-// list has room for all K selections, so none can overflow.
-__global__ __launch_bounds__(kBlock) void k_rk_pick(int64_t d, uint32_t key0, uint32_t key1,
-                                                    RandkWorkspace* __restrict__ ws, uint32_t K)
-{
-    const uint32_t th = ws->ctl.thr_hi, tl = ws->ctl.thr_lo, ti = ws->ctl.thr_idx;
-    const int lane = threadIdx.x & 63;
-    const uint64_t below = (uint64_t(1) << lane) - 1u;
-    const uint32_t shard = (blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) % kRkShards;
-    uint32_t* list = ws->stage[shard];
-    const int64_t nq = (d + 3) >> 2;
-    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock * kRkUnroll;
-    for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kBlock * kRkUnroll + threadIdx.x; q0 < nq; q0 += step) {
-        uint4 w[kRkUnroll];
-        key_blocks(q0, nq, 2u, key0, key1, w);
-#pragma unroll
-        for (int u = 0; u < kRkUnroll; ++u) {
-            const int64_t q = q0 + static_cast<int64_t>(u) * kBlock;
-            const uint32_t mask = q < nq ? selected_mask_hi(w[u], q, d, key0, key1, th, tl, ti) : 0u;
-            uint32_t before = 0u, total = 0u;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint64_t b = __ballot((mask >> j) & 1u);
-                before += __popcll(b & below);
-                total += __popcll(b);
-            }
-            if (total == 0u)
-                continue;  // wave-uniform
-            uint32_t base = 0u;
-            if (lane == 0)
-                base = atomicAdd(&ws->n_stage[shard][0], total);
-            base = __shfl(base, 0, 64);
-            uint32_t pos = base + before;
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if ((mask >> j) & 1u) {
-                    if (pos < K)  // at most K in all lists together; the guard keeps writes in bounds
-                        list[pos] = static_cast<uint32_t>((q << 2) + j);
-                    ++pos;
-                }
-        }
-    }
 }
 
 constexpr int kRkBuckets = 4 * kRkSortThreads;  // buckets of the index range in the sort
@@ -677,14 +653,21 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
                        ws);
     hipLaunchKernelGGL(k_rk_hist2, dim3(gx), dim3(kBlock), 0, stream, d, static_cast<uint32_t>(K), key0, key1, ws);
     hipLaunchKernelGGL(k_rk_scan2, dim3(1), dim3(kBlock), 0, stream, ws);
-    hipLaunchKernelGGL(k_rk_collect, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws);
-    hipLaunchKernelGGL(k_rk_threshold, dim3(1), dim3(kRkSortThreads), 0, stream, ws);
     if (K <= kRkSortMax) {
-        hipLaunchKernelGGL(k_rk_pick, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws, static_cast<uint32_t>(K));
+        // the collection pass also appends the keys below the boundary
+        // prefix; the threshold block appends the selected candidates
+        hipLaunchKernelGGL(k_rk_collect<true>, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
+                           static_cast<uint32_t>(K));
+        hipLaunchKernelGGL(k_rk_threshold<true>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
+                           static_cast<uint32_t>(K));
         hipLaunchKernelGGL(k_rk_sort, dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
                            static_cast<uint32_t>(K), d);
         return hipGetLastError();
     }
+    hipLaunchKernelGGL(k_rk_collect<false>, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
+                       static_cast<uint32_t>(K));
+    hipLaunchKernelGGL(k_rk_threshold<false>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
+                       static_cast<uint32_t>(K));
     // ordered compaction over contiguous chunks (a multiple of 1024 coordinates)
     const int64_t per_block = 1024;
     int64_t chunk = (d + kRkMaxBlocks - 1) / kRkMaxBlocks;
