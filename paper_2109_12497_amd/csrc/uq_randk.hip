@@ -372,77 +372,43 @@ __device__ __forceinline__ uint32_t bucket_of(uint32_t i, double scale)
 // The K staged indices in increasing order, by kRkSlices blocks.  The index
 // range is cut into kRkBuckets buckets (a monotone map) and block j owns the
 // contiguous run of buckets j * kRkSliceBuckets .. + kRkSliceBuckets - 1.
-// Every block reads all staged indices (concatenated lists; thread t holds
-// positions t, t + 1024, ...), counts those in earlier slices (its output
-// offset), bins its own through LDS counters (about K / kRkBuckets per bucket)
-// and writes each at the offset plus its bucket's start plus its rank inside
-// the bucket (the indices are distinct).
+// Every block reads all staged indices (16 threads per staging list), counts
+// those in earlier slices (its output offset) and bins its own through LDS
+// counters (about K / kRkBuckets per bucket); a second read places them by
+// bucket, and each is written at the offset plus its bucket's start plus its
+// rank inside the bucket (the indices are distinct).
 constexpr int kRkSlices = 64;
 constexpr int kRkSliceBuckets = kRkBuckets / kRkSlices;
 static_assert(kRkSliceBuckets == 64, "one wave scans a slice's buckets");
+static_assert(kRkShards * 16 == kRkSortThreads, "16 threads per staging list");
 
 __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace* __restrict__ ws,
                                                             uint32_t* __restrict__ sel, uint32_t K, int64_t d)
 {
-    constexpr int kPer = kRkSortMax / kRkSortThreads;  // 16 items per thread
     __shared__ uint32_t buf[kRkSortMax];
     __shared__ uint32_t count[kRkSliceBuckets];
     __shared__ uint32_t start[kRkSliceBuckets];
     __shared__ uint32_t wave_below[kRkSortThreads / 64];
-    __shared__ uint32_t list_start[kRkShards + 1];
+    __shared__ uint32_t n_mine;
     const uint32_t t = threadIdx.x;
     const uint32_t slice = blockIdx.x;
     const int lane = t & 63, wave = t >> 6;
     if (t < kRkSliceBuckets)
         count[t] = 0u;
-    static_assert(kRkShards == 64, "one wave scans the list lengths");
-    if (wave == 0) {
-        const uint32_t len = ws->n_stage[lane][0];
-        uint32_t x = len;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const uint32_t y = __shfl_up(x, off, 64);
-            if (lane >= off)
-                x += y;
-        }
-        list_start[lane] = x - len;
-        if (lane == 63)
-            list_start[kRkShards] = x;
-    }
-    __syncthreads();
-    // this thread's items, all loads issued before any is used
-    uint32_t item[kPer];
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-        const uint32_t j = t + r * kRkSortThreads;
-        uint32_t v = 0u;
-        if (j < K) {
-            // the list holding concatenated position j
-            int lo = 0, hi = kRkShards;  // list_start[lo] <= j < list_start[hi]
-            while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                if (list_start[mid] <= j)
-                    lo = mid;
-                else
-                    hi = mid;
-            }
-            v = ws->stage[lo][j - list_start[lo]];
-        }
-        item[r] = v;
-    }
+    const uint32_t* list = ws->stage[t >> 4];
+    const uint32_t len = min(ws->n_stage[t >> 4][0], static_cast<uint32_t>(kRkSortMax));
+    const uint32_t sub = t & 15u;
     const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
-    uint32_t bucket[kPer];
+    __syncthreads();
     uint32_t below = 0u;
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-        bucket[r] = bucket_of(item[r], scale);
-        if (t + r * kRkSortThreads < K) {
-            const uint32_t s = bucket[r] / kRkSliceBuckets;
-            if (s < slice)
-                ++below;
-            else if (s == slice)
-                atomicAdd(&count[bucket[r] % kRkSliceBuckets], 1u);
-        }
+#pragma unroll 4
+    for (uint32_t p = sub; p < len; p += 16u) {
+        const uint32_t b = bucket_of(list[p], scale);
+        const uint32_t sl = b / kRkSliceBuckets;
+        if (sl < slice)
+            ++below;
+        else if (sl == slice)
+            atomicAdd(&count[b % kRkSliceBuckets], 1u);
     }
     // indices in earlier slices: the block's output offset
 #pragma unroll
@@ -466,33 +432,38 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
                 x += y;
         }
         start[lane] = x - c;
+        if (lane == 63)
+            n_mine = x;
         count[lane] = 0u;  // reused as the bucket's fill cursor
     }
     __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kPer; ++r)
-        if (t + r * kRkSortThreads < K && bucket[r] / kRkSliceBuckets == slice) {
-            const uint32_t b = bucket[r] % kRkSliceBuckets;
-            const uint32_t p = start[b] + atomicAdd(&count[b], 1u);
-            if (p < static_cast<uint32_t>(kRkSortMax))
-                buf[p] = item[r];
+#pragma unroll 4
+    for (uint32_t p = sub; p < len; p += 16u) {
+        const uint32_t v = list[p];
+        const uint32_t b = bucket_of(v, scale);
+        if (b / kRkSliceBuckets == slice) {
+            const uint32_t lb = b % kRkSliceBuckets;
+            const uint32_t pos = start[lb] + atomicAdd(&count[lb], 1u);
+            if (pos < static_cast<uint32_t>(kRkSortMax))
+                buf[pos] = v;
         }
+    }
     __syncthreads();
-    // each index goes to the offset plus its bucket's start plus the number of
-    // smaller indices in its bucket
-#pragma unroll
-    for (int r = 0; r < kPer; ++r)
-        if (t + r * kRkSortThreads < K && bucket[r] / kRkSliceBuckets == slice) {
-            const uint32_t b = bucket[r] % kRkSliceBuckets, s0 = start[b];
-            const uint32_t room = static_cast<uint32_t>(kRkSortMax) - min(s0, static_cast<uint32_t>(kRkSortMax));
-            const uint32_t n = min(count[b], room);
-            uint32_t rank = 0u;
-            for (uint32_t a = 0; a < n; ++a)
-                rank += buf[s0 + a] < item[r] ? 1u : 0u;
-            const uint32_t pos = offset + s0 + rank;
-            if (pos < K)
-                sel[pos] = item[r];
-        }
+    // each of the slice's indices goes to the offset plus its bucket's start
+    // plus the number of smaller indices in its bucket
+    const uint32_t n = min(n_mine, static_cast<uint32_t>(kRkSortMax));
+    for (uint32_t e = t; e < n; e += kRkSortThreads) {
+        const uint32_t v = buf[e];
+        const uint32_t lb = bucket_of(v, scale) % kRkSliceBuckets;
+        const uint32_t s0 = start[lb];
+        const uint32_t m = min(count[lb], static_cast<uint32_t>(kRkSortMax) - min(s0, static_cast<uint32_t>(kRkSortMax)));
+        uint32_t rank = 0u;
+        for (uint32_t a = 0; a < m; ++a)
+            rank += buf[s0 + a] < v ? 1u : 0u;
+        const uint32_t pos = offset + s0 + rank;
+        if (pos < K)
+            sel[pos] = v;
+    }
 }
 
 // K > kRkSortMax: block b owns coordinates [b * chunk, (b + 1) * chunk); one
