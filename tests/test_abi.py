@@ -120,6 +120,18 @@ def test_shared_scale_rejects(kw, want):
     assert uq.uq_last_error() != ""
 
 
+@pytest.mark.parametrize("M", [1, 2, 8, 16, 17])
+def test_shared_scale_needs_the_full_workspace(M):
+    """The workspace of uq_workspace_bytes(d, M) covers any K; one 256-byte
+    line less is refused before anything is launched (with 2 to 16 rows the
+    size includes the 4 d bytes of row maxima of the fused pass)."""
+    d = 100_003
+    need = uq.uq_workspace_bytes(d, M)
+    assert (need >= 4 * d) == (2 <= M <= 16)
+    for K, scales, idx in ((1, S127, A), (4, S4, A)):
+        assert status_shared(d=d, M=M, ldg=100_032, scales=scales, K=K, idx=idx, ws_bytes=need - 256) == E["ws"]
+
+
 @pytest.mark.parametrize("kw,want", [
     (dict(s=0), "range"), (dict(s=128), "range"), (dict(g=None), "inval"), (dict(codes=None), "inval"),
     (dict(w=None), "inval"), (dict(d=-5), "inval"), (dict(rows=0), "inval"), (dict(rows=65536), "range"),
