@@ -56,6 +56,27 @@ def test_sum_row_groups(M, d, bits, scales):
     assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
 
 
+@pytest.mark.parametrize("bits,scales", [(4, [7.0]), (4, [7.0, 112.0, 1792.0]), (2, [1.0])])
+def test_packed_tightest_leading_dimensions(bits, scales):
+    """Packed rows padded only to a multiple of 16 bytes and gradient rows to a
+    multiple of 4 floats."""
+    d, M = 10_003, 9
+    ldg = 10_004
+    ldp = ((d * bits + 7) // 8 + 15) // 16 * 16
+    host = synth.mixed_rows(M, d, seed=bits + 60, ldg=ldg)
+    g = torch.from_numpy(host).to(DEV)
+    st = Step(d, M, scales, device=DEV, bits=bits, ldc=ldp)
+    assert st.codes.stride(0) == ldp
+    st.run(g, 27)
+    torch.cuda.synchronize()
+    ref = O.pipeline(host, scales, 27, d=d, W=np.float32(st.w[0].item()))
+    packed = st.codes[:, :(d * bits + 7) // 8].cpu().numpy()
+    for m in range(M):
+        assert np.array_equal(O.unpack_codes(packed[m], d, bits), ref["codes"][m]), m
+    assert np.array_equal(st.sum[:d].cpu().numpy(), ref["sum"])
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
 @pytest.mark.parametrize("bits,scales", [(4, [7.0]), (2, [1.0])])
 def test_packed_equals_int8_path(bits, scales):
     d, M = 300_001, 5

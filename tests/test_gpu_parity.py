@@ -101,6 +101,25 @@ def test_max_rows(d):
         assert_matches_oracle(res, host, d, scales, seed=99)
 
 
+@pytest.mark.parametrize("scales", [S_SINGLE, S_MULTI4], ids=["s127", "K4"])
+@pytest.mark.parametrize("M", [5, 17])
+def test_tightest_leading_dimensions(scales, M):
+    """Gradient rows padded only to a multiple of 4 floats and code rows only
+    to a multiple of 16 bytes, so that rows start at irregular addresses."""
+    d = 10_003
+    ldg, ldc = 10_004, 10_016
+    host = synth.mixed_rows(M, d, seed=M + 40, ldg=ldg)
+    g = torch.from_numpy(np.ascontiguousarray(host)).to(DEV)
+    assert g.stride(0) == ldg
+    step = Step(d, M, scales, device=DEV, ldc=ldc)
+    assert step.codes.stride(0) == ldc
+    step.run(g, 314)
+    torch.cuda.synchronize()
+    res = dict(W=np.float32(step.w[0].item()), sum=step.sum[:d].cpu().numpy(), out=step.out[:d].cpu().numpy(),
+               idx=None if step.idx is None else step.idx[:d].cpu().numpy(), codes=step.codes[:, :d].cpu().numpy())
+    assert_matches_oracle(res, host, d, scales, seed=314)
+
+
 def test_seed_high_word_and_worker_offset():
     d, M = 3001, 2
     host = synth.gaussian_rows(M, d, seed=5, ldg=3008)
