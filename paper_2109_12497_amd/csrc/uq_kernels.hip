@@ -441,7 +441,7 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
 #pragma unroll
     for (int j = 0; j < kIndexQuads; ++j) {
         const int64_t q = tile0 + threadIdx.x + kBlock * j;
-        a[j] = q < nquad ? *reinterpret_cast<const f32x4*>(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        a[j] = q < nquad ? load_nt(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
 
     // W = RN32(sqrt(max_m S_m)), NaN if any S_m is NaN (as k_finish): lane m
@@ -470,8 +470,7 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
 #pragma unroll
             for (int j = 0; j < kIndexQuads; ++j) {
                 const int64_t q = t0 + threadIdx.x + kBlock * j;
-                a[j] = q < nquad ? *reinterpret_cast<const f32x4*>(amax + (q << 2))
-                                 : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                a[j] = q < nquad ? load_nt(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
             }
         }
         int32_t cnt[kIndexQuads][4];
