@@ -224,6 +224,18 @@ int uq_gather(const float* g, int64_t d, int32_t M, int64_t ldg, const uint32_t*
  */
 int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, int64_t d, void* stream);
 
+/*
+ * Test hook, not part of the aggregation step: caps the grids of the
+ * streaming passes (norm, index, quantise, sum, reconstruction) at `blocks`
+ * blocks, 8 <= blocks <= 2^22; 0 restores the default 2^22 (the dispatch
+ * packet counts work-items in 32 bits).  The passes cover whatever their grid
+ * does not with grid-stride loops, which the default reaches only past about
+ * 2^33 coordinates; a lower cap lets tests run those loops at small sizes.
+ * Outputs do not depend on the cap.  Process-wide: set it only while no other
+ * thread issues library calls.  UQ_EINVAL for a value out of range.
+ */
+int uq_set_grid_cap(int64_t blocks);
+
 /* Static text for a status code. */
 const char* uq_strerror(int status);
 

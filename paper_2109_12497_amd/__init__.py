@@ -64,13 +64,14 @@ def _load() -> ctypes.CDLL:
     L.uq_randk_select.argtypes = [i64, i64, u64, P, P, sz, P]
     L.uq_gather.argtypes = [P, i64, i32, i64, P, i64, P, i64, P]
     L.uq_scatter.argtypes = [P, P, i64, P, i64, P]
+    L.uq_set_grid_cap.argtypes = [i64]
     L.uq_strerror.argtypes = [ctypes.c_int]
     L.uq_strerror.restype = ctypes.c_char_p
     L.uq_last_error.argtypes = []
     L.uq_last_error.restype = ctypes.c_char_p
     for name in ("uq_shared_scale", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
                  "uq_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_randk_select", "uq_gather",
-                 "uq_scatter"):
+                 "uq_scatter", "uq_set_grid_cap"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -112,6 +113,11 @@ class _HostScales:
 def _check(status: int) -> None:
     if status != UQ_OK:
         raise UQError(status, f"{lib.uq_strerror(status).decode()}: {lib.uq_last_error().decode()}")
+
+
+def uq_set_grid_cap(blocks: int) -> None:
+    """Test hook: cap the streaming passes' grids at `blocks` blocks (0: the default)."""
+    _check(lib.uq_set_grid_cap(blocks))
 
 
 def uq_workspace_bytes(d: int, M: int) -> int:

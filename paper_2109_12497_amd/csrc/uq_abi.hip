@@ -371,6 +371,14 @@ int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, in
     return launched(uq::launch_scatter(vals, sel, K, out, d, static_cast<hipStream_t>(stream)));
 }
 
+int uq_set_grid_cap(int64_t blocks)
+{
+    if (!uq::set_one_shot_cap(blocks))
+        return fail(UQ_EINVAL, "grid cap %lld is outside [%lld, 2^22] (0 restores the default)",
+                    (long long)blocks, (long long)uq::kMinOneShotCap);
+    return ok();
+}
+
 const char* uq_strerror(int status)
 {
     switch (status) {

@@ -14,6 +14,8 @@
 // Every per-coordinate result is a pure function of its inputs and the
 // coordinate index, so the output is independent of the launch geometry;
 // the norm's reduction tree depends only on d.
+#include <atomic>
+
 #include "uq_device.hpp"
 #include "uq_launch.hpp"
 
@@ -77,20 +79,23 @@ __global__ __launch_bounds__(kBlock) void k_sumsq(const float* __restrict__ g, i
 }
 
 // ---------------------------------------------------------------------------
-// Norm, pass 2 (one block): S_m = fixed-order sum of row m's chunk partials
-// (lane-strided sequential sums, then a fixed butterfly), one wave per row;
-// W = RN32(sqrt(max_m S_m)), NaN if any S_m is NaN.
+// Norm, pass 2 (one block of kFinishThreads): S_m = fixed-order sum of row m's
+// chunk partials (lane-strided sequential sums, then a fixed butterfly), one
+// wave per row (16 rows at once); W = RN32(sqrt(max_m S_m)), NaN if any S_m
+// is NaN.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_finish(const double* __restrict__ part, int32_t nchunks,
-                                                   int32_t M, float* __restrict__ w)
+constexpr int kFinishThreads = 1024;
+
+__global__ __launch_bounds__(kFinishThreads) void k_finish(const double* __restrict__ part, int32_t nchunks,
+                                                           int32_t M, float* __restrict__ w)
 {
-    __shared__ double wave_best[kBlock / 64];
-    __shared__ int wave_nan[kBlock / 64];
+    __shared__ double wave_best[kFinishThreads / 64];
+    __shared__ int wave_nan[kFinishThreads / 64];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     double best = 0.0;
     bool any_nan = false;
-    for (int32_t m = wave; m < M; m += kBlock / 64) {
+    for (int32_t m = wave; m < M; m += kFinishThreads / 64) {
         // nchunks <= 1024: at most 16 partials per lane, all loads in flight at once
         const double* p = part + static_cast<int64_t>(m) * nchunks;
         double x[16];
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(kBlock) void k_finish(const double* __restrict__ pa
     if (threadIdx.x == 0) {
         double b = 0.0;
         int nan = 0;
-        for (int i = 0; i < kBlock / 64; ++i) {
+        for (int i = 0; i < kFinishThreads / 64; ++i) {
             b = wave_best[i] > b ? wave_best[i] : b;
             nan |= wave_nan[i];
         }
@@ -711,14 +716,66 @@ __device__ __forceinline__ void tile_codes(const float v[8], const float inv[8],
     }
 }
 
-// The whole tiles of one code row.  inv_t / inv0 hold s_k / W, multiplied by
-// 2^16 when PRE (then s0x = s0 * 2^16 too), so that xs = x * 2^16 comes out of
-// one multiply and one min; without PRE (an entry is above 2^100, or
-// infinite) the 2^16 is applied after the min.  Both give
-// xs = RN(|v| s_k / W) * 2^16 exactly whenever |v| s_k / W is a normal
-// number, and T = floor(xs) = 0 with a zero threshold low half otherwise, so
-// the codes do not depend on PRE.  With one scale the wave's first tile
-// (`first`, if below ntiles) arrives already loaded in `in0`.
+// One tile of one code row: the codes from the lane's loaded inputs, then
+// the stores.  inv_t / inv0 hold s_k / W, multiplied by 2^16 when PRE (then
+// s0x = s0 * 2^16 too), so that xs = x * 2^16 comes out of one multiply and
+// one min; without PRE (an entry is above 2^100, or infinite) the 2^16 is
+// applied after the min.  Both give xs = RN(|v| s_k / W) * 2^16 exactly
+// whenever |v| s_k / W is a normal number, and T = floor(xs) = 0 with a zero
+// threshold low half otherwise, so the codes do not depend on PRE.
+template <bool MULTI, int BITS, bool PRE>
+__device__ __forceinline__ void code_tile(const TileIn& in, uint8_t* __restrict__ out, int64_t T,
+                                          const float* inv_t, float inv0, float s0x, uint32_t kmax,
+                                          uint32_t worker, uint32_t key0, uint32_t key1, uint32_t one2)
+{
+    const float v[8] = {in.A.x, in.A.y, in.A.z, in.A.w, in.B.x, in.B.y, in.B.z, in.B.w};
+    float inv[8];
+    if (MULTI) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            inv[j] = inv_t[min((in.ka >> (8 * j)) & 0xFFu, kmax)];
+            inv[j + 4] = inv_t[min((in.kb >> (8 * j)) & 0xFFu, kmax)];
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            inv[j] = inv0;
+    }
+    uint32_t p[4];
+    tile_codes<PRE>(v, inv, s0x, T, worker, key0, key1, one2, p);
+    const int64_t a_off = (T << 9) + 4 * (threadIdx.x & 63);
+    store_pairs<BITS>(out, a_off, p[0], p[1]);
+    store_pairs<BITS>(out, a_off + 256, p[2], p[3]);
+}
+
+// The whole tiles of one code row when the grid covers them all at once: the
+// wave's tile `first` and, with several scales and tpw = 2, first + 1, as
+// straight-line code.  With one scale (tpw = 1) the tile arrives already
+// loaded in `in0`.  The loop form below, run with the same tiles, measured
+// 9% slower with one scale and 1% slower with several (its 64-bit tile
+// bounds are compared on the vector unit).
+template <bool MULTI, int BITS, bool PRE>
+__device__ __forceinline__ void quantise_few(const float* __restrict__ row, uint8_t* __restrict__ out,
+                                             const uint8_t* __restrict__ idx, int64_t ntiles, int64_t first,
+                                             int32_t tpw, const TileIn& in0, const float* inv_t, float inv0,
+                                             float s0x, uint32_t kmax, uint32_t worker, uint32_t key0,
+                                             uint32_t key1)
+{
+    uint32_t one2 = 0x00010001u;
+    asm("" : "+s"(one2));
+    const int lane = threadIdx.x & 63;
+    if (first < ntiles) {
+        const TileIn in = MULTI ? load_tile<MULTI>(row, idx, (first << 9) + 4 * lane) : in0;
+        code_tile<MULTI, BITS, PRE>(in, out, first, inv_t, inv0, s0x, kmax, worker, key0, key1, one2);
+    }
+    if (MULTI && tpw == 2 && first + 1 < ntiles) {
+        const TileIn in = load_tile<MULTI>(row, idx, ((first + 1) << 9) + 4 * lane);
+        code_tile<MULTI, BITS, PRE>(in, out, first + 1, inv_t, inv0, s0x, kmax, worker, key0, key1, one2);
+    }
+}
+
+// The whole tiles of one code row on a capped grid: each wave takes `tpw`
+// consecutive tiles from `first`, then strides by the grid.
 template <bool MULTI, int BITS, bool PRE>
 __device__ __forceinline__ void quantise_tiles(const float* __restrict__ row, uint8_t* __restrict__ out,
                                                const uint8_t* __restrict__ idx, int64_t ntiles, int64_t first,
@@ -730,32 +787,11 @@ __device__ __forceinline__ void quantise_tiles(const float* __restrict__ row, ui
     uint32_t one2 = 0x00010001u;
     asm("" : "+s"(one2));
     for (int64_t c0 = first; c0 < ntiles; c0 += stride) {
-      const int64_t c1 = c0 + tpw < ntiles ? c0 + tpw : ntiles;
-      for (int64_t T = c0; T < c1; ++T) {
-        const int64_t a_off = (T << 9) + 4 * lane;
-        TileIn in;
-        if (!MULTI && T == first)
-            in = in0;
-        else
-            in = load_tile<MULTI>(row, idx, a_off);
-        const float v[8] = {in.A.x, in.A.y, in.A.z, in.A.w, in.B.x, in.B.y, in.B.z, in.B.w};
-        float inv[8];
-        if (MULTI) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                inv[j] = inv_t[min((in.ka >> (8 * j)) & 0xFFu, kmax)];
-                inv[j + 4] = inv_t[min((in.kb >> (8 * j)) & 0xFFu, kmax)];
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                inv[j] = inv0;
+        const int64_t c1 = c0 + tpw < ntiles ? c0 + tpw : ntiles;
+        for (int64_t T = c0; T < c1; ++T) {
+            const TileIn in = (!MULTI && T == first) ? in0 : load_tile<MULTI>(row, idx, (T << 9) + 4 * lane);
+            code_tile<MULTI, BITS, PRE>(in, out, T, inv_t, inv0, s0x, kmax, worker, key0, key1, one2);
         }
-        uint32_t p[4];
-        tile_codes<PRE>(v, inv, s0x, T, worker, key0, key1, one2, p);
-        store_pairs<BITS>(out, a_off, p[0], p[1]);
-        store_pairs<BITS>(out, a_off + 256, p[2], p[3]);
-      }
     }
 }
 
@@ -828,9 +864,10 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
 
     const float W = *wptr;
     // tables; on the zero path every entry is 0, which makes every code 0
-    const bool zero = zero_path(W, div_rn32(S.s[0], W));
+    const float q0 = div_rn32(S.s[0], W);
+    const bool zero = zero_path(W, q0);
     // the largest entry is the last scale's; 2^16 times it stays finite
-    const bool pre = zero || div_rn32(S.s_last, W) <= 0x1p100f;
+    const bool pre = zero || (MULTI ? div_rn32(S.s_last, W) : q0) <= 0x1p100f;
     float inv0 = 0.0f;
     if (MULTI) {
         if (threadIdx.x < S.K) {
@@ -840,12 +877,19 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
         }
         __syncthreads();
     } else {
-        inv0 = zero ? 0.0f : div_rn32(S.s[0], W);
+        inv0 = zero ? 0.0f : q0;
     }
     const float s0 = S.s[0];
     const uint32_t kmax = static_cast<uint32_t>(S.K - 1);
 
-    if (pre)
+    if (stride >= ntiles && tpw <= (MULTI ? 2 : 1)) {
+        if (pre)
+            quantise_few<MULTI, BITS, true>(row, out, idx, ntiles, first, tpw, in0, inv_p, inv0 * 65536.0f,
+                                            s0 * 65536.0f, kmax, worker, key0, key1);
+        else
+            quantise_few<MULTI, BITS, false>(row, out, idx, ntiles, first, tpw, in0, inv_p, inv0, s0, kmax,
+                                             worker, key0, key1);
+    } else if (pre)
         quantise_tiles<MULTI, BITS, true>(row, out, idx, ntiles, first, stride, in0, inv_p, inv0 * 65536.0f,
                                           s0 * 65536.0f, kmax, worker, key0, key1, tpw);
     else
@@ -1045,13 +1089,31 @@ static int32_t quantise_tiles_per_wave(int32_t K)
 // Enough blocks for every unit to get its own thread / wave / tile (the
 // streaming kernels run fastest as one pass with no grid-stride reuse).  The
 // dispatch packet counts work-items in 32 bits, so the grid is capped at 2^22
-// blocks; every kernel strides over whatever the grid does not cover.
+// blocks; every kernel strides over whatever the grid does not cover.  Tests
+// lower the cap to reach those strides at small sizes.
 constexpr int64_t kMaxBlocks = int64_t(1) << 22;
+static std::atomic<int64_t> g_one_shot_cap{kMaxBlocks};
+
+bool set_one_shot_cap(int64_t blocks)
+{
+    if (blocks == 0)
+        blocks = kMaxBlocks;
+    if (blocks < kMinOneShotCap || blocks > kMaxBlocks)
+        return false;
+    g_one_shot_cap.store(blocks, std::memory_order_relaxed);
+    return true;
+}
+
+static int64_t one_shot_cap()
+{
+    return g_one_shot_cap.load(std::memory_order_relaxed);
+}
 
 static unsigned one_shot(int64_t units, int64_t per_block)
 {
+    const int64_t cap = one_shot_cap();
     int64_t blocks = (units + per_block - 1) / per_block;
-    blocks = blocks < 1 ? 1 : (blocks > kMaxBlocks ? kMaxBlocks : blocks);
+    blocks = blocks < 1 ? 1 : (blocks > cap ? cap : blocks);
     return static_cast<unsigned>(blocks);
 }
 
@@ -1083,13 +1145,13 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
     double* part = static_cast<double*>(ws);
     const NormPlan plan = norm_plan(d);
     if (plan.nchunks > 0) {
-        // rows beyond kMaxBlocks / nchunks are taken in turn by the same blocks
-        int64_t gy = kMaxBlocks / plan.nchunks;
-        gy = gy > M ? M : gy;
+        // rows beyond the grid cap / nchunks are taken in turn by the same blocks
+        int64_t gy = one_shot_cap() / plan.nchunks;
+        gy = gy < 1 ? 1 : (gy > M ? M : gy);
         dim3 grid(static_cast<unsigned>(plan.nchunks), static_cast<unsigned>(gy));
         hipLaunchKernelGGL(k_sumsq, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk, plan.nchunks, part);
     }
-    hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, stream, part, plan.nchunks, M, w);
+    hipLaunchKernelGGL(k_finish, dim3(1), dim3(kFinishThreads), 0, stream, part, plan.nchunks, M, w);
     if (S.K > 1 && d > 0) {
         const unsigned gx = one_shot((d + 3) / 4, kBlock);
         hipLaunchKernelGGL(k_index, dim3(gx), dim3(kBlock), 0, stream, g, d, M, ldg, w, S, idx);
@@ -1108,8 +1170,8 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
     // `tpw` consecutive 512-coordinate tiles per wave, four waves per block
     const int32_t tpw = quantise_tiles_per_wave(S.K);
     unsigned tile_blocks = one_shot(d >> 9, (kBlock / 64) * tpw);
-    // keep rows x tile blocks within kMaxBlocks; the waves stride over the rest
-    const int64_t per_row = kMaxBlocks / rows / 8 * 8;
+    // keep rows x tile blocks within the grid cap; the waves stride over the rest
+    const int64_t per_row = one_shot_cap() / rows / 8 * 8;
     if (static_cast<int64_t>(tile_blocks) > per_row)
         tile_blocks = static_cast<unsigned>(per_row < 8 ? 8 : per_row);
     dim3 grid(tile_blocks, static_cast<unsigned>(rows));

@@ -83,6 +83,12 @@ inline bool use_fused(int64_t d, int32_t M, int32_t K)
 // threads per compute unit of the current device.
 int64_t grid_cap();
 
+// The cap on the one-shot grids of the streaming passes (norm, index,
+// quantise, sum, reconstruction): 2^22 blocks unless lowered, to no fewer than
+// kMinOneShotCap, by the test hook.  Returns false for a value out of range.
+constexpr int64_t kMinOneShotCap = 8;
+bool set_one_shot_cap(int64_t blocks);
+
 // ws: at least uq_workspace_bytes(d, M) bytes (norm partials, or the fused
 // path's layout)
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,

@@ -246,3 +246,17 @@ def test_sum_packed_rejects(kw, want):
     args.update(kw)
     assert L.uq_sum_packed(args["packed"], args["d"], args["rows"], args["ldp"], args["bits"], args["acc"],
                            args["sum_"], None) == E[want]
+
+
+@pytest.mark.parametrize("blocks", [-1, 1, 7, (1 << 22) + 1, 1 << 40])
+def test_grid_cap_rejects(blocks):
+    assert L.uq_set_grid_cap(blocks) == uq.UQ_EINVAL
+    assert b"grid cap" in L.uq_last_error()
+
+
+def test_grid_cap_accepts_the_range_and_restores():
+    for blocks in (8, 1000, 1 << 22, 0):
+        assert L.uq_set_grid_cap(blocks) == uq.UQ_OK
+    uq.uq_set_grid_cap(0)
+    with pytest.raises(uq.UQError):
+        uq.uq_set_grid_cap(3)

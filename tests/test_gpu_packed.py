@@ -43,6 +43,28 @@ def test_packed_matches_oracle(d, scales, bits):
     assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
 
 
+@pytest.mark.parametrize("scales,bits", [([7.0], 4), ([7.0, 112.0, 1792.0], 4), ([1.0], 2)],
+                         ids=["s7-4bit", "K3-4bit", "s1-2bit"])
+def test_packed_capped_grids(scales, bits):
+    """The packed quantiser and sum on a grid capped at 8 blocks (every
+    wave and block strides over several tiles), against the oracle."""
+    import paper_2109_12497_amd as uq
+
+    M, d = 5, 70_001
+    host = synth.mixed_rows(M, d, seed=bits + 3, ldg=synth.round_up(d, 64))
+    uq.uq_set_grid_cap(8)
+    try:
+        st = run(host, d, scales, bits, seed=23)
+    finally:
+        uq.uq_set_grid_cap(0)
+    ref = O.pipeline(host, scales, 23, d=d, W=np.float32(st.w[0].item()))
+    packed = st.codes[:, :(d * bits + 7) // 8].cpu().numpy()
+    for m in range(M):
+        assert np.array_equal(O.unpack_codes(packed[m], d, bits), ref["codes"][m]), m
+    assert np.array_equal(st.sum[:d].cpu().numpy(), ref["sum"])
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
 @pytest.mark.parametrize("M", [8, 11, 17])
 @pytest.mark.parametrize("d", [4095, 4096, 12_291])
 @pytest.mark.parametrize("bits,scales", [(8, [127.0]), (4, [7.0]), (2, [1.0])])

@@ -101,6 +101,25 @@ def test_max_rows(d):
         assert_matches_oracle(res, host, d, scales, seed=99)
 
 
+@pytest.mark.parametrize("cap", [8, 24, 1000])
+@pytest.mark.parametrize("M", [1, 3, 17])
+def test_capped_grids(cap, M):
+    """Every streaming pass on a grid capped far below its one-shot size, so
+    that its threads, waves and blocks stride over several units (the default
+    cap of 2^22 blocks binds only past about 2^33 coordinates); one row, the
+    fused pass's row counts and more than 16 rows.  The results must not
+    depend on the grid."""
+    d = 100_003
+    host = synth.mixed_rows(M, d, seed=M + cap, ldg=synth.round_up(d, 64))
+    uq.uq_set_grid_cap(cap)
+    try:
+        for scales in (S_SINGLE, S_MULTI4):
+            res, _, _ = gpu_step(host, d, scales, seed=cap + M)
+            assert_matches_oracle(res, host, d, scales, seed=cap + M)
+    finally:
+        uq.uq_set_grid_cap(0)
+
+
 @pytest.mark.parametrize("scales", [S_SINGLE, S_MULTI4], ids=["s127", "K4"])
 @pytest.mark.parametrize("M", [5, 17])
 def test_tightest_leading_dimensions(scales, M):
