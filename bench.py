@@ -49,7 +49,8 @@ def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> 
     several scales and 2 to 16 workers the norm pass also writes the
     largest |g| over the workers (4 bytes per coordinate), which the index
     pass reads instead of the gradients; with more workers the index pass
-    reads every gradient again."""
+    reads every gradient again.  The sum stores the int32 sums and, in the
+    same pass, the reconstruction (the sums are not read back)."""
     multi = K > 1
     cb = code_bytes(d, bits)
     if not multi:
@@ -62,8 +63,8 @@ def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> 
         "shared_scale": scale_bytes,
         "quantize": ((M * quantize_bytes_per_launch(d, 1, K, bits)) if streamed
                      else quantize_bytes_per_launch(d, M, K, bits)),
-        "sum": (M * cb + 4 * d) if not streamed else (cb + 4 * d) + (M - 1) * (cb + 8 * d),
-        "dequantize": d * (4 + 4 + (1 if multi else 0)),
+        "sum_dequantize": (((M * cb + 4 * d) if not streamed else (cb + 4 * d) + (M - 1) * (cb + 8 * d)) +
+                           d * (4 + (1 if multi else 0))),
     }
     b["total"] = sum(b.values())
     return b
@@ -332,13 +333,14 @@ def main() -> int:
     reps = stage_reps(args.steps, elapsed / args.steps)
     stage_ms = {"shared_scale": stage_time(lambda: step.shared_scale(g), reps)}
     if streamed:
-        # one worker row per call, M calls per step
+        # one worker row per call, M calls per step, the last of them fused
+        # with the reconstruction
         stage_ms["quantize"] = M * stage_time(lambda: step.quantize(g[:1], seed, rows=1), reps)
-        stage_ms["sum"] = M * stage_time(lambda: step.sum_codes(rows=1, accumulate=1), reps)
+        stage_ms["sum_dequantize"] = ((M - 1) * stage_time(lambda: step.sum_codes(rows=1, accumulate=1), reps) +
+                                      stage_time(lambda: step.sum_dequantize(rows=1, accumulate=1), reps))
     else:
         stage_ms["quantize"] = stage_time(lambda: step.quantize(g, seed), reps)
-        stage_ms["sum"] = stage_time(lambda: step.sum_codes(), reps)
-    stage_ms["dequantize"] = stage_time(lambda: step.dequantize(), reps)
+        stage_ms["sum_dequantize"] = stage_time(lambda: step.sum_dequantize(), reps)
     nbytes = algorithmic_bytes(d, M, K, streamed, bits)
 
     # -- dominant kernel (the quantiser): launches back to back between two

@@ -151,6 +151,20 @@ int uq_sum_codes(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int3
 int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w,
                   const float* scales, int32_t K, const uint8_t* idx, float* out, void* stream);
 
+/*
+ * uq_sum_codes (bits = 8) or uq_sum_packed (bits = 4 or 2) followed by
+ * uq_dequantize on the sums, in one pass: the same sum and out, bit for bit,
+ * without reading the sums back.  The reconstruction is applied to the
+ * stored sums, so with accumulate = 1 it sees the running total.
+ *   codes    [rows][ldc] int8 codes (bits = 8) or packed rows (bits = 4, 2)
+ *   sum      [d] int32 (written, or read and written)
+ *   M, w, scales, K, idx, out   as for uq_dequantize
+ * The checks of both calls apply.
+ */
+int uq_sum_dequantize(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t bits,
+                      int32_t accumulate, int32_t* sum, int32_t M, const float* w, const float* scales,
+                      int32_t K, const uint8_t* idx, float* out, void* stream);
+
 /* ------------------------------------------------------------------------
  * Sub-byte codes.  The paper stores every code in 8 bits because its
  * framework had no narrower type, and found bit-packing too slow (Sec. 5,

@@ -57,6 +57,7 @@ def _load() -> ctypes.CDLL:
     L.uq_quantize_multi.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, P, i64, P]
     L.uq_sum_codes.argtypes = [P, i64, i32, i64, i32, P, P]
     L.uq_dequantize.argtypes = [P, i64, i32, P, P, i32, P, P, P]
+    L.uq_sum_dequantize.argtypes = [P, i64, i32, i64, i32, i32, P, i32, P, P, i32, P, P, P]
     L.uq_quantize_packed.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i64, P]
     L.uq_sum_packed.argtypes = [P, i64, i32, i64, i32, i32, P, P]
     L.uq_randk_workspace_bytes.argtypes = [i64, i64]
@@ -70,7 +71,7 @@ def _load() -> ctypes.CDLL:
     L.uq_last_error.argtypes = []
     L.uq_last_error.restype = ctypes.c_char_p
     for name in ("uq_shared_scale", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
-                 "uq_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_randk_select", "uq_gather",
+                 "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_randk_select", "uq_gather",
                  "uq_scatter", "uq_set_grid_cap"):
         getattr(L, name).restype = ctypes.c_int
     return L
@@ -148,6 +149,12 @@ def uq_sum_codes(codes, d, rows, ldc, accumulate, sum, stream=None) -> None:
 def uq_dequantize(sum, d, M, w, scales, K, idx, out, stream=None) -> None:
     hs = _HostScales(scales)
     _check(lib.uq_dequantize(_ptr(sum), d, M, _ptr(w), hs.ptr, K, _ptr(idx), _ptr(out), _stream(stream)))
+
+
+def uq_sum_dequantize(codes, d, rows, ldc, bits, accumulate, sum, M, w, scales, K, idx, out, stream=None) -> None:
+    hs = _HostScales(scales)
+    _check(lib.uq_sum_dequantize(_ptr(codes), d, rows, ldc, bits, accumulate, _ptr(sum), M, _ptr(w), hs.ptr, K,
+                                 _ptr(idx), _ptr(out), _stream(stream)))
 
 
 def uq_quantize_packed(g, d, rows, ldg, worker0, w, scales, K, idx, seed, bits, packed, ldp, stream=None) -> None:

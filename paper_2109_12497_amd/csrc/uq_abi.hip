@@ -146,6 +146,44 @@ int launched(hipError_t e)
             return uq_rc_;            \
     } while (0)
 
+// The sum's arguments (bits = 8: int8 codes, ld in bytes >= d; 4 or 2:
+// packed rows of ceil(d * bits / 8) bytes).
+int check_sum(const void* codes, int64_t d, int32_t rows, int64_t ld, int32_t bits, int32_t accumulate,
+              const int32_t* sum)
+{
+    if (d < 0 || d > kMaxElems)
+        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
+    if (rows < 1)
+        return fail(UQ_EINVAL, "rows = %d is smaller than 1", rows);
+    if (rows > (1 << 24))
+        return fail(UQ_ERANGE, "rows = %d exceeds 2^24 (int32 sums could overflow)", rows);
+    if (accumulate != 0 && accumulate != 1)
+        return fail(UQ_EINVAL, "accumulate must be 0 or 1");
+    UQ_TRY(check_rows(codes, bits == 8 ? d : (d * bits + 7) / 8, rows, ld, 16, bits == 8 ? "codes" : "packed"));
+    return check_vec(sum, d, "sum");
+}
+
+// The reconstruction's arguments (d already checked); fills *S.
+int check_reconstruction(int64_t d, int32_t M, const float* w, const float* scales, int32_t K, const uint8_t* idx,
+                         const float* out, uq::ScaleSet* S)
+{
+    if (M < 1)
+        return fail(UQ_EINVAL, "M = %d is smaller than 1", M);
+    UQ_TRY(check_scales(scales, K, S));
+    if ((K == 1) != (idx == nullptr))
+        return fail(UQ_EINVAL, "idx must be NULL exactly when K == 1");
+    for (int32_t k = 0; k < K; ++k)
+        if (!exact_product(M, S->s[k]))
+            return fail(UQ_ERANGE, "M * scales[%d] = %d * %g is not exact in fp32", k, M, (double)S->s[k]);
+    if (static_cast<double>(M) * S->s[0] >= 2147483648.0)
+        return fail(UQ_ERANGE, "M * s_0 >= 2^31 (int32 sums could overflow)");
+    UQ_TRY(check_vec(out, d, "out"));
+    UQ_TRY(check_w(w));
+    if (K > 1)
+        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    return UQ_OK;
+}
+
 }  // namespace
 
 namespace uq {
@@ -269,16 +307,7 @@ int uq_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, i
 {
     if (bits != 4 && bits != 2)
         return fail(UQ_ERANGE, "bits = %d is not 4 or 2", bits);
-    if (d < 0 || d > kMaxElems)
-        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
-    if (rows < 1)
-        return fail(UQ_EINVAL, "rows = %d is smaller than 1", rows);
-    if (rows > (1 << 24))
-        return fail(UQ_ERANGE, "rows = %d exceeds 2^24 (int32 sums could overflow)", rows);
-    if (accumulate != 0 && accumulate != 1)
-        return fail(UQ_EINVAL, "accumulate must be 0 or 1");
-    UQ_TRY(check_rows(packed, (d * bits + 7) / 8, rows, ldp, 16, "packed"));
-    UQ_TRY(check_vec(sum, d, "sum"));
+    UQ_TRY(check_sum(packed, d, rows, ldp, bits, accumulate, sum));
     return launched(uq::launch_sum_packed(packed, d, rows, ldp, bits, accumulate, sum,
                                           static_cast<hipStream_t>(stream)));
 }
@@ -286,16 +315,7 @@ int uq_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, i
 int uq_sum_codes(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate, int32_t* sum,
                  void* stream)
 {
-    if (d < 0 || d > kMaxElems)
-        return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
-    if (rows < 1)
-        return fail(UQ_EINVAL, "rows = %d is smaller than 1", rows);
-    if (rows > (1 << 24))
-        return fail(UQ_ERANGE, "rows = %d exceeds 2^24 (int32 sums could overflow)", rows);
-    if (accumulate != 0 && accumulate != 1)
-        return fail(UQ_EINVAL, "accumulate must be 0 or 1");
-    UQ_TRY(check_rows(codes, d, rows, ldc, 16, "codes"));
-    UQ_TRY(check_vec(sum, d, "sum"));
+    UQ_TRY(check_sum(codes, d, rows, ldc, 8, accumulate, sum));
     return launched(uq::launch_sum(codes, d, rows, ldc, accumulate, sum, static_cast<hipStream_t>(stream)));
 }
 
@@ -304,23 +324,23 @@ int uq_dequantize(const int32_t* sum, int64_t d, int32_t M, const float* w, cons
 {
     if (d < 0 || d > kMaxElems)
         return fail(UQ_EINVAL, "d = %lld is out of range", (long long)d);
-    if (M < 1)
-        return fail(UQ_EINVAL, "M = %d is smaller than 1", M);
-    uq::ScaleSet S;
-    UQ_TRY(check_scales(scales, K, &S));
-    if ((K == 1) != (idx == nullptr))
-        return fail(UQ_EINVAL, "idx must be NULL exactly when K == 1");
-    for (int32_t k = 0; k < K; ++k)
-        if (!exact_product(M, S.s[k]))
-            return fail(UQ_ERANGE, "M * scales[%d] = %d * %g is not exact in fp32", k, M, (double)S.s[k]);
-    if (static_cast<double>(M) * S.s[0] >= 2147483648.0)
-        return fail(UQ_ERANGE, "M * s_0 >= 2^31 (int32 sums could overflow)");
     UQ_TRY(check_vec(sum, d, "sum"));
-    UQ_TRY(check_vec(out, d, "out"));
-    UQ_TRY(check_w(w));
-    if (K > 1)
-        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    uq::ScaleSet S;
+    UQ_TRY(check_reconstruction(d, M, w, scales, K, idx, out, &S));
     return launched(uq::launch_dequant(sum, d, M, w, S, idx, out, static_cast<hipStream_t>(stream)));
+}
+
+int uq_sum_dequantize(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t bits, int32_t accumulate,
+                      int32_t* sum, int32_t M, const float* w, const float* scales, int32_t K, const uint8_t* idx,
+                      float* out, void* stream)
+{
+    if (bits != 8 && bits != 4 && bits != 2)
+        return fail(UQ_ERANGE, "bits = %d is not 8, 4 or 2", bits);
+    UQ_TRY(check_sum(codes, d, rows, ldc, bits, accumulate, sum));
+    uq::ScaleSet S;
+    UQ_TRY(check_reconstruction(d, M, w, scales, K, idx, out, &S));
+    return launched(uq::launch_sum_dequant(codes, d, rows, ldc, bits, accumulate, sum, M, w, S, idx, out,
+                                           static_cast<hipStream_t>(stream)));
 }
 
 size_t uq_randk_workspace_bytes(int64_t d, int64_t K)

@@ -910,8 +910,19 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
 // flight at a time.  The tile's sums are then staged through LDS so that the
 // int32 stores (and, when accumulating, the loads of the old sums) are
 // coalesced: thread t writes quads t, t+256, t+512 and t+768 of the tile.
+// With DEQ (1: one scale, 2: several) the same threads also apply the
+// reconstruction to the sums they store, so that they need not be read again.
 // ---------------------------------------------------------------------------
 constexpr int64_t kSumTile = 4096;
+
+// The reconstruction's inputs when it is fused into the sum.
+struct DeqArgs {
+    const float* w;
+    const uint8_t* idx;  // [d] shared scale index (several scales)
+    float* out;
+    ScaleSet S;
+    int32_t M;
+};
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -945,17 +956,40 @@ __device__ __forceinline__ void add_fields(u32x4 w, int32_t acc[16])
     }
 }
 
-template <int BITS>
+template <int BITS, int DEQ>
 __global__ __launch_bounds__(kBlock) void k_sum(const uint8_t* __restrict__ codes, int64_t d, int32_t rows,
-                                                int64_t ldc, int32_t accumulate, int32_t* __restrict__ sum)
+                                                int64_t ldc, int32_t accumulate, int32_t* __restrict__ sum,
+                                                DeqArgs da)
 {
     constexpr int kRowsInFlight = 8;
     // the tile's sums with one padding word after every 16, so that both the
     // row-of-16 writes and the quad reads are free of bank conflicts
     __shared__ int32_t stage[kSumTile + kSumTile / 16];
+    __shared__ float deq_s[kMaxScales];
     const int t = threadIdx.x;
+    if (DEQ) {
+        // deq_k = RN32(W / (M s_k)) as in k_dequant; the barrier after the
+        // first tile's staging publishes them
+        const float W = *da.w;
+        const bool zero = zero_path(W, div_rn32(da.S.s[0], W));
+        if (t < da.S.K) {
+            const float denom = static_cast<float>(static_cast<double>(da.M) * static_cast<double>(da.S.s[t]));
+            deq_s[t] = zero ? 0.0f : div_rn32(W, denom);
+        }
+    }
+    const int32_t kmax = da.S.K - 1;
     for (int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSumTile; tile0 < d;
          tile0 += static_cast<int64_t>(gridDim.x) * kSumTile) {
+        // several scales: the index words of the thread's four quads
+        uint32_t kq[4] = {0u, 0u, 0u, 0u};
+        if (DEQ == 2) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int64_t q0 = tile0 + 1024 * c + 4 * t;
+                if (q0 + 4 <= d)
+                    kq[c] = *reinterpret_cast<const uint32_t*>(da.idx + q0);
+            }
+        }
         const int64_t c0 = tile0 + 16 * t;
         int32_t acc[16];
 #pragma unroll
@@ -994,9 +1028,32 @@ __global__ __launch_bounds__(kBlock) void k_sum(const uint8_t* __restrict__ code
                     a.x += o.x; a.y += o.y; a.z += o.z; a.w += o.w;
                 }
                 *reinterpret_cast<int4*>(sum + q0) = a;
+                if (DEQ) {
+                    f32x4 o;
+                    if (DEQ == 2) {
+                        const uint32_t kk = kq[c];
+                        o.x = static_cast<float>(a.x) * deq_s[min(static_cast<int32_t>(kk & 0xFFu), kmax)];
+                        o.y = static_cast<float>(a.y) * deq_s[min(static_cast<int32_t>((kk >> 8) & 0xFFu), kmax)];
+                        o.z = static_cast<float>(a.z) * deq_s[min(static_cast<int32_t>((kk >> 16) & 0xFFu), kmax)];
+                        o.w = static_cast<float>(a.w) * deq_s[min(static_cast<int32_t>(kk >> 24), kmax)];
+                    } else {
+                        const float f = deq_s[0];
+                        o.x = static_cast<float>(a.x) * f;
+                        o.y = static_cast<float>(a.y) * f;
+                        o.z = static_cast<float>(a.z) * f;
+                        o.w = static_cast<float>(a.w) * f;
+                    }
+                    store_nt(da.out + q0, o);
+                }
             } else {
-                for (int j = 0; j < 4 && q0 + j < d; ++j)
-                    sum[q0 + j] = stage[S + j] + (accumulate ? sum[q0 + j] : 0);
+                for (int j = 0; j < 4 && q0 + j < d; ++j) {
+                    const int32_t v = stage[S + j] + (accumulate ? sum[q0 + j] : 0);
+                    sum[q0 + j] = v;
+                    if (DEQ) {
+                        const int32_t k = DEQ == 2 ? min(static_cast<int32_t>(da.idx[q0 + j]), kmax) : 0;
+                        da.out[q0 + j] = static_cast<float>(v) * deq_s[k];
+                    }
+                }
             }
         }
         __syncthreads();  // the next tile reuses stage
@@ -1197,8 +1254,8 @@ hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc,
     if (d == 0)
         return hipSuccess;
     const unsigned gx = one_shot(d, kSumTile);
-    hipLaunchKernelGGL(k_sum<8>, dim3(gx), dim3(kBlock), 0, stream, reinterpret_cast<const uint8_t*>(codes), d,
-                       rows, ldc, accumulate, sum);
+    hipLaunchKernelGGL((k_sum<8, 0>), dim3(gx), dim3(kBlock), 0, stream, reinterpret_cast<const uint8_t*>(codes),
+                       d, rows, ldc, accumulate, sum, DeqArgs{});
     return hipGetLastError();
 }
 
@@ -1209,9 +1266,34 @@ hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int
         return hipSuccess;
     const unsigned gx = one_shot(d, kSumTile);
     if (bits == 4)
-        hipLaunchKernelGGL(k_sum<4>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
+        hipLaunchKernelGGL((k_sum<4, 0>), dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum,
+                           DeqArgs{});
     else
-        hipLaunchKernelGGL(k_sum<2>, dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum);
+        hipLaunchKernelGGL((k_sum<2, 0>), dim3(gx), dim3(kBlock), 0, stream, packed, d, rows, ldp, accumulate, sum,
+                           DeqArgs{});
+    return hipGetLastError();
+}
+
+hipError_t launch_sum_dequant(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t bits,
+                              int32_t accumulate, int32_t* sum, int32_t M, const float* w, const ScaleSet& S,
+                              const uint8_t* idx, float* out, hipStream_t stream)
+{
+    if (d == 0)
+        return hipSuccess;
+    const unsigned gx = one_shot(d, kSumTile);
+    const DeqArgs da{w, idx, out, S, M};
+#define UQ_LAUNCH_SUM_DEQ(BITS, DEQ)                                                                               \
+    hipLaunchKernelGGL((k_sum<BITS, DEQ>), dim3(gx), dim3(kBlock), 0, stream, codes, d, rows, ldc, accumulate, sum, \
+                       da)
+    const bool multi = S.K > 1;
+    if (bits == 8) {
+        if (multi) UQ_LAUNCH_SUM_DEQ(8, 2); else UQ_LAUNCH_SUM_DEQ(8, 1);
+    } else if (bits == 4) {
+        if (multi) UQ_LAUNCH_SUM_DEQ(4, 2); else UQ_LAUNCH_SUM_DEQ(4, 1);
+    } else {
+        if (multi) UQ_LAUNCH_SUM_DEQ(2, 2); else UQ_LAUNCH_SUM_DEQ(2, 1);
+    }
+#undef UQ_LAUNCH_SUM_DEQ
     return hipGetLastError();
 }
 

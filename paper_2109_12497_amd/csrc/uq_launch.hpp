@@ -101,6 +101,10 @@ hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int
                              int32_t accumulate, int32_t* sum, hipStream_t stream);
 hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,
                       int32_t* sum, hipStream_t stream);
+// the sum (bits = 8, 4 or 2) with the reconstruction applied to the sums it stores
+hipError_t launch_sum_dequant(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t bits,
+                              int32_t accumulate, int32_t* sum, int32_t M, const float* w, const ScaleSet& S,
+                              const uint8_t* idx, float* out, hipStream_t stream);
 // GlobalRandK: at most kRandkCandidates keys sharing the threshold's 20-bit
 // prefix are kept (expected d / 2^20 <= 4096 for d < 2^32, standard deviation
 // 64 at most).

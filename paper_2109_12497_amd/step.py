@@ -2,7 +2,8 @@
 
 `Step` owns the device buffers of a fixed problem shape and issues the
 library calls in the order of the algorithms (Sec. 3.1-3.2):
-shared scale (+ shared index) -> quantise -> integer sum -> reconstruct.
+shared scale (+ shared index) -> quantise -> integer sum -> reconstruct,
+the last two as one call (uq_sum_dequantize) unless fused=False.
 No arithmetic of the method happens here.
 """
 from __future__ import annotations
@@ -10,8 +11,8 @@ from __future__ import annotations
 import torch
 
 from . import (uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_packed, uq_quantize_single,
-               uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes, uq_sum_packed,
-               uq_workspace_bytes)
+               uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes,
+               uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
 
 
 def round_up(x: int, m: int) -> int:
@@ -25,11 +26,14 @@ class Step:
     summed by one call.  streamed=True: one code row is reused; each worker is
     quantised and accumulated into the int32 sum in turn.
     bits = 4 or 2: the codes are held packed ([M, ldc] bytes, ldc >= d*bits/8).
+    fused=True: the last sum call also reconstructs (uq_sum_dequantize);
+    False: uq_sum_codes / uq_sum_packed, then uq_dequantize.
     """
 
     def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None,
-                 bits: int = 8):
+                 bits: int = 8, fused: bool = True):
         self.d, self.M = d, M
+        self.fused = fused
         self.scales = [float(s) for s in scales]
         self.K = len(self.scales)
         self.streamed = streamed
@@ -77,6 +81,12 @@ class Step:
     def dequantize(self, stream=None):
         uq_dequantize(self.sum, self.d, self.M, self.w, self.scales, self.K, self.idx, self.out, stream)
 
+    def sum_dequantize(self, rows: int | None = None, accumulate: int = 0, codes=None, stream=None):
+        rows = self.M if rows is None else rows
+        codes = self.codes if codes is None else codes
+        uq_sum_dequantize(codes, self.d, rows, codes.stride(0), self.bits, accumulate, self.sum, self.M, self.w,
+                          self.scales, self.K, self.idx, self.out, stream)
+
     # -- the whole step ----------------------------------------------------------
     def run(self, g, seed: int, stream=None):
         """g: [M, ldg] float32 on the device.  Returns the output view [d]."""
@@ -86,11 +96,19 @@ class Step:
         if self.streamed:
             for m in range(self.M):
                 self.quantize(g[m:m + 1], seed, rows=1, worker0=m, stream=stream)
-                self.sum_codes(rows=1, accumulate=1 if m > 0 else 0, stream=stream)
+                acc = 1 if m > 0 else 0
+                if self.fused and m == self.M - 1:
+                    self.sum_dequantize(rows=1, accumulate=acc, stream=stream)
+                else:
+                    self.sum_codes(rows=1, accumulate=acc, stream=stream)
         else:
             self.quantize(g, seed, stream=stream)
-            self.sum_codes(stream=stream)
-        self.dequantize(stream)
+            if self.fused:
+                self.sum_dequantize(stream=stream)
+            else:
+                self.sum_codes(stream=stream)
+        if not self.fused:
+            self.dequantize(stream)
         return self.out[:self.d]
 
 

@@ -172,6 +172,28 @@ def test_dequantize_rejects(kw, want):
     assert status_deq(**kw) == E[want]
 
 
+def status_sumdeq(codes=A, d=100, rows=2, ldc=128, bits=8, acc=0, sum_=A, M=2, w=A, scales=S127, K=1, idx=None,
+                  out=A):
+    hs = uq._HostScales(scales)
+    return L.uq_sum_dequantize(codes, d, rows, ldc, bits, acc, sum_, M, w, hs.ptr, K, idx, out, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    # the sum's checks
+    (dict(codes=None), "inval"), (dict(sum_=None), "inval"), (dict(rows=0), "inval"),
+    (dict(rows=(1 << 24) + 1), "range"), (dict(acc=2), "inval"), (dict(ldc=120), "align"),
+    (dict(ldc=64), "inval"), (dict(sum_=A + 4), "align"), (dict(d=-1), "inval"),
+    (dict(bits=3), "range"), (dict(bits=16), "range"), (dict(bits=4, ldc=48), "inval"),
+    # the reconstruction's checks
+    (dict(out=None), "inval"), (dict(w=None), "inval"), (dict(M=0), "inval"), (dict(idx=A), "inval"),
+    (dict(K=4, scales=S4, idx=None), "inval"), (dict(out=A + 4), "align"),
+    (dict(M=3, K=2, scales=[7.0, 11184811.0], idx=A), "range"), (dict(M=20_000_000, scales=[127.0]), "range"),
+    (dict(K=4, scales=S4, idx=A + 2), "align"),
+])
+def test_sum_dequantize_rejects(kw, want):
+    assert status_sumdeq(**kw) == E[want]
+
+
 def test_binding_raises_with_detail():
     with pytest.raises(uq.UQError) as e:
         uq.uq_quantize_single(A, 100, 2, 128, 0, A, 200, 1, A, 128, stream=0)

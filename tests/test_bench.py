@@ -21,11 +21,13 @@ def per_coord(M, K, streamed=False, bits=8, d=1 << 20):
 
 @pytest.mark.parametrize("M", [1, 2, 8, 16, 17, 300])
 def test_step_bytes_per_coordinate(M):
-    # one scale: norm 4M, quantise 5M, sum M + 4, reconstruction 8
-    assert per_coord(M, 1) == 10 * M + 12
-    # several scales: the index read once by the quantiser; with 2 to 16
-    # workers the norm pass also writes the row maxima the index pass reads
-    want = 10 * M + 23 if 2 <= M <= bench.FUSED_MAX_ROWS else 14 * M + 15
+    # one scale: norm 4M, quantise 5M, sum M + 4 with the reconstruction's
+    # 4-byte output in the same pass
+    assert per_coord(M, 1) == 10 * M + 8
+    # several scales: the index read once by the quantiser and once by the
+    # sum's reconstruction; with 2 to 16 workers the norm pass also writes the
+    # row maxima the index pass reads
+    want = 10 * M + 19 if 2 <= M <= bench.FUSED_MAX_ROWS else 14 * M + 11
     assert per_coord(M, 4) == want
 
 
@@ -35,7 +37,8 @@ def test_streamed_and_packed_bytes():
     # quantise row by row (the index read by every launch), accumulate into
     # the int32 sum (set for the first row, += after)
     assert b["quantize"] == M * (5 * d + d)
-    assert b["sum"] == (d + 4 * d) + (M - 1) * (d + 8 * d)
+    # (and in the last call the output and the index for the reconstruction)
+    assert b["sum_dequantize"] == (d + 4 * d) + (M - 1) * (d + 8 * d) + 4 * d + d
     # 4-bit codes: half a byte per code written and read back
     assert bench.code_bytes(1001, 4) == 501 and bench.code_bytes(1001, 2) == 251
     assert bench.quantize_bytes_per_launch(1000, 3, 1, 4) == 3 * (4000 + 500)

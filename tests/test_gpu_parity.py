@@ -101,6 +101,53 @@ def test_max_rows(d):
         assert_matches_oracle(res, host, d, scales, seed=99)
 
 
+@pytest.mark.parametrize("scales,bits", [(S_SINGLE, 8), (S_MULTI4, 8), ([7.0], 4), ([7.0, 112.0, 1792.0], 4),
+                                         ([1.0], 2), ([1.0, 16.0], 2)],
+                         ids=["s127", "K4", "s7-4bit", "K3-4bit", "s1-2bit", "K2-2bit"])
+@pytest.mark.parametrize("d", [1, 5, 4095, 4097, 65_539])
+def test_fused_sum_reconstruction_equals_separate_calls(scales, bits, d):
+    """uq_sum_dequantize against the sum call followed by uq_dequantize: the
+    same sums and outputs bit for bit, when the sum is set and when three of
+    the five workers' rows are added to a running sum."""
+    M = 5
+    host = synth.mixed_rows(M, d, seed=d + bits, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(np.ascontiguousarray(host)).to(DEV)
+    sep = Step(d, M, scales, device=DEV, bits=bits, fused=False)
+    fus = Step(d, M, scales, device=DEV, bits=bits, fused=True)
+    sep.run(g, 5)
+    fus.run(g, 5)
+    torch.cuda.synchronize()
+    assert torch.equal(sep.codes, fus.codes)
+
+    def same():
+        assert torch.equal(sep.sum[:d], fus.sum[:d])
+        assert torch.equal(sep.out[:d].view(torch.int32), fus.out[:d].view(torch.int32))
+
+    same()
+    sep.sum_codes(rows=3, accumulate=1)
+    sep.dequantize()
+    fus.sum_dequantize(rows=3, accumulate=1)
+    torch.cuda.synchronize()
+    same()
+
+
+@pytest.mark.parametrize("streamed", [False, True], ids=["rows", "streamed"])
+@pytest.mark.parametrize("scales", [S_SINGLE, S_MULTI4], ids=["s127", "K4"])
+def test_separate_sum_and_reconstruction_match_oracle(scales, streamed):
+    """The step with the separate sum and reconstruction calls, against the oracle."""
+    M, d = 6, 20_011
+    host = synth.mixed_rows(M, d, seed=M + d, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(np.ascontiguousarray(host)).to(DEV)
+    step = Step(d, M, scales, device=DEV, streamed=streamed, fused=False)
+    step.run(g, 41)
+    torch.cuda.synchronize()
+    res = dict(W=np.float32(step.w[0].item()), sum=step.sum[:d].cpu().numpy(), out=step.out[:d].cpu().numpy(),
+               idx=None if step.idx is None else step.idx[:d].cpu().numpy())
+    if not streamed:
+        res["codes"] = step.codes[:, :d].cpu().numpy()
+    assert_matches_oracle(res, host, d, scales, seed=41)
+
+
 @pytest.mark.parametrize("cap", [8, 24, 1000])
 @pytest.mark.parametrize("M", [1, 3, 17])
 def test_capped_grids(cap, M):
