@@ -168,6 +168,24 @@ def test_capped_grids(cap, M):
 
 
 @pytest.mark.parametrize("scales", [S_SINGLE, S_MULTI4], ids=["s127", "K4"])
+def test_capped_grids_separate_sum_and_reconstruction(scales):
+    """The separate sum and reconstruction kernels on a grid capped at 8 blocks."""
+    M, d = 3, 70_001
+    host = synth.mixed_rows(M, d, seed=17, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(np.ascontiguousarray(host)).to(DEV)
+    uq.uq_set_grid_cap(8)
+    try:
+        step = Step(d, M, scales, device=DEV, fused=False)
+        step.run(g, 19)
+        torch.cuda.synchronize()
+    finally:
+        uq.uq_set_grid_cap(0)
+    res = dict(W=np.float32(step.w[0].item()), sum=step.sum[:d].cpu().numpy(), out=step.out[:d].cpu().numpy(),
+               idx=None if step.idx is None else step.idx[:d].cpu().numpy(), codes=step.codes[:, :d].cpu().numpy())
+    assert_matches_oracle(res, host, d, scales, seed=19)
+
+
+@pytest.mark.parametrize("scales", [S_SINGLE, S_MULTI4], ids=["s127", "K4"])
 @pytest.mark.parametrize("M", [5, 17])
 def test_tightest_leading_dimensions(scales, M):
     """Gradient rows padded only to a multiple of 4 floats and code rows only
