@@ -205,7 +205,7 @@ int uq_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, i
  * sampled coordinates (the paper's K), not a number of scales.
  * ------------------------------------------------------------------------ */
 
-/* Workspace bytes uq_randk_select needs (a fixed size, about 4.3 MiB). */
+/* Workspace bytes uq_randk_select needs (a fixed size, about 4.4 MiB). */
 size_t uq_randk_workspace_bytes(int64_t d, int64_t K);
 
 /*
@@ -249,6 +249,19 @@ int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, in
  * thread issues library calls.  UQ_EINVAL for a value out of range.
  */
 int uq_set_grid_cap(int64_t blocks);
+
+/*
+ * Test hook, not part of the aggregation step: how uq_randk_select finds the
+ * K-subset (for K <= 16384; larger K always use the histogram passes).
+ *   1  (default) one collection pass over a bracket of the K-th key computed
+ *      from d and K, with an exact fallback inside the selection when the
+ *      bracket misses (probability below 1e-20)
+ *   0  the histogram passes (two histograms, then the collection pass)
+ *   2  the bracket made to miss, so that the fallback always runs
+ * Every mode selects the same coordinates.  Process-wide: set it only while
+ * no other thread issues library calls.  UQ_EINVAL for another value.
+ */
+int uq_set_randk_mode(int32_t mode);
 
 /* Static text for a status code. */
 const char* uq_strerror(int status);

@@ -66,13 +66,14 @@ def _load() -> ctypes.CDLL:
     L.uq_gather.argtypes = [P, i64, i32, i64, P, i64, P, i64, P]
     L.uq_scatter.argtypes = [P, P, i64, P, i64, P]
     L.uq_set_grid_cap.argtypes = [i64]
+    L.uq_set_randk_mode.argtypes = [i32]
     L.uq_strerror.argtypes = [ctypes.c_int]
     L.uq_strerror.restype = ctypes.c_char_p
     L.uq_last_error.argtypes = []
     L.uq_last_error.restype = ctypes.c_char_p
     for name in ("uq_shared_scale", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
                  "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_randk_select", "uq_gather",
-                 "uq_scatter", "uq_set_grid_cap"):
+                 "uq_scatter", "uq_set_grid_cap", "uq_set_randk_mode"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -119,6 +120,11 @@ def _check(status: int) -> None:
 def uq_set_grid_cap(blocks: int) -> None:
     """Test hook: cap the streaming passes' grids at `blocks` blocks (0: the default)."""
     _check(lib.uq_set_grid_cap(blocks))
+
+
+def uq_set_randk_mode(mode: int) -> None:
+    """Test hook: 1 bracket (default), 0 histogram passes, 2 bracket forced to miss."""
+    _check(lib.uq_set_randk_mode(mode))
 
 
 def uq_workspace_bytes(d: int, M: int) -> int:

@@ -391,6 +391,13 @@ int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, in
     return launched(uq::launch_scatter(vals, sel, K, out, d, static_cast<hipStream_t>(stream)));
 }
 
+int uq_set_randk_mode(int32_t mode)
+{
+    if (!uq::set_randk_mode(mode))
+        return fail(UQ_EINVAL, "GlobalRandK mode %d is not 0, 1 or 2", mode);
+    return ok();
+}
+
 int uq_set_grid_cap(int64_t blocks)
 {
     if (!uq::set_one_shot_cap(blocks))

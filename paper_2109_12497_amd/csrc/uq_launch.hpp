@@ -111,6 +111,10 @@ hipError_t launch_sum_dequant(const uint8_t* codes, int64_t d, int32_t rows, int
 constexpr int kRandkCandidates = 8192;
 
 size_t randk_workspace_bytes();
+// How the K-subset is found (test hook): the bracket with its exact
+// fallback (default), the multi-pass histograms, or the bracket made to miss.
+constexpr int32_t kRandkBracket = 1, kRandkHistogram = 0, kRandkBracketMiss = 2;
+bool set_randk_mode(int32_t mode);
 hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, hipStream_t stream);
 hipError_t launch_gather(const float* g, int64_t d, int32_t M, int64_t ldg, const uint32_t* sel, int64_t K,
                          float* sub, int64_t lds, hipStream_t stream);

@@ -6,28 +6,42 @@
 // Selection.  Coordinate i has the 64-bit key (hi, lo): hi is word i%4 of
 // Philox block (i/4, 0, purpose 2), lo the same word of block (i/4, 0,
 // purpose 3).  The K coordinates with the smallest (hi, lo, i) are chosen.
-// Keys are regenerated in every pass (no key array in memory):
+// Keys are regenerated in every pass (no key array in memory).
+//
+// For K <= kRkSortMax the host first brackets the K-th key: hi is uniform, so
+// the count of keys below any x is binomial and an interval [x_lo, x_hi] of hi
+// ten standard deviations either side of K holds the K-th key except with
+// probability below 1e-20.  One pass over the keys appends every key below
+// x_lo to kRkShards staging lists (each wave adds its selections with one
+// atomic, spread over the lists' counters: device-scope atomics on one
+// address serialise) and collects the ~20 sqrt(K) keys inside the interval
+// with their low words; one block checks that the interval held the K-th key
+// and appends the smallest of them, and 64 blocks sort the lists, each one
+// slice of the index range.  Should the bracket miss, the one block computes
+// the exact selection itself with the steps below, so the result never
+// depends on it.
+//
+// The histogram passes (K > kRkSortMax, or by the test hook):
 //   1. per-block LDS histograms of hi >> 24 (256 bins), merged with atomics;
 //   2. every block of the next pass finds the bin b1 holding the K-th key
 //      (and how many of its keys are still needed) from that histogram, and
 //      keys in bin b1 histogram (hi >> 12) & 0xFFF (global atomics);
 //   3. one block finds the sub-bin b2;
 //   4. keys whose top 20 bits are (b1, b2) are collected with their low
-//      words (expected d / 2^20 of them, at most kRandkCandidates);
+//      words (expected d / 2^20 of them, at most kRandkCandidates), and for
+//      K <= kRkSortMax the keys below that prefix are staged as above;
 //   5. one block ranks the candidates and takes the (key, index) threshold;
 //   6. the coordinates at or below the threshold (exactly K) are output in
-//      increasing order.  For K <= kRkSortMax the keys below the boundary
-//      prefix are appended during pass 4 (each wave adds its selections to
-//      one of kRkShards staging lists with one atomic, spread over the
-//      shards' counters: device-scope atomics on one address serialise), the
-//      ranking block of step 5 appends the selected candidates, and 64
-//      blocks sort the lists, each one slice of the index range; for larger
-//      K contiguous per-block ranges are counted, the counts scanned, and
-//      each block writes its selections at its offset, ordered by wave
-//      ballots.
+//      increasing order: by the sort above, or for larger K contiguous
+//      per-block ranges are counted, the counts scanned, and each block
+//      writes its selections at its offset, ordered by wave ballots.
 // The key passes run persistent grids, four independent Philox blocks per
 // thread and iteration.
+#include <stddef.h>
 #include <stdint.h>
+
+#include <atomic>
+#include <cmath>
 
 #include "uq_device.hpp"
 #include "uq_launch.hpp"
@@ -42,12 +56,14 @@ constexpr int kRkShards = 64;      // staging lists of the K <= kRkSortMax path
 constexpr int kRkUnroll = 4;       // Philox blocks per thread and iteration
 constexpr int kRkCopies = 16;      // level-1 histogram copies the blocks merge into
 constexpr int kRkLine = 64;        // uint32 per 256-byte line: one atomic counter per line
+constexpr int kRkShardCand = 256;  // bracket candidates per staging list
 
 struct RandkControl {
     uint32_t b1, need1, b2, need2;  // bins found by the two scans
     uint32_t n_cand, pad0;          // candidate append counter
     uint32_t thr_hi, thr_lo, thr_idx;
-    uint32_t pad[7];
+    uint32_t x_lo, x_hi;            // collection interval of hi (inclusive)
+    uint32_t pad[5];
 };
 
 constexpr int kRkMaxBlocks = 2048;  // ordered-compaction blocks
@@ -64,6 +80,8 @@ struct RandkWorkspace {
     uint32_t block_offset[kRkMaxBlocks];
     uint32_t n_stage[kRkShards][kRkLine];     // staging list lengths (element 0 of each line)
     uint32_t stage[kRkShards][kRkSortMax];    // unordered selections (K <= kRkSortMax)
+    uint32_t n_bcand[kRkShards][kRkLine];     // bracket candidates per list (element 0 of each line)
+    uint32_t bcand[kRkShards][kRkShardCand][3];  // (hi, lo, index)
 };
 
 __device__ __forceinline__ uint4 selection_block(uint32_t q, uint32_t purpose, uint32_t key0, uint32_t key1)
@@ -128,16 +146,24 @@ __device__ __forceinline__ void find_bin(const uint32_t* hist, uint32_t need, ui
 }
 
 static_assert(kRkCopies * kRkBins1 == kRkBins2, "one zeroing loop covers both histograms");
-__global__ __launch_bounds__(kBlock) void k_rk_init(RandkWorkspace* __restrict__ ws)
+__global__ __launch_bounds__(kBlock) void k_rk_init(RandkWorkspace* __restrict__ ws, uint32_t x_lo, uint32_t x_hi)
 {
     for (int b = threadIdx.x; b < kRkBins2; b += kBlock) {
         reinterpret_cast<uint32_t*>(ws->hist1)[b] = 0u;  // kRkCopies * kRkBins1 == kRkBins2
         ws->hist2[b] = 0u;
     }
-    if (threadIdx.x < sizeof(RandkControl) / 4)
-        reinterpret_cast<uint32_t*>(&ws->ctl)[threadIdx.x] = 0u;
-    if (threadIdx.x < kRkShards)
+    if (threadIdx.x < sizeof(RandkControl) / 4) {
+        uint32_t v = 0u;
+        if (threadIdx.x == offsetof(RandkControl, x_lo) / 4)
+            v = x_lo;
+        if (threadIdx.x == offsetof(RandkControl, x_hi) / 4)
+            v = x_hi;
+        reinterpret_cast<uint32_t*>(&ws->ctl)[threadIdx.x] = v;
+    }
+    if (threadIdx.x < kRkShards) {
         ws->n_stage[threadIdx.x][0] = 0u;
+        ws->n_bcand[threadIdx.x][0] = 0u;
+    }
 }
 
 // The kRkUnroll key groups q0 + u * kBlock (u < kRkUnroll) of one thread and
@@ -222,22 +248,34 @@ __global__ __launch_bounds__(kBlock) void k_rk_hist2(int64_t d, uint32_t K, uint
     }
 }
 
-// One block: the level-2 sub-bin b2 holding the need1-th key of bin b1.
+// One block: the level-2 sub-bin b2 holding the need1-th key of bin b1; the
+// collection interval is the keys with that 20-bit prefix.
 __global__ __launch_bounds__(kBlock) void k_rk_scan2(RandkWorkspace* __restrict__ ws)
 {
     __shared__ uint32_t scratch[kBlock / 64];
-    find_bin<kRkBins2 / kBlock>(ws->hist2, ws->ctl.need1, scratch, &ws->ctl.b2, &ws->ctl.need2);
+    __shared__ uint32_t found[2];
+    find_bin<kRkBins2 / kBlock>(ws->hist2, ws->ctl.need1, scratch, &found[0], &found[1]);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        ws->ctl.b2 = found[0];
+        ws->ctl.need2 = found[1];
+        ws->ctl.x_lo = (ws->ctl.b1 << 24) | (found[0] << 12);
+        ws->ctl.x_hi = (ws->ctl.b1 << 24) | (found[0] << 12) | 0xFFFu;
+    }
 }
 
-// Pass 3: collect the keys whose top 20 bits are (b1, b2), with low words.
-// With PICK (K <= kRkSortMax) the keys below that prefix, all selected, are
-// appended to the staging lists in the same pass: each wave adds its
-// selections of a key group to list (wave id mod kRkShards) with one atomic.
-template <bool PICK>
+// Pass 3: collect the keys whose hi lies in [x_lo, x_hi], with low words.
+// With PICK (K <= kRkSortMax) the keys below x_lo are appended to the staging
+// lists in the same pass (all selected when the interval holds the K-th
+// key): each wave adds its selections of a key group to list (wave id mod
+// kRkShards) with one atomic.  SHARDED (the bracket, about 20 sqrt(K)
+// candidates) puts the candidates in per-list arrays, so that their append
+// counters are spread too; otherwise (d / 2^20 expected) they go to one list.
+template <bool PICK, bool SHARDED>
 __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0, uint32_t key1,
                                                        RandkWorkspace* __restrict__ ws, uint32_t K)
 {
-    const uint32_t prefix = (ws->ctl.b1 << 12) | ws->ctl.b2;
+    const uint32_t x_lo = ws->ctl.x_lo, x_hi = ws->ctl.x_hi;
     const int lane = threadIdx.x & 63;
     const uint64_t below_lanes = (uint64_t(1) << lane) - 1u;
     const uint32_t shard = (blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) % kRkShards;
@@ -256,20 +294,30 @@ __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0,
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const bool in = (q << 2) + j < d;
-            any = any || (in && (word_of(w, j) >> 12) == prefix);
-            take |= (PICK && in && (word_of(w, j) >> 12) < prefix) ? (1u << j) : 0u;
+            const uint32_t hi = word_of(w, j);
+            any = any || (in && hi >= x_lo && hi <= x_hi);
+            take |= (PICK && in && hi < x_lo) ? (1u << j) : 0u;
         }
         if (any) {
             const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int64_t i = (q << 2) + j;
-                if (i < d && (word_of(w, j) >> 12) == prefix) {
-                    const uint32_t slot = atomicAdd(&ws->ctl.n_cand, 1u);
-                    if (slot < static_cast<uint32_t>(kRandkCandidates)) {
-                        ws->cand[slot][0] = word_of(w, j);
-                        ws->cand[slot][1] = word_of(l, j);
-                        ws->cand[slot][2] = static_cast<uint32_t>(i);
+                if (i < d && word_of(w, j) >= x_lo && word_of(w, j) <= x_hi) {
+                    if (SHARDED) {
+                        const uint32_t slot = atomicAdd(&ws->n_bcand[shard][0], 1u);
+                        if (slot < static_cast<uint32_t>(kRkShardCand)) {
+                            ws->bcand[shard][slot][0] = word_of(w, j);
+                            ws->bcand[shard][slot][1] = word_of(l, j);
+                            ws->bcand[shard][slot][2] = static_cast<uint32_t>(i);
+                        }
+                    } else {
+                        const uint32_t slot = atomicAdd(&ws->ctl.n_cand, 1u);
+                        if (slot < static_cast<uint32_t>(kRandkCandidates)) {
+                            ws->cand[slot][0] = word_of(w, j);
+                            ws->cand[slot][1] = word_of(l, j);
+                            ws->cand[slot][2] = static_cast<uint32_t>(i);
+                        }
                     }
                 }
             }
@@ -357,6 +405,268 @@ __device__ __forceinline__ uint32_t selected_mask(int64_t q, int64_t d, uint32_t
         mask |= take ? (1u << j) : 0u;
     }
     return mask;
+}
+
+// ---------------------------------------------------------------------------
+// Selection by a bracket.  The number of keys with hi < x is binomial,
+// Binomial(d, x / 2^32), so the host can name an interval [x_lo, x_hi] of hi
+// that holds the K-th key except with probability below 1e-20 (ten standard
+// deviations either side); one collection pass then appends every key below
+// x_lo to the staging lists and gathers the roughly 20 sqrt(K) keys inside
+// the interval as candidates, and k_rk_pick completes the selection.  It
+// checks that the interval did hold the K-th key (fewer than K keys below it,
+// at least K at or below its top, every candidate kept); if not, it computes
+// the exact selection on its own, slowly, with the same histogram steps as the
+// multi-pass path, so the result never depends on the bracket.
+// ---------------------------------------------------------------------------
+constexpr int kRkPickBuckets = 2048;  // the interval cut into equal parts
+constexpr int kRkCross = 512;         // candidates of the crossing part kept in LDS
+constexpr int kRkPickMax = 4096;      // bracket candidates the selection block holds in LDS
+
+__device__ __forceinline__ uint32_t pick_bucket(uint32_t hi, uint32_t x_lo, uint64_t width)
+{
+    return static_cast<uint32_t>((static_cast<uint64_t>(hi - x_lo) * kRkPickBuckets) / width);
+}
+
+// Appends the set bits of `mask` (coordinates 4q + j) of every thread to
+// list 0 at positions *base + (block-wide exclusive count); every thread of
+// the block must call it; *base advances by the block's total.
+__device__ __forceinline__ void append_in_order(uint32_t mask, int64_t q, uint32_t* list, uint32_t* base,
+                                                uint32_t* scratch, uint32_t K)
+{
+    const uint32_t n = __builtin_popcount(mask);
+    const uint32_t incl = block_inclusive_scan(n, scratch);
+    uint32_t pos = *base + incl - n;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if ((mask >> j) & 1u) {
+            if (pos < K)
+                list[pos] = static_cast<uint32_t>((q << 2) + j);
+            ++pos;
+        }
+    // the block's total: the last thread's inclusive count
+    if (threadIdx.x == kBlock - 1)
+        scratch[kBlock / 64] = incl;
+    __syncthreads();
+    *base += scratch[kBlock / 64];
+    __syncthreads();
+}
+
+// The exact selection by one block (the bracket missed): level-1 and level-2
+// histograms in LDS, the candidates sharing the K-th key's 20-bit prefix
+// ranked for the threshold, then every selected coordinate appended to
+// list 0 (the other lists emptied).
+__device__ void pick_exact(int64_t d, uint32_t K, uint32_t key0, uint32_t key1, RandkWorkspace* __restrict__ ws,
+                           uint32_t* h, uint32_t* scratch, uint32_t* found)
+{
+    const int64_t nq = (d + 3) >> 2;
+    const int64_t step = static_cast<int64_t>(kBlock) * kRkUnroll;
+    // level 1
+    for (int b = threadIdx.x; b < kRkBins2; b += kBlock)
+        h[b] = 0u;
+    __syncthreads();
+    for (int64_t q0 = threadIdx.x; q0 < nq; q0 += step) {
+        uint4 w[kRkUnroll];
+        key_blocks(q0, nq, 2u, key0, key1, w);
+#pragma unroll
+        for (int u = 0; u < kRkUnroll; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (((q0 + static_cast<int64_t>(u) * kBlock) << 2) + j < d)
+                    atomicAdd(&h[word_of(w[u], j) >> 24], 1u);
+    }
+    __syncthreads();
+    find_bin<1>(h, K, scratch, &found[0], &found[1]);
+    __syncthreads();
+    const uint32_t b1 = found[0], need1 = found[1];
+    __syncthreads();
+    // level 2
+    for (int b = threadIdx.x; b < kRkBins2; b += kBlock)
+        h[b] = 0u;
+    __syncthreads();
+    for (int64_t q0 = threadIdx.x; q0 < nq; q0 += step) {
+        uint4 w[kRkUnroll];
+        key_blocks(q0, nq, 2u, key0, key1, w);
+#pragma unroll
+        for (int u = 0; u < kRkUnroll; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t hi = word_of(w[u], j);
+                if (((q0 + static_cast<int64_t>(u) * kBlock) << 2) + j < d && (hi >> 24) == b1)
+                    atomicAdd(&h[(hi >> 12) & 0xFFFu], 1u);
+            }
+    }
+    __syncthreads();
+    find_bin<kRkBins2 / kBlock>(h, need1, scratch, &found[0], &found[1]);
+    __syncthreads();
+    const uint32_t prefix = (b1 << 12) | found[0], need2 = found[1];
+    __syncthreads();
+    if (threadIdx.x == 0)
+        found[0] = 0u;  // candidate count
+    __syncthreads();
+    // the candidates with that prefix
+    for (int64_t q = threadIdx.x; q < nq; q += kBlock) {
+        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+        bool any = false;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            any = any || (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix);
+        if (any) {
+            const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix) {
+                    const uint32_t slot = atomicAdd(&found[0], 1u);
+                    if (slot < static_cast<uint32_t>(kRandkCandidates)) {
+                        ws->cand[slot][0] = word_of(w, j);
+                        ws->cand[slot][1] = word_of(l, j);
+                        ws->cand[slot][2] = static_cast<uint32_t>((q << 2) + j);
+                    }
+                }
+        }
+    }
+    __syncthreads();
+    const uint32_t n = min(found[0], static_cast<uint32_t>(kRandkCandidates));
+    for (uint32_t t = threadIdx.x; t < n; t += kBlock) {
+        const uint32_t hh = ws->cand[t][0], ll = ws->cand[t][1], ii = ws->cand[t][2];
+        uint32_t rank = 0u;
+        for (uint32_t u = 0; u < n; ++u)
+            rank += key_less(ws->cand[u][0], ws->cand[u][1], ws->cand[u][2], hh, ll, ii) ? 1u : 0u;
+        if (rank == need2 - 1u) {
+            scratch[kBlock / 64 + 1] = hh;
+            scratch[kBlock / 64 + 2] = ll;
+            scratch[kBlock / 64 + 3] = ii;
+        }
+    }
+    __syncthreads();
+    const uint32_t th = scratch[kBlock / 64 + 1], tl = scratch[kBlock / 64 + 2], ti = scratch[kBlock / 64 + 3];
+    __syncthreads();
+    // every coordinate at or below the threshold, into list 0
+    if (threadIdx.x < kRkShards)
+        ws->n_stage[threadIdx.x][0] = 0u;
+    uint32_t base = 0u;
+    for (int64_t qb = 0; qb < nq; qb += kBlock) {
+        const int64_t q = qb + threadIdx.x;
+        const uint32_t mask = q < nq ? selected_mask(q, d, key0, key1, th, tl, ti) : 0u;
+        append_in_order(mask, q, ws->stage[0], &base, scratch, K);
+    }
+    if (threadIdx.x == 0)
+        ws->n_stage[0][0] = base;
+}
+
+// One block after the bracket's collection pass: the keys below x_lo are
+// staged (n_below of them); of the candidates, the need = K - n_below
+// smallest by (hi, lo, index) are selected.  The interval is cut into
+// kRkPickBuckets equal parts counted in LDS; the part where the count reaches
+// `need` is ranked exactly, the parts before it are taken whole.
+__global__ __launch_bounds__(kBlock) void k_rk_pick(int64_t d, uint32_t K, uint32_t key0, uint32_t key1,
+                                                    RandkWorkspace* __restrict__ ws)
+{
+    __shared__ uint32_t h[kRkBins2];  // the parts' counts (or the fallback's histograms)
+    __shared__ uint32_t scratch[kBlock / 64 + 4];
+    __shared__ uint32_t found[2];
+    __shared__ uint32_t n_list[kRkShards], list_off[kRkShards];
+    __shared__ uint32_t cl[kRkPickMax][3];  // the candidates, gathered from the lists
+    __shared__ uint32_t cross[kRkCross][3];
+    __shared__ uint32_t n_cross, n_new, overflow;
+    static_assert(kRkPickBuckets <= kRkBins2, "the parts fit the histogram array");
+    static_assert(kRkShards * 4 == kBlock, "four threads per list gather the candidates");
+    const uint32_t x_lo = ws->ctl.x_lo, x_hi = ws->ctl.x_hi;
+    const uint64_t width = static_cast<uint64_t>(x_hi - x_lo) + 1u;
+    if (threadIdx.x == 0) {
+        n_cross = 0u;
+        n_new = 0u;
+        overflow = 0u;
+    }
+    __syncthreads();
+    uint32_t below = 0u, cands = 0u;
+    if (threadIdx.x < kRkShards) {
+        below = ws->n_stage[threadIdx.x][0];
+        cands = ws->n_bcand[threadIdx.x][0];
+        n_list[threadIdx.x] = cands;
+        if (cands > static_cast<uint32_t>(kRkShardCand))
+            atomicOr(&overflow, 1u);
+    }
+    const uint32_t n_below = block_inclusive_scan(below, scratch);
+    if (threadIdx.x == kBlock - 1)
+        found[0] = n_below;  // the last thread's inclusive sum is the total
+    const uint32_t c_incl = block_inclusive_scan(cands, scratch);
+    if (threadIdx.x == kBlock - 1)
+        found[1] = c_incl;
+    if (threadIdx.x < kRkShards)
+        list_off[threadIdx.x] = c_incl - cands;
+    for (int b = threadIdx.x; b < kRkPickBuckets; b += kBlock)
+        h[b] = 0u;
+    __syncthreads();
+    const uint32_t staged = found[0];
+    const uint32_t n_c = found[1];
+    bool valid = overflow == 0u && n_c <= static_cast<uint32_t>(kRkPickMax) && staged < K && staged + n_c >= K;
+    uint32_t bstar = 0u, rest = 0u;
+    if (valid) {
+        // gather: four threads per list, independent loads
+        {
+            const uint32_t sh = threadIdx.x >> 2, n = n_list[sh], off = list_off[sh];
+#pragma unroll 4
+            for (uint32_t j = threadIdx.x & 3u; j < n; j += 4u) {
+                cl[off + j][0] = ws->bcand[sh][j][0];
+                cl[off + j][1] = ws->bcand[sh][j][1];
+                cl[off + j][2] = ws->bcand[sh][j][2];
+            }
+        }
+        __syncthreads();
+        for (uint32_t t = threadIdx.x; t < n_c; t += kBlock)
+            atomicAdd(&h[pick_bucket(cl[t][0], x_lo, width)], 1u);
+        __syncthreads();
+        find_bin<kRkPickBuckets / kBlock>(h, K - staged, scratch, &found[0], &found[1]);
+        __syncthreads();
+        bstar = found[0];
+        rest = found[1];
+        // the crossing part's candidates
+        for (uint32_t t = threadIdx.x; t < n_c; t += kBlock)
+            if (pick_bucket(cl[t][0], x_lo, width) == bstar) {
+                const uint32_t slot = atomicAdd(&n_cross, 1u);
+                if (slot < static_cast<uint32_t>(kRkCross)) {
+                    cross[slot][0] = cl[t][0];
+                    cross[slot][1] = cl[t][1];
+                    cross[slot][2] = cl[t][2];
+                }
+            }
+        __syncthreads();
+        valid = n_cross <= static_cast<uint32_t>(kRkCross);  // block-uniform
+    }
+    if (!valid) {
+        pick_exact(d, K, key0, key1, ws, h, scratch, found);
+        return;
+    }
+    // n_list now holds each list's staged count (the gather is done)
+    if (threadIdx.x < kRkShards)
+        n_list[threadIdx.x] = below;
+    __syncthreads();
+    // the selected candidates are dealt to the lists in turn after their
+    // staged keys, so that the sort's threads get even shares
+    for (uint32_t t = threadIdx.x; t < n_c; t += kBlock) {
+        const uint32_t hh = cl[t][0], ll = cl[t][1], ii = cl[t][2];
+        const uint32_t b = pick_bucket(hh, x_lo, width);
+        bool take = b < bstar;
+        if (b == bstar) {
+            uint32_t rank = 0u;
+            for (uint32_t u = 0; u < n_cross; ++u)
+                rank += key_less(cross[u][0], cross[u][1], cross[u][2], hh, ll, ii) ? 1u : 0u;
+            take = rank < rest;
+        }
+        if (take) {
+            const uint32_t c = atomicAdd(&n_new, 1u);
+            const uint32_t sh = c % kRkShards;
+            const uint32_t pos = n_list[sh] + c / kRkShards;
+            if (pos < static_cast<uint32_t>(kRkSortMax))
+                ws->stage[sh][pos] = ii;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < kRkShards) {
+        const uint32_t sh = threadIdx.x;
+        ws->n_stage[sh][0] = n_list[sh] + (n_new > sh ? (n_new - sh + kRkShards - 1) / kRkShards : 0u);
+    }
 }
 
 constexpr int kRkBuckets = 4 * kRkSortThreads;  // buckets of the index range in the sort
@@ -609,13 +919,60 @@ static unsigned key_grid(int64_t d)
     return static_cast<unsigned>(blocks);
 }
 
+static std::atomic<int32_t> g_randk_mode{kRandkBracket};
+
+bool set_randk_mode(int32_t mode)
+{
+    if (mode != kRandkBracket && mode != kRandkHistogram && mode != kRandkBracketMiss)
+        return false;
+    g_randk_mode.store(mode, std::memory_order_relaxed);
+    return true;
+}
+
+// The bracket [x_lo, x_hi] of hi for the K-th key (see k_rk_pick): the count
+// of keys with hi < x has mean d x / 2^32 and standard deviation at most
+// sqrt(K (1 - K / d)) near the K-th key; ten of those (plus one) either side
+// of K.  False when the expected candidates would not fit.
+static bool randk_bracket(int64_t d, int64_t K, uint32_t* x_lo, uint32_t* x_hi)
+{
+    const double dd = static_cast<double>(d), kk = static_cast<double>(K);
+    const double sd = std::sqrt(kk * (1.0 - kk / dd)) + 1.0;
+    const double span = 4294967296.0;
+    double a = std::floor((kk - 10.0 * sd - 1.0) / dd * span);
+    double b = std::ceil((kk + 10.0 * sd + 1.0) / dd * span);
+    a = a < 0.0 ? 0.0 : a;
+    b = b > span - 1.0 ? span - 1.0 : b;
+    if (a > b)
+        return false;
+    const double expected = dd * (b - a + 1.0) / span;
+    if (expected + 10.0 * std::sqrt(expected) + 16.0 > static_cast<double>(kRkPickMax))
+        return false;
+    *x_lo = static_cast<uint32_t>(a);
+    *x_hi = static_cast<uint32_t>(b);
+    return true;
+}
+
 hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws_raw, hipStream_t stream)
 {
     RandkWorkspace* ws = static_cast<RandkWorkspace*>(ws_raw);
     const uint32_t key0 = static_cast<uint32_t>(seed);
     const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
     const unsigned gx = key_grid(d);  // persistent grid for the key passes
-    hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws);
+    const int32_t mode = g_randk_mode.load(std::memory_order_relaxed);
+    uint32_t x_lo = 0u, x_hi = 0u;
+    if (K <= kRkSortMax && mode != kRandkHistogram && randk_bracket(d, K, &x_lo, &x_hi)) {
+        if (mode == kRandkBracketMiss)
+            x_lo = x_hi = 0u;  // an interval that cannot hold the K-th key: the exact fallback runs
+        hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, x_lo, x_hi);
+        hipLaunchKernelGGL((k_rk_collect<true, true>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
+                           static_cast<uint32_t>(K));
+        hipLaunchKernelGGL(k_rk_pick, dim3(1), dim3(kBlock), 0, stream, d, static_cast<uint32_t>(K), key0, key1,
+                           ws);
+        hipLaunchKernelGGL(k_rk_sort, dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
+                           static_cast<uint32_t>(K), d);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, 0u, 0u);
     // the first histogram merges its LDS bins into global memory: few,
     // long-lived blocks keep those atomics to a few per bin
     int64_t hist_blocks = grid_cap() / 32;  // two blocks per compute unit
@@ -627,7 +984,7 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
     if (K <= kRkSortMax) {
         // the collection pass also appends the keys below the boundary
         // prefix; the threshold block appends the selected candidates
-        hipLaunchKernelGGL(k_rk_collect<true>, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
+        hipLaunchKernelGGL((k_rk_collect<true, false>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
                            static_cast<uint32_t>(K));
         hipLaunchKernelGGL(k_rk_threshold<true>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
                            static_cast<uint32_t>(K));
@@ -635,7 +992,7 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
                            static_cast<uint32_t>(K), d);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(k_rk_collect<false>, dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
+    hipLaunchKernelGGL((k_rk_collect<false, false>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
                        static_cast<uint32_t>(K));
     hipLaunchKernelGGL(k_rk_threshold<false>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
                        static_cast<uint32_t>(K));

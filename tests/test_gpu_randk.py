@@ -13,6 +13,7 @@ if not torch.cuda.is_available():
 
 import synth  # noqa: E402
 from oracle import oracle as O  # noqa: E402
+import paper_2109_12497_amd as uq  # noqa: E402
 from paper_2109_12497_amd.step import RandKStep  # noqa: E402
 
 DEV = torch.device("cuda:0")
@@ -32,8 +33,16 @@ def gpu_select(d, K, seed):
     # both sides of the largest K that one block sorts
     (100_000, 16_384, 11), (100_000, 16_385, 12),
 ])
-def test_selection_matches_oracle(d, K, seed):
-    got = gpu_select(d, K, seed)
+@pytest.mark.parametrize("mode", [1, 0, 2], ids=["bracket", "histograms", "bracket-missed"])
+def test_selection_matches_oracle(d, K, seed, mode):
+    """Each way of finding the subset (for K <= 16384: the bracket of the K-th
+    key, the histogram passes, and the bracket made to miss so that the
+    selection block's exact fallback runs) against the oracle."""
+    uq.uq_set_randk_mode(mode)
+    try:
+        got = gpu_select(d, K, seed)
+    finally:
+        uq.uq_set_randk_mode(1)
     want = O.randk_select(d, K, seed)
     assert np.array_equal(got, want)
 
