@@ -60,8 +60,9 @@ NETWORKS = {
 }
 
 # Streaming rate of this library's kernels on one MI355X (the measured norm,
-# index, quantise and reconstruction kernels run at 5.6-7.0 TB/s).
-LOCAL_TBPS = 6.0
+# quantise and sum + reconstruction kernels run at 6.3-7.1 TB/s, the fused
+# norm and index passes at 5.2-5.8).
+LOCAL_TBPS = 6.4
 
 
 @dataclass(frozen=True)
