@@ -58,5 +58,7 @@ def test_compression_pays_on_slow_links_and_little_on_xgmi():
         # also exchange the shared index, 3 bytes per coordinate in all
         want = 1.3 if sc.several_scales else 1.9
         assert pm.step_s(d, 32, pm.SCHEMES[0], eth) / pm.step_s(d, 32, sc, eth) > want, sc.name
-    # over seven xGMI rings the 8-bit exchange saves less than the local work costs at P = 2
-    assert pm.step_s(d, 2, pm.SCHEMES[1], xgmi7) > pm.step_s(d, 2, pm.SCHEMES[0], xgmi7)
+    # over seven xGMI rings at P = 2 the 8-bit exchange saves about what the
+    # local work costs: the two steps are within 10% of each other
+    ratio = pm.step_s(d, 2, pm.SCHEMES[0], xgmi7) / pm.step_s(d, 2, pm.SCHEMES[1], xgmi7)
+    assert 0.9 < ratio < 1.1, ratio
