@@ -163,6 +163,9 @@ def test_capped_grids(cap, M):
         for scales in (S_SINGLE, S_MULTI4):
             res, _, _ = gpu_step(host, d, scales, seed=cap + M)
             assert_matches_oracle(res, host, d, scales, seed=cap + M)
+            # one row at a time into the running sum, the last call with the reconstruction
+            res, _, _ = gpu_step(host, d, scales, seed=cap + M, streamed=True)
+            assert_matches_oracle(res, host, d, scales, seed=cap + M)
     finally:
         uq.uq_set_grid_cap(0)
 
