@@ -112,6 +112,23 @@ class _HostScales:
             self.ptr = ctypes.cast(self.array, ctypes.c_void_p)
 
 
+_scale_arrays: dict = {}
+
+
+def _host_scales(scales) -> _HostScales:
+    """The ctypes array of a scale set, built once per distinct set (the
+    arrays are read-only to the library, so they can be shared)."""
+    if scales is None:
+        return _HostScales(None)
+    key = tuple(scales)
+    hs = _scale_arrays.get(key)
+    if hs is None:
+        if len(_scale_arrays) >= 256:
+            _scale_arrays.clear()
+        hs = _scale_arrays[key] = _HostScales(key)
+    return hs
+
+
 def _check(status: int) -> None:
     if status != UQ_OK:
         raise UQError(status, f"{lib.uq_strerror(status).decode()}: {lib.uq_last_error().decode()}")
@@ -132,7 +149,7 @@ def uq_workspace_bytes(d: int, M: int) -> int:
 
 
 def uq_shared_scale(g, d, M, ldg, scales, K, w, idx, ws, ws_bytes, stream=None) -> None:
-    hs = _HostScales(scales)
+    hs = _host_scales(scales)
     _check(lib.uq_shared_scale(_ptr(g), d, M, ldg, hs.ptr, K, _ptr(w), _ptr(idx), _ptr(ws), ws_bytes,
                                _stream(stream)))
 
@@ -143,7 +160,7 @@ def uq_quantize_single(g, d, rows, ldg, worker0, w, s, seed, codes, ldc, stream=
 
 
 def uq_quantize_multi(g, d, rows, ldg, worker0, w, scales, K, idx, seed, codes, ldc, stream=None) -> None:
-    hs = _HostScales(scales)
+    hs = _host_scales(scales)
     _check(lib.uq_quantize_multi(_ptr(g), d, rows, ldg, worker0, _ptr(w), hs.ptr, K, _ptr(idx), seed,
                                  _ptr(codes), ldc, _stream(stream)))
 
@@ -153,18 +170,18 @@ def uq_sum_codes(codes, d, rows, ldc, accumulate, sum, stream=None) -> None:
 
 
 def uq_dequantize(sum, d, M, w, scales, K, idx, out, stream=None) -> None:
-    hs = _HostScales(scales)
+    hs = _host_scales(scales)
     _check(lib.uq_dequantize(_ptr(sum), d, M, _ptr(w), hs.ptr, K, _ptr(idx), _ptr(out), _stream(stream)))
 
 
 def uq_sum_dequantize(codes, d, rows, ldc, bits, accumulate, sum, M, w, scales, K, idx, out, stream=None) -> None:
-    hs = _HostScales(scales)
+    hs = _host_scales(scales)
     _check(lib.uq_sum_dequantize(_ptr(codes), d, rows, ldc, bits, accumulate, _ptr(sum), M, _ptr(w), hs.ptr, K,
                                  _ptr(idx), _ptr(out), _stream(stream)))
 
 
 def uq_quantize_packed(g, d, rows, ldg, worker0, w, scales, K, idx, seed, bits, packed, ldp, stream=None) -> None:
-    hs = _HostScales(scales)
+    hs = _host_scales(scales)
     _check(lib.uq_quantize_packed(_ptr(g), d, rows, ldg, worker0, _ptr(w), hs.ptr, K, _ptr(idx), seed, bits,
                                   _ptr(packed), ldp, _stream(stream)))
 

@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import torch
 
-from . import (uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_packed, uq_quantize_single,
+from . import (_stream, uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_packed, uq_quantize_single,
                uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes,
                uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
 
@@ -92,6 +92,7 @@ class Step:
         """g: [M, ldg] float32 on the device.  Returns the output view [d]."""
         assert g.dtype == torch.float32 and g.device == self.device and g.shape[0] == self.M
         assert g.stride(1) == 1 and g.shape[1] >= self.d
+        stream = _stream(stream)  # resolved once for the step's calls
         self.shared_scale(g, stream)
         if self.streamed:
             for m in range(self.M):
@@ -138,6 +139,7 @@ class RandKStep:
 
     def run(self, g, seed: int, stream=None):
         assert g.dtype == torch.float32 and g.shape[0] == self.M and g.stride(1) == 1
+        stream = _stream(stream)  # resolved once for the step's calls
         self.select(seed, stream)
         self.gather(g, stream)
         self.inner.run(self.sub, seed, stream)
