@@ -10,12 +10,15 @@
  *                       shared per-coordinate scale index;
  *   uq_quantize_single  or uq_quantize_multi: the integer codes of each worker;
  *   uq_sum_codes        the all-reduce of the codes (an exact integer sum);
- *   uq_dequantize       the averaged gradient reconstructed from the sum.
+ *   uq_dequantize       the averaged gradient reconstructed from the sum
+ *                       (uq_sum_dequantize does these two in one pass).
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers, except `scales`, which is a HOST
  *     array of K floats.  The caller owns every buffer; the library never
- *     allocates device memory and keeps no state between calls.
+ *     allocates device memory and keeps no state between calls (the two test
+ *     hooks at the end set process-wide options that change how work is
+ *     launched or searched, never a result).
  *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
  *     asynchronously on it; no entry point synchronises.  Argument checks are
  *     done on the host before anything is enqueued; on an error nothing is
