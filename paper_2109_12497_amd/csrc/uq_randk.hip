@@ -94,8 +94,9 @@ __device__ __forceinline__ uint32_t word_of(uint4 w, int j)
     return j == 0 ? w.x : (j == 1 ? w.y : (j == 2 ? w.z : w.w));
 }
 
-// Inclusive scan of one value per thread over a block of kBlock threads
-// (scratch: kBlock / 64 words of LDS).
+// Inclusive scan of one value per thread over a block of THREADS threads
+// (scratch: THREADS / 64 words of LDS).
+template <int THREADS = kBlock>
 __device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t x, uint32_t* scratch)
 {
     const int lane = threadIdx.x & 63;
@@ -116,11 +117,11 @@ __device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t x, uint32_t* s
     return x + before;
 }
 
-// The bin of hist[0 .. kBlock * PER) where the cumulative count first reaches
-// `need` (1 <= need <= the total), and how many keys of that bin are still
-// needed.  Thread t owns bins [t * PER, (t + 1) * PER); the owner of the
+// The bin of hist[0 .. THREADS * PER) where the cumulative count first
+// reaches `need` (1 <= need <= the total), and how many keys of that bin are
+// still needed.  Thread t owns bins [t * PER, (t + 1) * PER); the owner of the
 // crossing writes *bin and *rest.
-template <int PER>
+template <int PER, int THREADS = kBlock>
 __device__ __forceinline__ void find_bin(const uint32_t* hist, uint32_t need, uint32_t* scratch, uint32_t* bin,
                                          uint32_t* rest)
 {
@@ -131,7 +132,7 @@ __device__ __forceinline__ void find_bin(const uint32_t* hist, uint32_t need, ui
         v[j] = hist[threadIdx.x * PER + j];
         s += v[j];
     }
-    const uint32_t incl = block_inclusive_scan(s, scratch);
+    const uint32_t incl = block_inclusive_scan<THREADS>(s, scratch);
     uint32_t cum = incl - s;
     if (cum < need && need <= incl) {
 #pragma unroll
@@ -413,260 +414,23 @@ __device__ __forceinline__ uint32_t selected_mask(int64_t q, int64_t d, uint32_t
 // that holds the K-th key except with probability below 1e-20 (ten standard
 // deviations either side); one collection pass then appends every key below
 // x_lo to the staging lists and gathers the roughly 20 sqrt(K) keys inside
-// the interval as candidates, and k_rk_pick completes the selection.  It
-// checks that the interval did hold the K-th key (fewer than K keys below it,
-// at least K at or below its top, every candidate kept); if not, it computes
-// the exact selection on its own, slowly, with the same histogram steps as the
-// multi-pass path, so the result never depends on the bracket.
+// the interval as candidates, and every block of the sort completes the
+// selection for itself: it checks that the interval did hold the K-th key
+// (fewer than K keys below it, at least K at or below its top, every
+// candidate kept), cuts the interval into kRkPickBuckets equal parts counted
+// in LDS, ranks the part where the count reaches K exactly and takes the parts
+// before it whole.  If the check fails, the block computes the exact
+// selection on its own, slowly (the histogram steps of the multi-pass path,
+// then one pass that writes its slice of the output in order), so the result
+// never depends on the bracket.
 // ---------------------------------------------------------------------------
 constexpr int kRkPickBuckets = 2048;  // the interval cut into equal parts
 constexpr int kRkCross = 512;         // candidates of the crossing part kept in LDS
-constexpr int kRkPickMax = 4096;      // bracket candidates the selection block holds in LDS
+constexpr int kRkPickMax = 4096;      // bracket candidates a sort block holds in LDS
 
 __device__ __forceinline__ uint32_t pick_bucket(uint32_t hi, uint32_t x_lo, uint64_t width)
 {
     return static_cast<uint32_t>((static_cast<uint64_t>(hi - x_lo) * kRkPickBuckets) / width);
-}
-
-// Appends the set bits of `mask` (coordinates 4q + j) of every thread to
-// list 0 at positions *base + (block-wide exclusive count); every thread of
-// the block must call it; *base advances by the block's total.
-__device__ __forceinline__ void append_in_order(uint32_t mask, int64_t q, uint32_t* list, uint32_t* base,
-                                                uint32_t* scratch, uint32_t K)
-{
-    const uint32_t n = __builtin_popcount(mask);
-    const uint32_t incl = block_inclusive_scan(n, scratch);
-    uint32_t pos = *base + incl - n;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        if ((mask >> j) & 1u) {
-            if (pos < K)
-                list[pos] = static_cast<uint32_t>((q << 2) + j);
-            ++pos;
-        }
-    // the block's total: the last thread's inclusive count
-    if (threadIdx.x == kBlock - 1)
-        scratch[kBlock / 64] = incl;
-    __syncthreads();
-    *base += scratch[kBlock / 64];
-    __syncthreads();
-}
-
-// The exact selection by one block (the bracket missed): level-1 and level-2
-// histograms in LDS, the candidates sharing the K-th key's 20-bit prefix
-// ranked for the threshold, then every selected coordinate appended to
-// list 0 (the other lists emptied).
-__device__ void pick_exact(int64_t d, uint32_t K, uint32_t key0, uint32_t key1, RandkWorkspace* __restrict__ ws,
-                           uint32_t* h, uint32_t* scratch, uint32_t* found)
-{
-    const int64_t nq = (d + 3) >> 2;
-    const int64_t step = static_cast<int64_t>(kBlock) * kRkUnroll;
-    // level 1
-    for (int b = threadIdx.x; b < kRkBins2; b += kBlock)
-        h[b] = 0u;
-    __syncthreads();
-    for (int64_t q0 = threadIdx.x; q0 < nq; q0 += step) {
-        uint4 w[kRkUnroll];
-        key_blocks(q0, nq, 2u, key0, key1, w);
-#pragma unroll
-        for (int u = 0; u < kRkUnroll; ++u)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (((q0 + static_cast<int64_t>(u) * kBlock) << 2) + j < d)
-                    atomicAdd(&h[word_of(w[u], j) >> 24], 1u);
-    }
-    __syncthreads();
-    find_bin<1>(h, K, scratch, &found[0], &found[1]);
-    __syncthreads();
-    const uint32_t b1 = found[0], need1 = found[1];
-    __syncthreads();
-    // level 2
-    for (int b = threadIdx.x; b < kRkBins2; b += kBlock)
-        h[b] = 0u;
-    __syncthreads();
-    for (int64_t q0 = threadIdx.x; q0 < nq; q0 += step) {
-        uint4 w[kRkUnroll];
-        key_blocks(q0, nq, 2u, key0, key1, w);
-#pragma unroll
-        for (int u = 0; u < kRkUnroll; ++u)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t hi = word_of(w[u], j);
-                if (((q0 + static_cast<int64_t>(u) * kBlock) << 2) + j < d && (hi >> 24) == b1)
-                    atomicAdd(&h[(hi >> 12) & 0xFFFu], 1u);
-            }
-    }
-    __syncthreads();
-    find_bin<kRkBins2 / kBlock>(h, need1, scratch, &found[0], &found[1]);
-    __syncthreads();
-    const uint32_t prefix = (b1 << 12) | found[0], need2 = found[1];
-    __syncthreads();
-    if (threadIdx.x == 0)
-        found[0] = 0u;  // candidate count
-    __syncthreads();
-    // the candidates with that prefix
-    for (int64_t q = threadIdx.x; q < nq; q += kBlock) {
-        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
-        bool any = false;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            any = any || (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix);
-        if (any) {
-            const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix) {
-                    const uint32_t slot = atomicAdd(&found[0], 1u);
-                    if (slot < static_cast<uint32_t>(kRandkCandidates)) {
-                        ws->cand[slot][0] = word_of(w, j);
-                        ws->cand[slot][1] = word_of(l, j);
-                        ws->cand[slot][2] = static_cast<uint32_t>((q << 2) + j);
-                    }
-                }
-        }
-    }
-    __syncthreads();
-    const uint32_t n = min(found[0], static_cast<uint32_t>(kRandkCandidates));
-    for (uint32_t t = threadIdx.x; t < n; t += kBlock) {
-        const uint32_t hh = ws->cand[t][0], ll = ws->cand[t][1], ii = ws->cand[t][2];
-        uint32_t rank = 0u;
-        for (uint32_t u = 0; u < n; ++u)
-            rank += key_less(ws->cand[u][0], ws->cand[u][1], ws->cand[u][2], hh, ll, ii) ? 1u : 0u;
-        if (rank == need2 - 1u) {
-            scratch[kBlock / 64 + 1] = hh;
-            scratch[kBlock / 64 + 2] = ll;
-            scratch[kBlock / 64 + 3] = ii;
-        }
-    }
-    __syncthreads();
-    const uint32_t th = scratch[kBlock / 64 + 1], tl = scratch[kBlock / 64 + 2], ti = scratch[kBlock / 64 + 3];
-    __syncthreads();
-    // every coordinate at or below the threshold, into list 0
-    if (threadIdx.x < kRkShards)
-        ws->n_stage[threadIdx.x][0] = 0u;
-    uint32_t base = 0u;
-    for (int64_t qb = 0; qb < nq; qb += kBlock) {
-        const int64_t q = qb + threadIdx.x;
-        const uint32_t mask = q < nq ? selected_mask(q, d, key0, key1, th, tl, ti) : 0u;
-        append_in_order(mask, q, ws->stage[0], &base, scratch, K);
-    }
-    if (threadIdx.x == 0)
-        ws->n_stage[0][0] = base;
-}
-
-// One block after the bracket's collection pass: the keys below x_lo are
-// staged (n_below of them); of the candidates, the need = K - n_below
-// smallest by (hi, lo, index) are selected.  The interval is cut into
-// kRkPickBuckets equal parts counted in LDS; the part where the count reaches
-// `need` is ranked exactly, the parts before it are taken whole.
-__global__ __launch_bounds__(kBlock) void k_rk_pick(int64_t d, uint32_t K, uint32_t key0, uint32_t key1,
-                                                    RandkWorkspace* __restrict__ ws)
-{
-    __shared__ uint32_t h[kRkBins2];  // the parts' counts (or the fallback's histograms)
-    __shared__ uint32_t scratch[kBlock / 64 + 4];
-    __shared__ uint32_t found[2];
-    __shared__ uint32_t n_list[kRkShards], list_off[kRkShards];
-    __shared__ uint32_t cl[kRkPickMax][3];  // the candidates, gathered from the lists
-    __shared__ uint32_t cross[kRkCross][3];
-    __shared__ uint32_t n_cross, n_new, overflow;
-    static_assert(kRkPickBuckets <= kRkBins2, "the parts fit the histogram array");
-    static_assert(kRkShards * 4 == kBlock, "four threads per list gather the candidates");
-    const uint32_t x_lo = ws->ctl.x_lo, x_hi = ws->ctl.x_hi;
-    const uint64_t width = static_cast<uint64_t>(x_hi - x_lo) + 1u;
-    if (threadIdx.x == 0) {
-        n_cross = 0u;
-        n_new = 0u;
-        overflow = 0u;
-    }
-    __syncthreads();
-    uint32_t below = 0u, cands = 0u;
-    if (threadIdx.x < kRkShards) {
-        below = ws->n_stage[threadIdx.x][0];
-        cands = ws->n_bcand[threadIdx.x][0];
-        n_list[threadIdx.x] = cands;
-        if (cands > static_cast<uint32_t>(kRkShardCand))
-            atomicOr(&overflow, 1u);
-    }
-    const uint32_t n_below = block_inclusive_scan(below, scratch);
-    if (threadIdx.x == kBlock - 1)
-        found[0] = n_below;  // the last thread's inclusive sum is the total
-    const uint32_t c_incl = block_inclusive_scan(cands, scratch);
-    if (threadIdx.x == kBlock - 1)
-        found[1] = c_incl;
-    if (threadIdx.x < kRkShards)
-        list_off[threadIdx.x] = c_incl - cands;
-    for (int b = threadIdx.x; b < kRkPickBuckets; b += kBlock)
-        h[b] = 0u;
-    __syncthreads();
-    const uint32_t staged = found[0];
-    const uint32_t n_c = found[1];
-    bool valid = overflow == 0u && n_c <= static_cast<uint32_t>(kRkPickMax) && staged < K && staged + n_c >= K;
-    uint32_t bstar = 0u, rest = 0u;
-    if (valid) {
-        // gather: four threads per list, independent loads
-        {
-            const uint32_t sh = threadIdx.x >> 2, n = n_list[sh], off = list_off[sh];
-#pragma unroll 4
-            for (uint32_t j = threadIdx.x & 3u; j < n; j += 4u) {
-                cl[off + j][0] = ws->bcand[sh][j][0];
-                cl[off + j][1] = ws->bcand[sh][j][1];
-                cl[off + j][2] = ws->bcand[sh][j][2];
-            }
-        }
-        __syncthreads();
-        for (uint32_t t = threadIdx.x; t < n_c; t += kBlock)
-            atomicAdd(&h[pick_bucket(cl[t][0], x_lo, width)], 1u);
-        __syncthreads();
-        find_bin<kRkPickBuckets / kBlock>(h, K - staged, scratch, &found[0], &found[1]);
-        __syncthreads();
-        bstar = found[0];
-        rest = found[1];
-        // the crossing part's candidates
-        for (uint32_t t = threadIdx.x; t < n_c; t += kBlock)
-            if (pick_bucket(cl[t][0], x_lo, width) == bstar) {
-                const uint32_t slot = atomicAdd(&n_cross, 1u);
-                if (slot < static_cast<uint32_t>(kRkCross)) {
-                    cross[slot][0] = cl[t][0];
-                    cross[slot][1] = cl[t][1];
-                    cross[slot][2] = cl[t][2];
-                }
-            }
-        __syncthreads();
-        valid = n_cross <= static_cast<uint32_t>(kRkCross);  // block-uniform
-    }
-    if (!valid) {
-        pick_exact(d, K, key0, key1, ws, h, scratch, found);
-        return;
-    }
-    // n_list now holds each list's staged count (the gather is done)
-    if (threadIdx.x < kRkShards)
-        n_list[threadIdx.x] = below;
-    __syncthreads();
-    // the selected candidates are dealt to the lists in turn after their
-    // staged keys, so that the sort's threads get even shares
-    for (uint32_t t = threadIdx.x; t < n_c; t += kBlock) {
-        const uint32_t hh = cl[t][0], ll = cl[t][1], ii = cl[t][2];
-        const uint32_t b = pick_bucket(hh, x_lo, width);
-        bool take = b < bstar;
-        if (b == bstar) {
-            uint32_t rank = 0u;
-            for (uint32_t u = 0; u < n_cross; ++u)
-                rank += key_less(cross[u][0], cross[u][1], cross[u][2], hh, ll, ii) ? 1u : 0u;
-            take = rank < rest;
-        }
-        if (take) {
-            const uint32_t c = atomicAdd(&n_new, 1u);
-            const uint32_t sh = c % kRkShards;
-            const uint32_t pos = n_list[sh] + c / kRkShards;
-            if (pos < static_cast<uint32_t>(kRkSortMax))
-                ws->stage[sh][pos] = ii;
-        }
-    }
-    __syncthreads();
-    if (threadIdx.x < kRkShards) {
-        const uint32_t sh = threadIdx.x;
-        ws->n_stage[sh][0] = n_list[sh] + (n_new > sh ? (n_new - sh + kRkShards - 1) / kRkShards : 0u);
-    }
 }
 
 constexpr int kRkBuckets = 4 * kRkSortThreads;  // buckets of the index range in the sort
@@ -692,8 +456,147 @@ constexpr int kRkSliceBuckets = kRkBuckets / kRkSlices;
 static_assert(kRkSliceBuckets == 64, "one wave scans a slice's buckets");
 static_assert(kRkShards * 16 == kRkSortThreads, "16 threads per staging list");
 
+// The exact selection, for one block's slice of the output (the bracket
+// missed): level-1 and level-2 histograms of hi in LDS, the candidates that
+// share the K-th key's 20-bit prefix ranked for the threshold (key, index),
+// then one pass in index order that counts the selections of earlier slices
+// (the slice's offset) and writes the slice's own at their places.
+// cand: LDS room for kRkSortMax / 3 candidates (about d / 2^20 are expected,
+// at most 4096 on average for d < 2^32).
+__device__ void sort_exact_slice(int64_t d, uint32_t K, uint32_t key0, uint32_t key1, uint32_t* __restrict__ sel,
+                                 uint32_t* h, uint32_t (*cand)[3], uint32_t* scratch, uint32_t* found)
+{
+    constexpr int T = kRkSortThreads;
+    constexpr uint32_t kCap = kRkSortMax / 3;
+    const int64_t nq = (d + 3) >> 2;
+    const uint32_t t = threadIdx.x;
+    // level 1: hi >> 24
+    for (int b = t; b < kRkBins2; b += T)
+        h[b] = 0u;
+    __syncthreads();
+    for (int64_t q = t; q < nq; q += T) {
+        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((q << 2) + j < d)
+                atomicAdd(&h[word_of(w, j) >> 24], 1u);
+    }
+    __syncthreads();
+    find_bin<kRkBins2 / T, T>(h, K, scratch, &found[0], &found[1]);  // bins past 255 are empty
+    __syncthreads();
+    const uint32_t b1 = found[0], need1 = found[1];
+    __syncthreads();
+    // level 2: (hi >> 12) & 0xFFF in bin b1
+    for (int b = t; b < kRkBins2; b += T)
+        h[b] = 0u;
+    __syncthreads();
+    for (int64_t q = t; q < nq; q += T) {
+        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t hi = word_of(w, j);
+            if ((q << 2) + j < d && (hi >> 24) == b1)
+                atomicAdd(&h[(hi >> 12) & 0xFFFu], 1u);
+        }
+    }
+    __syncthreads();
+    find_bin<kRkBins2 / T, T>(h, need1, scratch, &found[0], &found[1]);
+    __syncthreads();
+    const uint32_t prefix = (b1 << 12) | found[0], need2 = found[1];
+    __syncthreads();
+    if (t == 0)
+        found[0] = 0u;  // candidate count
+    __syncthreads();
+    for (int64_t q = t; q < nq; q += T) {
+        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+        bool any = false;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            any = any || (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix);
+        if (any) {
+            const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix) {
+                    const uint32_t slot = atomicAdd(&found[0], 1u);
+                    if (slot < kCap) {
+                        cand[slot][0] = word_of(w, j);
+                        cand[slot][1] = word_of(l, j);
+                        cand[slot][2] = static_cast<uint32_t>((q << 2) + j);
+                    }
+                }
+        }
+    }
+    __syncthreads();
+    const uint32_t n = min(found[0], kCap);
+    for (uint32_t c = t; c < n; c += T) {
+        uint32_t rank = 0u;
+        for (uint32_t u = 0; u < n; ++u)
+            rank += key_less(cand[u][0], cand[u][1], cand[u][2], cand[c][0], cand[c][1], cand[c][2]) ? 1u : 0u;
+        if (rank == need2 - 1u) {
+            scratch[T / 64 + 1] = cand[c][0];
+            scratch[T / 64 + 2] = cand[c][1];
+            scratch[T / 64 + 3] = cand[c][2];
+        }
+    }
+    __syncthreads();
+    const uint32_t th = scratch[T / 64 + 1], tl = scratch[T / 64 + 2], ti = scratch[T / 64 + 3];
+    __syncthreads();
+    // the slice's selections in index order, after those of earlier slices
+    const uint32_t slice = blockIdx.x;
+    const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
+    uint32_t below = 0u, mine = 0u;
+    for (int64_t qb = 0; qb < nq; qb += T) {
+        // past the slice: nothing more to write (the bucket map is monotone)
+        if (bucket_of(static_cast<uint32_t>(qb << 2), scale) / kRkSliceBuckets > slice)
+            break;
+        const int64_t q = qb + t;
+        const uint32_t mask = q < nq ? selected_mask(q, d, key0, key1, th, tl, ti) : 0u;
+        uint32_t mb = 0u, mm = 0u;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((mask >> j) & 1u) {
+                const uint32_t sl = bucket_of(static_cast<uint32_t>((q << 2) + j), scale) / kRkSliceBuckets;
+                mb |= sl < slice ? (1u << j) : 0u;
+                mm |= sl == slice ? (1u << j) : 0u;
+            }
+        const uint32_t nb = __builtin_popcount(mb), nm = __builtin_popcount(mm);
+        const uint32_t ib = block_inclusive_scan<T>(nb, scratch);
+        if (t == T - 1)
+            scratch[T / 64] = ib;
+        __syncthreads();
+        below += scratch[T / 64];  // earlier slices' selections have smaller indices
+        __syncthreads();
+        const uint32_t im = block_inclusive_scan<T>(nm, scratch);
+        uint32_t pos = below + mine + im - nm;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((mm >> j) & 1u) {
+                if (pos < K)
+                    sel[pos] = static_cast<uint32_t>((q << 2) + j);
+                ++pos;
+            }
+        if (t == T - 1)
+            scratch[T / 64] = im;
+        __syncthreads();
+        mine += scratch[T / 64];
+        __syncthreads();
+    }
+}
+
+// The staged indices (and, with BRACKET, the picks this block makes among
+// the bracket's candidates) in increasing order, by kRkSlices blocks.  The
+// index range is cut into kRkBuckets buckets (a monotone map) and block j owns
+// the contiguous run of buckets j * kRkSliceBuckets .. + kRkSliceBuckets - 1.
+// Every block reads all staged indices (16 threads per staging list), counts
+// those in earlier slices (its output offset) and bins its own through LDS
+// counters (about K / kRkBuckets per bucket); a second read places them by
+// bucket, and each is written at the offset plus its bucket's start plus its
+// rank inside the bucket (the indices are distinct).
+template <bool BRACKET>
 __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace* __restrict__ ws,
-                                                            uint32_t* __restrict__ sel, uint32_t K, int64_t d)
+                                                            uint32_t* __restrict__ sel, uint32_t K, int64_t d,
+                                                            uint32_t key0, uint32_t key1)
 {
     __shared__ uint32_t buf[kRkSortMax];
     __shared__ uint32_t count[kRkSliceBuckets];
@@ -703,17 +606,122 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
     const uint32_t t = threadIdx.x;
     const uint32_t slice = blockIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    if (t < kRkSliceBuckets)
-        count[t] = 0u;
     const uint32_t* list = ws->stage[t >> 4];
     const uint32_t len = min(ws->n_stage[t >> 4][0], static_cast<uint32_t>(kRkSortMax));
     const uint32_t sub = t & 15u;
     const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
+
+    // BRACKET: this block's picks among the candidates, in h[0 .. n_pick)
+    __shared__ uint32_t h[BRACKET ? kRkBins2 : 1];
+    __shared__ uint32_t cl[BRACKET ? kRkPickMax : 1][3];
+    __shared__ uint32_t cross[BRACKET ? kRkCross : 1][3];
+    __shared__ uint32_t scratch[kRkSortThreads / 64 + 4];
+    __shared__ uint32_t found[2];
+    __shared__ uint32_t n_list[kRkShards], list_off[kRkShards];
+    __shared__ uint32_t n_cross, n_pick, overflow;
+    uint32_t npick = 0u;
+    if (BRACKET) {
+        static_assert(kRkPickBuckets == 2 * kRkSortThreads, "two parts per thread in the scan");
+        const uint32_t x_lo = ws->ctl.x_lo, x_hi = ws->ctl.x_hi;
+        const uint64_t width = static_cast<uint64_t>(x_hi - x_lo) + 1u;
+        if (t == 0) {
+            n_cross = 0u;
+            n_pick = 0u;
+            overflow = 0u;
+        }
+        for (int b = t; b < kRkPickBuckets; b += kRkSortThreads)
+            h[b] = 0u;
+        __syncthreads();
+        uint32_t below = 0u, cands = 0u;
+        if (t < kRkShards) {
+            below = ws->n_stage[t][0];
+            cands = ws->n_bcand[t][0];
+            n_list[t] = cands;
+            if (cands > static_cast<uint32_t>(kRkShardCand))
+                atomicOr(&overflow, 1u);
+        }
+        const uint32_t ib = block_inclusive_scan<kRkSortThreads>(below, scratch);
+        if (t == kRkSortThreads - 1)
+            found[0] = ib;  // the last thread's inclusive sum is the total
+        const uint32_t ic = block_inclusive_scan<kRkSortThreads>(cands, scratch);
+        if (t == kRkSortThreads - 1)
+            found[1] = ic;
+        if (t < kRkShards)
+            list_off[t] = ic - cands;
+        __syncthreads();
+        const uint32_t staged = found[0];
+        const uint32_t n_c = found[1];
+        bool valid = overflow == 0u && n_c <= static_cast<uint32_t>(kRkPickMax) && staged < K && staged + n_c >= K;
+        uint32_t bstar = 0u, rest = 0u;
+        if (valid) {
+            {  // gather: 16 threads per list
+                const uint32_t sh = t >> 4, n = n_list[sh], off = list_off[sh];
+                for (uint32_t j = sub; j < n; j += 16u) {
+                    cl[off + j][0] = ws->bcand[sh][j][0];
+                    cl[off + j][1] = ws->bcand[sh][j][1];
+                    cl[off + j][2] = ws->bcand[sh][j][2];
+                }
+            }
+            __syncthreads();
+            for (uint32_t c = t; c < n_c; c += kRkSortThreads)
+                atomicAdd(&h[pick_bucket(cl[c][0], x_lo, width)], 1u);
+            __syncthreads();
+            find_bin<kRkPickBuckets / kRkSortThreads, kRkSortThreads>(h, K - staged, scratch, &found[0], &found[1]);
+            __syncthreads();
+            bstar = found[0];
+            rest = found[1];
+            for (uint32_t c = t; c < n_c; c += kRkSortThreads)
+                if (pick_bucket(cl[c][0], x_lo, width) == bstar) {
+                    const uint32_t slot = atomicAdd(&n_cross, 1u);
+                    if (slot < static_cast<uint32_t>(kRkCross)) {
+                        cross[slot][0] = cl[c][0];
+                        cross[slot][1] = cl[c][1];
+                        cross[slot][2] = cl[c][2];
+                    }
+                }
+            __syncthreads();
+            valid = n_cross <= static_cast<uint32_t>(kRkCross);  // block-uniform
+        }
+        if (!valid) {
+            sort_exact_slice(d, K, key0, key1, sel, h, reinterpret_cast<uint32_t(*)[3]>(buf), scratch, found);
+            return;
+        }
+        // the picks, into h (the parts' counts are no longer needed)
+        for (uint32_t c = t; c < n_c; c += kRkSortThreads) {
+            const uint32_t hh = cl[c][0], ll = cl[c][1], ii = cl[c][2];
+            const uint32_t b = pick_bucket(hh, x_lo, width);
+            bool take = b < bstar;
+            if (b == bstar) {
+                uint32_t rank = 0u;
+                for (uint32_t u = 0; u < n_cross; ++u)
+                    rank += key_less(cross[u][0], cross[u][1], cross[u][2], hh, ll, ii) ? 1u : 0u;
+                take = rank < rest;
+            }
+            if (take) {
+                const uint32_t pos = atomicAdd(&n_pick, 1u);
+                if (pos < static_cast<uint32_t>(kRkBins2))
+                    h[pos] = ii;
+            }
+        }
+        __syncthreads();
+        npick = min(n_pick, static_cast<uint32_t>(kRkBins2));
+    }
+
+    if (t < kRkSliceBuckets)
+        count[t] = 0u;
     __syncthreads();
     uint32_t below = 0u;
 #pragma unroll 4
     for (uint32_t p = sub; p < len; p += 16u) {
         const uint32_t b = bucket_of(list[p], scale);
+        const uint32_t sl = b / kRkSliceBuckets;
+        if (sl < slice)
+            ++below;
+        else if (sl == slice)
+            atomicAdd(&count[b % kRkSliceBuckets], 1u);
+    }
+    for (uint32_t p = t; p < npick; p += kRkSortThreads) {
+        const uint32_t b = bucket_of(h[p], scale);
         const uint32_t sl = b / kRkSliceBuckets;
         if (sl < slice)
             ++below;
@@ -758,6 +766,16 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
                 buf[pos] = v;
         }
     }
+    for (uint32_t p = t; p < npick; p += kRkSortThreads) {
+        const uint32_t v = h[p];
+        const uint32_t b = bucket_of(v, scale);
+        if (b / kRkSliceBuckets == slice) {
+            const uint32_t lb = b % kRkSliceBuckets;
+            const uint32_t pos = start[lb] + atomicAdd(&count[lb], 1u);
+            if (pos < static_cast<uint32_t>(kRkSortMax))
+                buf[pos] = v;
+        }
+    }
     __syncthreads();
     // each of the slice's indices goes to the offset plus its bucket's start
     // plus the number of smaller indices in its bucket
@@ -775,6 +793,7 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
             sel[pos] = v;
     }
 }
+
 
 // K > kRkSortMax: block b owns coordinates [b * chunk, (b + 1) * chunk); one
 // pass counts its selections, the next writes them in order at the scanned
@@ -929,7 +948,7 @@ bool set_randk_mode(int32_t mode)
     return true;
 }
 
-// The bracket [x_lo, x_hi] of hi for the K-th key (see k_rk_pick): the count
+// The bracket [x_lo, x_hi] of hi for the K-th key (see k_rk_sort): the count
 // of keys with hi < x has mean d x / 2^32 and standard deviation at most
 // sqrt(K (1 - K / d)) near the K-th key; ten of those (plus one) either side
 // of K.  False when the expected candidates would not fit.
@@ -966,10 +985,8 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
         hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, x_lo, x_hi);
         hipLaunchKernelGGL((k_rk_collect<true, true>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
                            static_cast<uint32_t>(K));
-        hipLaunchKernelGGL(k_rk_pick, dim3(1), dim3(kBlock), 0, stream, d, static_cast<uint32_t>(K), key0, key1,
-                           ws);
-        hipLaunchKernelGGL(k_rk_sort, dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
-                           static_cast<uint32_t>(K), d);
+        hipLaunchKernelGGL((k_rk_sort<true>), dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
+                           static_cast<uint32_t>(K), d, key0, key1);
         return hipGetLastError();
     }
     hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, 0u, 0u);
@@ -988,8 +1005,8 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
                            static_cast<uint32_t>(K));
         hipLaunchKernelGGL(k_rk_threshold<true>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
                            static_cast<uint32_t>(K));
-        hipLaunchKernelGGL(k_rk_sort, dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
-                           static_cast<uint32_t>(K), d);
+        hipLaunchKernelGGL((k_rk_sort<false>), dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
+                           static_cast<uint32_t>(K), d, key0, key1);
         return hipGetLastError();
     }
     hipLaunchKernelGGL((k_rk_collect<false, false>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
