@@ -15,11 +15,11 @@
 // x_lo to kRkShards staging lists (each wave adds its selections with one
 // atomic, spread over the lists' counters: device-scope atomics on one
 // address serialise) and collects the ~20 sqrt(K) keys inside the interval
-// with their low words; one block checks that the interval held the K-th key
-// and appends the smallest of them, and 64 blocks sort the lists, each one
-// slice of the index range.  Should the bracket miss, the one block computes
-// the exact selection itself with the steps below, so the result never
-// depends on it.
+// with their low words; each of the 64 blocks that sort the lists (one slice
+// of the index range each) checks that the interval held the K-th key and
+// picks the smallest candidates itself.  Should the bracket miss, every such
+// block computes the exact selection itself with the steps below, so the
+// result never depends on it.
 //
 // The histogram passes (K > kRkSortMax, or by the test hook):
 //   1. per-block LDS histograms of hi >> 24 (256 bins), merged with atomics;
