@@ -574,3 +574,50 @@ def test_streamed_rows_longer_than_2_pow_31():
     assert int(step.sum[:d].abs().max()) <= M * scales[0]
     del g, step
     torch.cuda.empty_cache()
+
+
+def _random_configs(n=24, seed=2109):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        bits = int(rng.choice([8, 8, 4, 2]))
+        K = int(rng.integers(1, 6))
+        d = int(rng.choice([int(rng.integers(1, 600)), int(rng.integers(600, 40_000)),
+                            int(rng.integers(40_000, 300_000))]))
+        M = int(rng.choice([1, 2, 3, 5, 8, 16, 17, 23]))
+        out.append(dict(d=d, M=M, scales=synth.scales_for(bits, K), bits=bits,
+                        streamed=bool(rng.integers(0, 2)), fused=bool(rng.integers(0, 3) > 0),
+                        cap=int(rng.choice([0, 0, 8, 64])), seed=int(rng.integers(0, 2 ** 63)), case=i))
+    return out
+
+
+@pytest.mark.parametrize("cfg", _random_configs(), ids=lambda c: f"case{c['case']}")
+def test_random_configurations(cfg):
+    """Seeded random mixes of d (ragged, one tile to several hundred), worker
+    count (across the fused pass's 2..16 and beyond), scale count, code width,
+    streamed or materialised codes, fused or separate sum and reconstruction,
+    and grid cap, against the oracle."""
+    d, M, scales, bits, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["bits"], cfg["seed"]
+    host = synth.mixed_rows(M, d, seed=cfg["case"] + 100, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(np.ascontiguousarray(host)).to(DEV)
+    uq.uq_set_grid_cap(cfg["cap"])
+    try:
+        step = Step(d, M, scales, device=DEV, streamed=cfg["streamed"], bits=bits, fused=cfg["fused"])
+        step.run(g, seed)
+        torch.cuda.synchronize()
+    finally:
+        uq.uq_set_grid_cap(0)
+    W = np.float32(step.w[0].item())
+    ref = O.pipeline(host, scales, seed, d=d, W=W)
+    assert ulps(W, ref["W_oracle"]) <= 1, (W, ref["W_oracle"])
+    if len(scales) > 1:
+        assert np.array_equal(step.idx[:d].cpu().numpy(), ref["idx"]), "scale index differs"
+    if not cfg["streamed"]:
+        if bits == 8:
+            assert np.array_equal(step.codes[:, :d].cpu().numpy(), ref["codes"]), "codes differ"
+        else:
+            packed = step.codes[:, :(d * bits + 7) // 8].cpu().numpy()
+            for m in range(M):
+                assert np.array_equal(O.unpack_codes(packed[m], d, bits), ref["codes"][m]), f"codes row {m}"
+    assert np.array_equal(step.sum[:d].cpu().numpy(), ref["sum"]), "sums differ"
+    assert np.array_equal(step.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32)), "outputs differ"
