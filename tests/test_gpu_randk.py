@@ -138,3 +138,25 @@ def test_selection_at_the_largest_d(d, K):
         below = {i0 + int(j) for j in near if _key(hi[j], lo[j], i0 + int(j)) <= top}
         inside = {i for i in chosen if i0 <= i < i0 + n}
         assert below == inside, (i0, len(below), len(inside))
+
+
+def _random_selections(n=18, seed=3344):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        d = int(rng.choice([int(rng.integers(1, 2000)), int(rng.integers(2000, 200_000)),
+                            int(rng.integers(200_000, 1_500_000))]))
+        K = int(rng.choice([1, int(rng.integers(1, d + 1)), min(d, int(rng.integers(1, 20_000)))]))
+        out.append((d, K, int(rng.integers(0, 2 ** 64, dtype=np.uint64)), i % 3))
+    return out
+
+
+@pytest.mark.parametrize("d,K,seed,mode", _random_selections())
+def test_random_selections(d, K, seed, mode):
+    """Seeded random (d, K, seed) in every selection mode, against the oracle."""
+    uq.uq_set_randk_mode([1, 0, 2][mode])
+    try:
+        got = gpu_select(d, K, seed)
+    finally:
+        uq.uq_set_randk_mode(1)
+    assert np.array_equal(got, O.randk_select(d, K, seed))
