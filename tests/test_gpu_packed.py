@@ -133,3 +133,34 @@ def test_packed_vgg16_full_size():
     codes8 = a.codes[:, i0:i0 + n].cpu().numpy()
     for m in range(M):
         assert np.array_equal(O.unpack_codes(packed[m], n, 4), codes8[m])
+
+
+@pytest.mark.parametrize("name", ["vgg16-single-4bit", "vgg16-multi-4bit"])
+def test_packed_workload_sampled_parity(name):
+    """The VGG-16-sized 4-bit workloads at full size (1.1 GB of packed codes
+    per step, stored nontemporally): oracle windows at both ends and at
+    random places, each a whole number of bytes of every code row."""
+    g, cfg = synth.make_gradients(name, device=DEV)
+    d, M, scales, seed, bits = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"], int(cfg["bits"])
+    st = Step(d, M, scales, device=DEV, bits=bits)
+    st.run(g, seed)
+    torch.cuda.synchronize()
+    W = np.float32(st.w[0].item())
+    rng = np.random.default_rng(d)
+    width = 1 << 14
+    starts = [0, (d - width - 5) // 8 * 8] + [int(x) // 8 * 8 for x in rng.integers(0, d - width, size=10)]
+    for i0 in starts:
+        i1 = min(d, i0 + width + 5)
+        host = g[:, i0:i1].cpu().numpy()
+        idx = O.scale_index_shared(host, W, scales) if len(scales) > 1 else None
+        if idx is not None:
+            assert np.array_equal(st.idx[i0:i1].cpu().numpy(), idx), f"idx window {i0}"
+        codes = np.stack([O.quantize(host[m], W, scales, seed, worker=m, i0=i0, idx=idx) for m in range(M)])
+        b0, b1 = i0 * bits // 8, (i1 * bits + 7) // 8
+        packed = st.codes[:, b0:b1].cpu().numpy()
+        for m in range(M):
+            assert np.array_equal(O.unpack_codes(packed[m], i1 - i0, bits), codes[m]), f"codes window {i0} row {m}"
+        sums = O.sum_codes(codes)
+        assert np.array_equal(st.sum[i0:i1].cpu().numpy(), sums), f"sum window {i0}"
+        out = O.dequantize(sums, M, W, scales, idx)
+        assert np.array_equal(st.out[i0:i1].cpu().numpy().view(np.int32), out.view(np.int32)), f"out window {i0}"
