@@ -135,13 +135,15 @@ def test_packed_vgg16_full_size():
         assert np.array_equal(O.unpack_codes(packed[m], n, 4), codes8[m])
 
 
-@pytest.mark.parametrize("name", ["vgg16-single-4bit", "vgg16-multi-4bit"])
-def test_packed_workload_sampled_parity(name):
-    """The VGG-16-sized 4-bit workloads at full size (1.1 GB of packed codes
-    per step, stored nontemporally): oracle windows at both ends and at
-    random places, each a whole number of bytes of every code row."""
-    g, cfg = synth.make_gradients(name, device=DEV)
-    d, M, scales, seed, bits = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"], int(cfg["bits"])
+@pytest.mark.parametrize("bits,scales", [(4, [7.0]), (4, synth.scales_for(4, 4)), (2, [1.0]), (2, [1.0, 16.0])],
+                         ids=["s7-4bit", "K4-4bit", "s1-2bit", "K2-2bit"])
+def test_packed_workload_sampled_parity(bits, scales):
+    """VGG-16-sized gradients (16 workers) as 4- and 2-bit codes at full size
+    (1.1 GB or 553 MB of packed codes per step, stored nontemporally): oracle
+    windows at both ends and at random places, each a whole number of bytes
+    of every code row."""
+    g, cfg = synth.make_gradients("vgg16-single", device=DEV)
+    d, M, seed = cfg["d"], cfg["M"], cfg["seed"]
     st = Step(d, M, scales, device=DEV, bits=bits)
     st.run(g, seed)
     torch.cuda.synchronize()
