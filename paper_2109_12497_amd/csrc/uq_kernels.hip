@@ -266,7 +266,7 @@ __device__ __forceinline__ void norm_max_load(const float* const rowp[ROWS / 4],
         }
 }
 
-template <int ROWS>
+template <int ROWS, bool NT>
 __global__ __launch_bounds__(kBlock) void k_norm_max(const float* __restrict__ g, int64_t d, int32_t M,
                                                      int64_t ldg, int64_t chunk, int32_t nchunks,
                                                      double* __restrict__ part, float* __restrict__ amax)
@@ -345,7 +345,11 @@ __global__ __launch_bounds__(kBlock) void k_norm_max(const float* __restrict__ g
         o.y = fmaxf(fmaxf(m0.y, m1.y), fmaxf(m2.y, m3.y));
         o.z = fmaxf(fmaxf(m0.z, m1.z), fmaxf(m2.z, m3.z));
         o.w = fmaxf(fmaxf(m0.w, m1.w), fmaxf(m2.w, m3.w));
-        *reinterpret_cast<f32x4*>(amax + ((q < q_end ? q : spare_quad) << 2)) = o;
+        f32x4* dst = reinterpret_cast<f32x4*>(amax + ((q < q_end ? q : spare_quad) << 2));
+        if (NT)
+            __builtin_nontemporal_store(o, dst);
+        else
+            *dst = o;
     }
     // the trailing d % 4 coordinates (last chunk only): each wave adds its own
     // rows' squares; wave 0 forms the maximum over all rows
@@ -1207,6 +1211,12 @@ static unsigned one_shot(int64_t units, int64_t per_block)
     return static_cast<unsigned>(blocks);
 }
 
+// The fused pass stores the row maxima nontemporally when they exceed this
+// many bytes: measured 2.4% faster at VGG-16 size (553 MB) and 3.2% at
+// 2^30 coordinates, 6% slower at ResNet-50 size (102 MB), where the index
+// pass reads them back from the 256 MB Infinity Cache.
+constexpr int64_t kMaximaNontemporalBytes = int64_t(512) << 20;
+
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
                                float* w, uint8_t* idx, void* ws, hipStream_t stream)
 {
@@ -1217,15 +1227,25 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         double* rows = reinterpret_cast<double*>(static_cast<char*>(ws) + L.rows_off);
         float* amax = reinterpret_cast<float*>(static_cast<char*>(ws) + L.amax_off);
         const dim3 grid(static_cast<unsigned>(plan.nchunks));
+        // maxima beyond twice the 256 MB Infinity Cache are stored
+        // nontemporally (the index pass cannot find them there anyway)
+        const bool nt = 4 * d > kMaximaNontemporalBytes;
+#define UQ_LAUNCH_NORM_MAX(R)                                                                                     \
+    do {                                                                                                          \
+        if (nt)                                                                                                   \
+            hipLaunchKernelGGL((k_norm_max<R, true>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,    \
+                               plan.nchunks, part, amax);                                                         \
+        else                                                                                                      \
+            hipLaunchKernelGGL((k_norm_max<R, false>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,   \
+                               plan.nchunks, part, amax);                                                         \
+    } while (0)
         if (M <= 4)
-            hipLaunchKernelGGL(k_norm_max<4>, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,
-                               plan.nchunks, part, amax);
+            UQ_LAUNCH_NORM_MAX(4);
         else if (M <= 8)
-            hipLaunchKernelGGL(k_norm_max<8>, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,
-                               plan.nchunks, part, amax);
+            UQ_LAUNCH_NORM_MAX(8);
         else
-            hipLaunchKernelGGL(k_norm_max<kFuseRows>, grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,
-                               plan.nchunks, part, amax);
+            UQ_LAUNCH_NORM_MAX(kFuseRows);
+#undef UQ_LAUNCH_NORM_MAX
         hipLaunchKernelGGL(k_rowsum, dim3(static_cast<unsigned>(M)), dim3(kBlock), 0, stream, part, plan.nchunks,
                            rows);
         const unsigned gx = one_shot((d + 3) / 4, kIndexTile);
