@@ -70,11 +70,19 @@ def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> 
     return b
 
 
+def _code_of(text: str) -> str:
+    """The kernel source without its comments and with whitespace runs
+    collapsed: counters stay tied to the code, not to its comments."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_digest() -> str:
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(_code_of(f.read()).encode())
     return h.hexdigest()[:16]
 
 

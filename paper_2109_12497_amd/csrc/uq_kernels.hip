@@ -855,6 +855,9 @@ __device__ __forceinline__ void quantise_tail(const float* __restrict__ row, uin
     }
 }
 
+// The quantiser: MULTI with a per-coordinate scale index, BITS the code
+// width (8, or 4 / 2 packed), NT codes stored nontemporally (the launcher sets
+// it for launches that write more than kCodesNontemporalBytes).
 template <bool MULTI, int BITS, bool NT>
 __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g, int64_t d, int64_t ldg,
                                                      int32_t worker0, const float* __restrict__ wptr,
@@ -866,7 +869,8 @@ __global__ __launch_bounds__(kBlock) void k_quantise(const float* __restrict__ g
     __shared__ float inv_p[kMaxScales];   // s_k / W * 2^16 when pre
 
     // 2-D grid: tile blocks in x, worker rows in y; each wave takes `tpw`
-    // consecutive tiles, then strides by the grid
+    // consecutive tiles (on a one-shot grid, only those), then strides by
+    // the grid
     const int32_t r = blockIdx.y;
     const uint32_t worker = static_cast<uint32_t>(worker0) + static_cast<uint32_t>(r);
     const float* row = g + static_cast<int64_t>(r) * ldg;
