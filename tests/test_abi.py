@@ -293,3 +293,16 @@ def test_randk_mode_rejects(mode):
 def test_randk_mode_accepts_and_restores():
     for mode in (0, 2, 1):
         assert L.uq_set_randk_mode(mode) == uq.UQ_OK
+
+
+def test_host_scale_arrays_are_shared_and_bounded():
+    """The binding builds a scale set's host array once and reuses it; the
+    cache of arrays stays bounded."""
+    a = uq._host_scales([127.0, 2032.0])
+    assert a is uq._host_scales((127.0, 2032.0))
+    assert list(a.array) == [127.0, 2032.0]
+    assert uq._host_scales([7.0]) is not a
+    for k in range(400):
+        uq._host_scales([float(k + 1)])
+    assert len(uq._scale_arrays) <= 256
+    assert uq._host_scales(None).ptr is None
