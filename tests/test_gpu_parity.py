@@ -621,3 +621,31 @@ def test_random_configurations(cfg):
                 assert np.array_equal(O.unpack_codes(packed[m], d, bits), ref["codes"][m]), f"codes row {m}"
     assert np.array_equal(step.sum[:d].cpu().numpy(), ref["sum"]), "sums differ"
     assert np.array_equal(step.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32)), "outputs differ"
+
+
+def test_concurrent_steps_on_two_streams():
+    """The library keeps no state between calls: two steps with their own
+    buffers, issued interleaved on two streams (default priority), give the
+    results each gives alone."""
+    d1, d2, M = 200_003, 150_001, 5
+    h1 = synth.mixed_rows(M, d1, seed=61, ldg=synth.round_up(d1, 64))
+    h2 = synth.mixed_rows(M, d2, seed=62, ldg=synth.round_up(d2, 64))
+    g1 = torch.from_numpy(np.ascontiguousarray(h1)).to(DEV)
+    g2 = torch.from_numpy(np.ascontiguousarray(h2)).to(DEV)
+    a = Step(d1, M, S_SINGLE, device=DEV)
+    b = Step(d2, M, S_MULTI4, device=DEV)
+    a.run(g1, 7)
+    b.run(g2, 8)
+    torch.cuda.synchronize()
+    ref_a, ref_b = a.out[:d1].clone(), b.out[:d2].clone()
+    ref_ca, ref_cb = a.codes.clone(), b.codes.clone()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(torch.cuda.current_stream())
+    s2.wait_stream(torch.cuda.current_stream())
+    for _ in range(5):
+        a.run(g1, 7, stream=s1)
+        b.run(g2, 8, stream=s2)
+    torch.cuda.synchronize()
+    assert torch.equal(a.codes, ref_ca) and torch.equal(b.codes, ref_cb)
+    assert torch.equal(a.out[:d1].view(torch.int32), ref_a.view(torch.int32))
+    assert torch.equal(b.out[:d2].view(torch.int32), ref_b.view(torch.int32))
