@@ -247,7 +247,10 @@ def bench_randk(args, g, cfg) -> int:
                 "aggregate": stage_time(lambda: st.inner.run(st.sub, seed), reps),
                 "scatter": stage_time(lambda: st.scatter(), reps)}
     stage_ms = {k: round(v, 4) for k, v in stage_ms.items()}
-    print(json.dumps({
+    base, parity = None, None
+    if not args.no_cpu_baseline:
+        base, parity = randk_cpu_baseline(g, cfg, args.cpu_budget, st, seed)
+    result = {
         "metric": METRIC, "value": round(M * d * args.steps / elapsed / 1e9, 3), "unit": "G elements/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(elapsed / args.steps * 1e3, 4), "higher_is_better": True, "scaling": "weak",
@@ -256,8 +259,43 @@ def bench_randk(args, g, cfg) -> int:
                    "quantizer": "multi" if len(scales) > 1 else "single",
                    "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
-        "stage_ms": stage_ms, "roofline": None, "cpu_baseline": None}))
+        "stage_ms": stage_ms, "roofline": None, "cpu_baseline": base}
+    if parity is not None:
+        result["parity_vs_oracle"] = parity
+    print(json.dumps(result))
     return 0
+
+
+def randk_cpu_baseline(g, cfg, budget_s: float, st, seed: int):
+    """The oracle's GlobalRandK step (its selection over all d keys, then
+    Algorithm 1/2 on the k gathered coordinates) on the host cores over the
+    whole workload, repeated up to about the budget; then one device step
+    compared with it bit for bit."""
+    import numpy as np
+    import torch
+
+    from oracle import oracle
+
+    d, M, scales, k = cfg["d"], cfg["M"], cfg["scales"], cfg["randk"]
+    host = g[:, :d].cpu().numpy()
+    t0 = time.perf_counter()
+    ref = oracle.randk_pipeline(host, k, scales, seed, d=d)
+    dt, runs = time.perf_counter() - t0, 1
+    while dt < 0.75 * budget_s and runs < 64 and dt / runs * (runs + 1) <= budget_s:
+        t1 = time.perf_counter()
+        oracle.randk_pipeline(host, k, scales, seed, d=d)
+        dt += time.perf_counter() - t1
+        runs += 1
+    base = {"value": round(M * d * runs / dt / 1e9, 6), "unit": "G elements/s", "cores": 1, "kind": "oracle",
+            "sample": "full workload" + (f", {runs} runs" if runs > 1 else ""), "seconds": round(dt, 2)}
+    st.run(g, seed)
+    torch.cuda.synchronize()
+    W = np.float32(st.inner.w[0].item())
+    if W != ref["W_oracle"]:
+        ref = oracle.randk_pipeline(host, k, scales, seed, d=d, W=W)
+    ok = (np.array_equal(st.sel[:k].cpu().numpy().view(np.uint32), ref["sel"]) and
+          np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["full"].view(np.int32)))
+    return base, "bit-exact" if ok else "MISMATCH"
 
 
 def main() -> int:

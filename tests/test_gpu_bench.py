@@ -1,7 +1,8 @@
 """bench.py end to end on the GPU at the small workload (d = 2^20, 4 workers,
 one scale s = 127): one JSON line carrying the throughput, the dominant
 kernel's roofline and the oracle's rate on the same input, with the device's
-step bit-exact against that oracle run; host launches and HIP-graph replays."""
+step bit-exact against that oracle run; host launches and HIP-graph replays.
+Also the GlobalRandK line at the ResNet-18 shape."""
 import json
 import os
 import subprocess
@@ -15,8 +16,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 D, M = 1 << 20, 4
 
 
-def run_bench(*extra):
-    cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", "small-gaussian", "--steps", "20",
+def run_bench(*extra, workload="small-gaussian"):
+    cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", workload, "--steps", "20",
            "--warmup", "5", "--cpu-budget", "1", *extra]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=240, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
@@ -49,4 +50,19 @@ def test_bench_line(extra):
 
     base = j["cpu_baseline"]
     assert base["kind"] == "oracle" and base["cores"] >= 1 and base["value"] > 0 and base["sample"]
+    assert j["parity_vs_oracle"] == "bit-exact"
+
+
+def test_randk_bench_line():
+    # GlobalRandK (k = 10000) on the ResNet-18-shaped workload: the oracle's
+    # whole selection and step as the CPU baseline, the device step bit-exact
+    j = run_bench(workload="resnet18-grandk")
+    d, m = 11_173_962, 8
+    assert (j["config"]["workload"], j["config"]["d"], j["config"]["M"], j["config"]["randk"]) == \
+        ("resnet18-grandk", d, m, 10_000)
+    assert j["value"] == pytest.approx(m * d / (j["ms_per_step"] * 1e-3) / 1e9, rel=0.02)
+    assert set(j["stage_ms"]) == {"select", "gather", "aggregate", "scatter"}
+    base = j["cpu_baseline"]
+    assert base["kind"] == "oracle" and base["cores"] >= 1 and base["value"] > 0
+    assert base["sample"].startswith("full workload")
     assert j["parity_vs_oracle"] == "bit-exact"
