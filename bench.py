@@ -8,8 +8,18 @@ integer sum of the codes -> reconstruct the averaged gradient.  The metric is
 gradient elements (M * d worker-coordinates) per second, and the fraction of
 the 8 TB/s HBM peak the step's algorithmic bytes reach.
 
-Prints one JSON line.  Extra modes:
-  --workload NAME       another workload of synth.WORKLOADS (default resnet18)
+The default workload is the largest that fits one GPU: d = 2^30 heavy-tailed
+(Student-t) coordinates, 16 workers streamed one at a time through a resident
+int32 sum, eight scales (Algorithm 2), each worker quantised and added into
+the sum in one fused call.
+
+Prints one JSON line: the step's rate, its stages' times and shares, the
+roofline of the stage with the largest share, the oracle's rate on one core
+and on all cores over a bounded sample, and the device's results on that
+sample checked against the oracle's.  Extra modes:
+  --workload NAME       another workload of synth.WORKLOADS
+  --composed            streamed workers: codes stored, then summed (two calls)
+  --quant-sum           resident workers: one fused quantise-and-sum call
   --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
@@ -44,28 +54,81 @@ def quantize_bytes_per_launch(d: int, rows: int, K: int, bits: int = 8) -> int:
     return rows * (4 * d + code_bytes(d, bits)) + (d if K > 1 else 0)
 
 
-def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8) -> dict:
-    """Bytes each stage must move at minimum (reads + writes), per step.  With
-    several scales and 2 to 16 workers the norm pass also writes the
-    largest |g| over the workers (4 bytes per coordinate), which the index
-    pass reads instead of the gradients; with more workers the index pass
-    reads every gradient again.  The sum stores the int32 sums and, in the
-    same pass, the reconstruction (the sums are not read back)."""
+def quant_sum_bytes_per_call(d: int, rows: int, K: int, accumulate: bool, reconstruct: bool) -> int:
+    """One fused quantise-and-sum call: the rows' gradients and (several
+    scales) the shared index in, the int32 sums out (the old sums in too when
+    accumulating) and, when it reconstructs, the output."""
+    return 4 * rows * d + (d if K > 1 else 0) + (4 * d if accumulate else 0) + 4 * d + (4 * d if reconstruct else 0)
+
+
+def scale_kernels(M: int, K: int) -> list:
+    """The kernels of one uq_shared_scale call, the longest first."""
+    if K == 1:
+        return ["k_sumsq", "k_finish"]
+    if 2 <= M <= FUSED_MAX_ROWS:
+        return ["k_norm_max", "k_rowsum", "k_index_max"]
+    return ["k_sumsq", "k_finish", "k_index"]
+
+
+def shared_scale_bytes(d: int, M: int, K: int) -> int:
+    """The gradients read once for the norm; with several scales and 2 to 16
+    workers that pass also writes the largest |g| over the workers (4 bytes
+    per coordinate), which the index pass reads instead of the gradients;
+    with more workers (or one) the index pass reads every gradient again.
+    The index is written once."""
+    if K == 1:
+        return 4 * M * d
+    if 2 <= M <= FUSED_MAX_ROWS:
+        return 4 * M * d + 4 * d + 4 * d + d
+    return 4 * M * d + 4 * M * d + d
+
+
+def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, quant_sum: bool = False) -> list:
+    """The library calls of one step as stages: name, the kernel it launches
+    (several for the shared scale, the longest first), calls per step and the
+    algorithmic bytes per call."""
     multi = K > 1
+    ib = d if multi else 0
     cb = code_bytes(d, bits)
-    if not multi:
-        scale_bytes = 4 * M * d
-    elif 2 <= M <= FUSED_MAX_ROWS:
-        scale_bytes = 4 * M * d + 4 * d + 4 * d + d
+    qk = ("k_quantise_multi" if multi else "k_quantise_single") + ("" if bits == 8 else f"_{bits}bit")
+    st = [dict(name="shared_scale", kernels=scale_kernels(M, K), calls=1, bytes=shared_scale_bytes(d, M, K))]
+    if quant_sum and streamed:
+        # one worker per call into the running sum; the last call reconstructs
+        if M == 1:
+            st.append(dict(name="quant_sum_last", kernels=["k_quant_sum_set_deq"], calls=1,
+                           bytes=quant_sum_bytes_per_call(d, 1, K, False, True)))
+        else:
+            st.append(dict(name="quant_sum_first", kernels=["k_quant_sum_set"], calls=1,
+                           bytes=quant_sum_bytes_per_call(d, 1, K, False, False)))
+            if M > 2:
+                st.append(dict(name="quant_sum", kernels=["k_quant_sum_acc"], calls=M - 2,
+                               bytes=quant_sum_bytes_per_call(d, 1, K, True, False)))
+            st.append(dict(name="quant_sum_last", kernels=["k_quant_sum_acc_deq"], calls=1,
+                           bytes=quant_sum_bytes_per_call(d, 1, K, True, True)))
+    elif quant_sum:
+        st.append(dict(name="quant_sum", kernels=["k_quant_sum_set_deq"], calls=1,
+                       bytes=quant_sum_bytes_per_call(d, M, K, False, True)))
+    elif streamed:
+        # the codes of one worker per call, then summed into the running sum
+        st.append(dict(name="quantize", kernels=[qk], calls=M, bytes=quantize_bytes_per_launch(d, 1, K, bits)))
+        if M > 1:
+            st.append(dict(name="sum_first", kernels=["k_sum"], calls=1, bytes=cb + 4 * d))
+            if M > 2:
+                st.append(dict(name="sum", kernels=["k_sum"], calls=M - 2, bytes=cb + 8 * d))
+        st.append(dict(name="sum_dequantize", kernels=["k_sum_dequant"], calls=1,
+                       bytes=cb + (8 * d if M > 1 else 4 * d) + 4 * d + ib))
     else:
-        scale_bytes = 4 * M * d + 4 * M * d + d
-    b = {
-        "shared_scale": scale_bytes,
-        "quantize": ((M * quantize_bytes_per_launch(d, 1, K, bits)) if streamed
-                     else quantize_bytes_per_launch(d, M, K, bits)),
-        "sum_dequantize": (((M * cb + 4 * d) if not streamed else (cb + 4 * d) + (M - 1) * (cb + 8 * d)) +
-                           d * (4 + (1 if multi else 0))),
-    }
+        st.append(dict(name="quantize", kernels=[qk], calls=1, bytes=quantize_bytes_per_launch(d, M, K, bits)))
+        st.append(dict(name="sum_dequantize", kernels=["k_sum_dequant"], calls=1, bytes=M * cb + 4 * d + 4 * d + ib))
+    return st
+
+
+def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8, quant_sum: bool = False) -> dict:
+    """Bytes each stage must move at minimum (reads + writes) per step, and
+    their total."""
+    b = {}
+    for s in plan_stages(d, M, K, bits, streamed, quant_sum):
+        b[s["name"]] = b.get(s["name"], 0) + s["calls"] * s["bytes"]
     b["total"] = sum(b.values())
     return b
 
@@ -163,10 +226,9 @@ def copy_probe(nbytes: int) -> None:
 
 def stage_ms_per_call(torch, stream, fn, reps: int, rounds: int = 3) -> float:
     """GPU time per call (ms) of fn repeated back to back between two events
-    on `stream`, its inputs already in place.  Best of `rounds` rounds: a
-    round in which the host fell behind the GPU (a stall in the runtime's
-    launch path) reads high, so the lowest round is the stage's own time."""
-    best = float("inf")
+    on `stream`, its inputs already in place: the mean over `rounds` rounds of
+    `reps` calls (rounds in which the host fell behind the GPU count too)."""
+    total = 0.0
     for _ in range(rounds):
         fn()
         torch.cuda.synchronize()
@@ -177,8 +239,8 @@ def stage_ms_per_call(torch, stream, fn, reps: int, rounds: int = 3) -> float:
             fn()
         b.record(stream)
         torch.cuda.synchronize()
-        best = min(best, a.elapsed_time(b) / reps)
-    return best
+        total += a.elapsed_time(b) / reps
+    return total / rounds
 
 
 def stage_reps(steps: int, step_s: float) -> int:
@@ -187,33 +249,81 @@ def stage_reps(steps: int, step_s: float) -> int:
     return max(10, min(steps, int(0.1 / max(step_s, 1e-9))))
 
 
-def cpu_baseline(g, cfg, budget_s: float):
-    """The oracle on the host cores over a bounded sample of the workload."""
+# One core's oracle time per worker-coordinate for the whole step, about:
+# two Philox blocks per code dominate; several scales add the index rule.
+ORACLE_NS_PER_ELEMENT = {False: 48e-9, True: 58e-9}
+
+
+def sample_size(d: int, M: int, multi: bool, budget_s: float) -> int:
+    """Coordinates of the CPU baseline's sample: about budget_s of one core's
+    oracle work over all M workers, at least 4096, at most d."""
+    return min(d, max(4096, int(budget_s / (ORACLE_NS_PER_ELEMENT[multi] * M))))
+
+
+def _timed_runs(fn, budget_s: float):
+    """fn() once, then again on the same input until about budget_s is spent
+    (a sample that finishes well inside the budget is not one short run).
+    Returns (first result, runs, seconds)."""
+    t0 = time.perf_counter()
+    first = fn()
+    dt, runs = time.perf_counter() - t0, 1
+    while dt < 0.75 * budget_s and runs < 64 and dt / runs * (runs + 1) <= budget_s:
+        t1 = time.perf_counter()
+        fn()
+        dt += time.perf_counter() - t1
+        runs += 1
+    return first, runs, dt
+
+
+def cpu_baseline(g, cfg, budget_s: float, W=None, threads=None):
+    """The oracle over a bounded sample of the workload (all M workers,
+    coordinates [0, dn)), on one host core and on `threads` cores (default:
+    the cores this process may use, at most 16).  W: the scale the later
+    steps use (the device's, so that its results are comparable); the oracle
+    still forms its own norm over the sample, so the work is the whole step's.
+    Returns the baseline record, the one-core run's result and dn."""
+    from oracle import oracle
+
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    threads = oracle.default_threads() if threads is None else threads
+    dn = sample_size(d, M, len(scales) > 1, budget_s)
+    host = g[:, :dn].cpu().numpy()
+    ref, runs1, dt1 = _timed_runs(lambda: oracle.pipeline(host, scales, seed, d=dn, W=W), budget_s)
+    _, runsn, dtn = _timed_runs(lambda: oracle.pipeline_threaded(host, scales, seed, d=dn, W=W, threads=threads),
+                                budget_s)
+    sample = "full workload" if dn == d else f"all {M} workers, coordinates [0, {dn}) of {d}"
+    rec = {"value": round(M * dn * runsn / dtn / 1e9, 6), "unit": "G elements/s", "cores": threads,
+           "kind": "oracle", "sample": f"{sample}, {runsn} runs", "seconds": round(dtn, 2),
+           "one_core": {"value": round(M * dn * runs1 / dt1 / 1e9, 6), "cores": 1, "runs": runs1,
+                        "seconds": round(dt1, 2)}}
+    return rec, ref, dn
+
+
+def parity_on_sample(step, ref, dn: int, d: int, bits: int) -> str:
+    """The device's step against the oracle's run on coordinates [0, dn) with
+    the same W: scale index, codes (when the step keeps them; packed codes
+    unpacked), sums and outputs bit for bit; W within one binary32 ulp of the
+    oracle's own when the sample is the whole vector."""
     import numpy as np
 
     from oracle import oracle
 
-    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
-    # ~41 ns per worker-coordinate for the oracle's whole step on one core
-    dn = min(d, max(4096, int(budget_s / (45e-9 * M))))
-    host = g[:, :dn].cpu().numpy()
-    t0 = time.perf_counter()
-    ref = oracle.pipeline(host, scales, seed, d=dn)
-    dt = time.perf_counter() - t0
-    # a sample that finishes well inside the budget is run again (same input,
-    # same result) until about the budget is spent, so the rate is not one
-    # short run's
-    runs = 1
-    while dt < 0.75 * budget_s and runs < 64 and dt / runs * (runs + 1) <= budget_s:
-        t1 = time.perf_counter()
-        oracle.pipeline(host, scales, seed, d=dn)
-        dt += time.perf_counter() - t1
-        runs += 1
-    sample = "full workload" if dn == d else f"all {M} workers, coordinates [0, {dn}) of {d}"
-    if runs > 1:
-        sample += f", {runs} runs"
-    return {"value": round(M * dn * runs / dt / 1e9, 6), "unit": "G elements/s", "cores": 1, "kind": "oracle",
-            "sample": sample, "seconds": round(dt, 2)}, ref, dn
+    ok = True
+    if dn == d:
+        a = int(np.float32(step.w[0].item()).view(np.int32))
+        ok = abs(a - int(np.float32(ref["W_oracle"]).view(np.int32))) <= 1
+    if ref["idx"] is not None:
+        ok = ok and np.array_equal(step.idx[:dn].cpu().numpy(), ref["idx"])
+    if step.codes is not None and not step.streamed:
+        if bits == 8:
+            ok = ok and np.array_equal(step.codes[:, :dn].cpu().numpy(), ref["codes"])
+        else:
+            packed = step.codes[:, :(dn * bits + 7) // 8].cpu().numpy()
+            ok = ok and all(np.array_equal(oracle.unpack_codes(packed[m], dn, bits), ref["codes"][m])
+                            for m in range(packed.shape[0]))
+    ok = ok and np.array_equal(step.sum[:dn].cpu().numpy(), ref["sum"])
+    ok = ok and np.array_equal(step.out[:dn].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+    return "bit-exact" if ok else "MISMATCH"
 
 
 def bench_randk(args, g, cfg) -> int:
@@ -298,16 +408,48 @@ def randk_cpu_baseline(g, cfg, budget_s: float, st, seed: int):
     return base, "bit-exact" if ok else "MISMATCH"
 
 
+def progress(msg: str) -> None:
+    """One line on stderr per finished phase of the run."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+
+def stage_fns(step, g, seed: int, M: int) -> dict:
+    """The library call behind each stage of plan_stages, on the step's own
+    buffers (its inputs are the previous stage's outputs, already in place)."""
+    last = M - 1
+    return {
+        "shared_scale": lambda: step.shared_scale(g),
+        "quant_sum_first": lambda: step.quantize_sum(g[0:1], seed, rows=1, worker0=0, accumulate=0,
+                                                     reconstruct=False),
+        "quant_sum": ((lambda: step.quantize_sum(g[1:2], seed, rows=1, worker0=1, accumulate=1, reconstruct=False))
+                      if step.streamed else (lambda: step.quantize_sum(g, seed))),
+        "quant_sum_last": lambda: step.quantize_sum(g[last:last + 1], seed, rows=1, worker0=last,
+                                                    accumulate=1 if M > 1 else 0, reconstruct=True),
+        "quantize": ((lambda: step.quantize(g[:1], seed, rows=1)) if step.streamed
+                     else (lambda: step.quantize(g, seed))),
+        "sum_first": lambda: step.sum_codes(rows=1, accumulate=0),
+        "sum": lambda: step.sum_codes(rows=1, accumulate=1),
+        "sum_dequantize": ((lambda: step.sum_dequantize(rows=1, accumulate=1 if M > 1 else 0)) if step.streamed
+                           else (lambda: step.sum_dequantize())),
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     # the first few tens of steps of a process run slower than the rest
-    # (clocks ramping up); the defaults time 200 steps after 50 untimed ones
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="resnet18")
+    # (clocks ramping up); the defaults time 100 steps after 20 untimed ones
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="student-t")
+    ap.add_argument("--composed", action="store_true",
+                    help="streamed workers: quantise and sum in separate calls (codes through HBM) instead of "
+                         "the fused quantise-and-sum")
+    ap.add_argument("--quant-sum", action="store_true",
+                    help="resident workers: quantise and sum all rows in one fused call (no codes stored)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work to aim for")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle work to aim for, for each of the two CPU figures")
     ap.add_argument("--copy-probe", type=int, default=0)
     ap.add_argument("--stream-probe", action="store_true")
     ap.add_argument("--graph", action="store_true",
@@ -320,7 +462,6 @@ def main() -> int:
               "multi-GPU runs are not part of this build (use --gpus 1).", file=sys.stderr)
         return 2
 
-    import numpy as np
     import torch
 
     if not torch.cuda.is_available():
@@ -334,31 +475,25 @@ def main() -> int:
         return 0
 
     import synth
-    from paper_2109_12497_amd.step import Step  # fails loudly if libuq.so is not built
+    from paper_2109_12497_amd.step import Step, capture  # fails loudly if libuq.so is not built
 
     g, cfg = synth.make_gradients(args.workload, device="cuda")
     d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
     streamed = bool(cfg.get("streamed", False))
     K = len(scales)
     stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    progress(f"{args.workload}: {M} x {d} gradients generated")
     if cfg.get("randk"):
         return bench_randk(args, g, cfg)
     bits = int(cfg.get("bits", 8))
-    step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits)
-    torch.cuda.synchronize()
-
-    for _ in range(args.warmup):
-        step.run(g, seed)
+    quant_sum = (streamed and not args.composed) or (not streamed and args.quant_sum)
+    step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits, quant_sum=quant_sum)
     torch.cuda.synchronize()
 
     # -- timed region: K whole steps (host launches, or with --graph replays
     # of the step's kernels captured once in a HIP graph)
-    from paper_2109_12497_amd.step import capture
-
-    if args.graph:
-        replay = capture(step, g, seed).replay
-    else:
-        replay = lambda: step.run(g, seed)  # noqa: E731
+    replay = capture(step, g, seed).replay if args.graph else (lambda: step.run(g, seed))
     for _ in range(args.warmup):
         replay()
     torch.cuda.synchronize()
@@ -369,40 +504,29 @@ def main() -> int:
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed / args.steps * 1e3
     value = M * d * args.steps / elapsed / 1e9
+    progress(f"{args.steps} steps timed: {ms_per_step:.4f} ms per step")
 
-    # -- per-stage times: each stage repeated back to back between two events
-    # on the stream (its inputs are the previous stage's outputs, already in
-    # place), so host launch overhead does not enter the figures
-    def stage_time(fn, reps):
-        return stage_ms_per_call(torch, stream, fn, reps)
-
+    # -- per-stage times: each stage's call repeated back to back between two
+    # events on the stream (mean over rounds), so host launch overhead does
+    # not enter them; a stage's share of the step is calls x time per call
+    stages = plan_stages(d, M, K, bits, streamed, quant_sum)
+    fns = stage_fns(step, g, seed, M)
     reps = stage_reps(args.steps, elapsed / args.steps)
-    stage_ms = {"shared_scale": stage_time(lambda: step.shared_scale(g), reps)}
-    if streamed:
-        # one worker row per call, M calls per step, the last of them fused
-        # with the reconstruction
-        stage_ms["quantize"] = M * stage_time(lambda: step.quantize(g[:1], seed, rows=1), reps)
-        stage_ms["sum_dequantize"] = ((M - 1) * stage_time(lambda: step.sum_codes(rows=1, accumulate=1), reps) +
-                                      stage_time(lambda: step.sum_dequantize(rows=1, accumulate=1), reps))
-    else:
-        stage_ms["quantize"] = stage_time(lambda: step.quantize(g, seed), reps)
-        stage_ms["sum_dequantize"] = stage_time(lambda: step.sum_dequantize(), reps)
-    nbytes = algorithmic_bytes(d, M, K, streamed, bits)
+    for st in stages:
+        st["ms"] = stage_ms_per_call(torch, stream, fns[st["name"]], reps)
+    step_bytes = sum(st["calls"] * st["bytes"] for st in stages)
+    progress("stages timed: " + ", ".join(f"{st['name']} {st['ms']:.4f} ms x {st['calls']}" for st in stages))
 
-    # -- dominant kernel (the quantiser): launches back to back between two
-    # events on the stream it runs on, so the average is the kernel's own
-    # duration (the figure rocprofv3 reports for k_quantise); best of three
-    # rounds, as for the stages, so that a round in which the host stalled
-    # does not count idle time as kernel time
-    reps = max(10, args.steps)
-    rows_per_launch = 1 if streamed else M
-    step.shared_scale(g)
-    q_launch_ms = stage_ms_per_call(
-        torch, stream, lambda: step.quantize(g[:rows_per_launch], seed, rows=rows_per_launch), reps)
-    q_bytes_launch = quantize_bytes_per_launch(d, rows_per_launch, K, bits)
-    achieved = q_bytes_launch / (q_launch_ms * 1e-3) / 1e9
-    kernel_name = ("k_quantise_multi" if K > 1 else "k_quantise_single") + ("" if bits == 8 else f"_{bits}bit")
-    traffic = measured_traffic(kernel_name, args.workload)
+    # -- the roofline of the stage with the largest share of the step: its
+    # algorithmic bytes per call over its mean time per call (for the shared
+    # scale, one call runs its two or three kernels: the figure then covers
+    # them together)
+    dom = max(stages, key=lambda st: st["calls"] * st["ms"])
+    achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+    traffic = None
+    per_kernel = [measured_traffic(k, args.workload) for k in dom["kernels"]]
+    if all(t is not None for t in per_kernel):
+        traffic = sum(per_kernel)
 
     result = {
         "metric": METRIC,
@@ -419,34 +543,36 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed,
                    "quantizer": "multi" if K > 1 else "single", "streamed": streamed, "code_bits": bits,
+                   "path": "quantise-and-sum fused" if quant_sum else "codes stored, then summed",
                    "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
-        "pct_hbm_peak": round(100 * nbytes["total"] / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),
-        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
-        "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes_per_launch": q_bytes_launch,
-                     "avg_launch_us": round(q_launch_ms * 1e3, 2)},
+        "pct_hbm_peak": round(100 * step_bytes / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),
+        "step_bytes": step_bytes,
+        "stage_ms": {st["name"]: round(st["ms"], 4) for st in stages},
+        "stage_share": {st["name"]: round(st["calls"] * st["ms"] / ms_per_step, 3) for st in stages},
+        "roofline": {"bound": "hbm", "kernel": "+".join(dom["kernels"]), "stage": dom["name"],
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": dom["bytes"], "avg_launch_us": round(dom["ms"] * 1e3, 2),
+                     "launches_per_step": dom["calls"]},
         "cpu_baseline": None,
     }
 
     if not args.no_cpu_baseline:
-        base, ref, dn = cpu_baseline(g, cfg, args.cpu_budget)
-        result["cpu_baseline"] = base
-        step.run(g, seed)  # one whole step, after the stage timings
-        torch.cuda.synchronize()
-        # the oracle ran on the same inputs: compare what it covers (free parity check)
-        W = np.float32(step.w[0].item())
-        if dn == d and not streamed:
-            same_w = W == ref["W_oracle"]
-            if not same_w:
-                from oracle import oracle
+        import numpy as np
 
-                ref = oracle.pipeline(g[:, :d].cpu().numpy(), scales, seed, d=d, W=W)
-            ok = (np.array_equal(step.codes[:, :d].cpu().numpy(), ref["codes"]) and
-                  np.array_equal(step.sum[:d].cpu().numpy(), ref["sum"]) and
-                  np.array_equal(step.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32)))
-            result["parity_vs_oracle"] = "bit-exact" if ok else "MISMATCH"
+        # one whole step after the stage timings, then the oracle on the same
+        # inputs and the same W over a bounded sample: the CPU figures, and the
+        # device's results on that sample checked against them
+        step.run(g, seed)
+        torch.cuda.synchronize()
+        W = np.float32(step.w[0].item())
+        base, ref, dn = cpu_baseline(g, cfg, args.cpu_budget, W=W)
+        progress(f"oracle: {base['one_core']['value']} G el/s on one core, {base['value']} on {base['cores']}")
+        result["cpu_baseline"] = base
+        result["parity_vs_oracle"] = parity_on_sample(step, ref, dn, d, bits)
+        progress(f"parity on coordinates [0, {dn}): {result['parity_vs_oracle']}")
+        result["parity_sample"] = f"coordinates [0, {dn}) of {d}, every worker"
     print(json.dumps(result))
     return 0
 

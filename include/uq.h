@@ -168,6 +168,32 @@ int uq_sum_dequantize(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc
                       int32_t accumulate, int32_t* sum, int32_t M, const float* w, const float* scales,
                       int32_t K, const uint8_t* idx, float* out, void* stream);
 
+/*
+ * Quantise and sum in one pass: the codes of uq_quantize_single (K = 1,
+ * scales = {s}) or uq_quantize_multi (K > 1) for `rows` workers, added into
+ * the int32 sum without being stored anywhere: Eq. (8) / Eq. (12) and the
+ * all-reduce of Algorithm 1/2 fused.  With out != NULL the reconstruction of
+ * Eq. (9) / Eq. (13) with the 1/M of the averaging step is applied to the
+ * sums as they are stored (the rule of uq_dequantize).  Bit for bit the same
+ * sum and out as uq_quantize_* followed by uq_sum_codes (and uq_dequantize);
+ * a worker streamed through a resident accumulator is one call with
+ * rows = 1, accumulate = 0 for the first worker and 1 after it, and out set
+ * on the last.
+ *   g, d, rows, ldg, worker0, w, seed   as for uq_quantize_single
+ *   scales, K, idx   as for uq_quantize_multi; idx is not read when K == 1
+ *   accumulate       0: sum = the rows' total; 1: sum += the rows' total
+ *   sum              [d] int32 (written, or read and written)
+ *   M, out           NULL: no reconstruction (M is then ignored); else out
+ *                    [d] fp32 (written) and M as for uq_dequantize, whose
+ *                    checks then apply
+ * Keeping a running sum in range over many accumulating calls is the
+ * caller's concern.
+ */
+int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                    const float* w, const float* scales, int32_t K, const uint8_t* idx,
+                    uint64_t seed, int32_t accumulate, int32_t* sum, int32_t M, float* out,
+                    void* stream);
+
 /* ------------------------------------------------------------------------
  * Sub-byte codes.  The paper stores every code in 8 bits because its
  * framework had no narrower type, and found bit-packing too slow (Sec. 5,

@@ -206,6 +206,111 @@ def pipeline(g: np.ndarray, scales, seed: int, d: int | None = None, W=None,
 
 
 # ---------------------------------------------------------------------------
+# The same steps on several host threads.  Every per-coordinate step is a pure
+# function of its coordinate, and each row's norm is still one sequential
+# index-order sum, so splitting the rows and fixed coordinate chunks over
+# threads changes no byte of any result; the C calls release the GIL.
+# ---------------------------------------------------------------------------
+
+def default_threads() -> int:
+    """Host threads for the parallel driver: the cores this process may use,
+    at most 16."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def _run_jobs(jobs, threads: int) -> None:
+    if threads <= 1 or len(jobs) <= 1:
+        for job in jobs:
+            job()
+        return
+    from concurrent.futures import ThreadPoolExecutor
+
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        for f in [ex.submit(job) for job in jobs]:
+            f.result()
+
+
+def _chunks(n: int, chunk: int):
+    return [(c, min(n, c + chunk)) for c in range(0, n, chunk)]
+
+
+def shared_scale_threaded(g: np.ndarray, d: int | None = None, threads: int = 1):
+    """shared_scale with the rows on `threads` threads (each row's sum of
+    squares sequential in index order, as there)."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    M, ldg = g.shape
+    d = ldg if d is None else d
+    L = lib()
+    S = np.zeros(M, dtype=np.float64)
+    base = g.ctypes.data
+
+    def norm(m):
+        S[m] = L.orc_sum_of_squares(base + 4 * m * ldg, d)
+
+    _run_jobs([lambda m=m: norm(m) for m in range(M)], threads)
+    return np.float32(L.orc_max_norm(_ptr(S), M)), S
+
+
+def window(g: np.ndarray, W, scales, seed: int, i0: int = 0, n: int | None = None, worker0: int = 0,
+           threads: int = 1, chunk: int = 1 << 20) -> dict:
+    """The steps after the shared scale for coordinates i0 .. i0+n-1, given W:
+    g [M, >= n] holds those coordinates of every worker.  Returns idx (None
+    for one scale), codes [M, n], sum [n] and out [n], as pipeline does."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    M, ldg = g.shape
+    n = ldg if n is None else n
+    s = _scales(scales)
+    K = s.size
+    W = np.float32(W)
+    L = lib()
+    gp, sp = g.ctypes.data, _ptr(s)
+    parts = _chunks(n, chunk)
+    idx = np.zeros(n, dtype=np.uint8) if K > 1 else None
+    if idx is not None:
+        ip = idx.ctypes.data
+
+        def index(c0, c1):
+            scratch = np.zeros(c1 - c0, dtype=np.uint8)
+            L.orc_scale_index_shared(gp + 4 * c0, c1 - c0, M, ldg, W, sp, K, ip + c0, _ptr(scratch))
+
+        _run_jobs([lambda a=a, b=b: index(a, b) for a, b in parts], threads)
+    codes = np.zeros((M, n), dtype=np.int8)
+    cp = codes.ctypes.data
+
+    def quant(m, c0, c1):
+        L.orc_quantize(gp + 4 * (m * ldg + c0), c1 - c0, i0 + c0, worker0 + m, W, sp, K,
+                       None if idx is None else ip + c0, seed, cp + m * n + c0)
+
+    _run_jobs([lambda m=m, a=a, b=b: quant(m, a, b) for m in range(M) for a, b in parts], threads)
+    sums = np.zeros(n, dtype=np.int32)
+    out = np.zeros(n, dtype=np.float32)
+    up, op = sums.ctypes.data, out.ctypes.data
+
+    def add_and_reconstruct(c0, c1):
+        L.orc_sum_codes(cp + c0, c1 - c0, M, n, up + 4 * c0)
+        L.orc_dequantize(up + 4 * c0, c1 - c0, M, W, sp, K, None if idx is None else ip + c0, op + 4 * c0)
+
+    _run_jobs([lambda a=a, b=b: add_and_reconstruct(a, b) for a, b in parts], threads)
+    return {"idx": idx, "codes": codes, "sum": sums, "out": out}
+
+
+def pipeline_threaded(g: np.ndarray, scales, seed: int, d: int | None = None, W=None, worker0: int = 0,
+                      threads: int | None = None, chunk: int = 1 << 20) -> dict:
+    """pipeline() with the rows (norm) and fixed coordinate chunks (every
+    later step) spread over `threads` host threads; byte for byte the same
+    result for any thread count."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    M, ldg = g.shape
+    d = ldg if d is None else d
+    threads = default_threads() if threads is None else threads
+    W_own, S = shared_scale_threaded(g, d, threads)
+    W = W_own if W is None else np.float32(W)
+    r = window(g, W, scales, seed, i0=0, n=d, worker0=worker0, threads=threads, chunk=chunk)
+    r.update(W=W, W_oracle=W_own, sumsq=S)
+    return r
+
+
+# ---------------------------------------------------------------------------
 # Sub-byte codes
 # ---------------------------------------------------------------------------
 

@@ -343,6 +343,36 @@ int uq_sum_dequantize(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc
                                            static_cast<hipStream_t>(stream)));
 }
 
+int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                    const float* scales, int32_t K, const uint8_t* idx, uint64_t seed, int32_t accumulate,
+                    int32_t* sum, int32_t M, float* out, void* stream)
+{
+    uq::ScaleSet S;
+    UQ_TRY(check_scales(scales, K, &S));
+    UQ_TRY(check_dims(d, rows, "rows"));
+    UQ_TRY(check_rows(g, d, rows, ldg, 4, "g"));
+    UQ_TRY(check_w(w));
+    if (worker0 < 0 || static_cast<int64_t>(worker0) + rows > (int64_t(1) << 31))
+        return fail(UQ_ERANGE, "worker ids %d .. %lld exceed [0, 2^31)", worker0,
+                    (long long)worker0 + rows - 1);
+    if (K > 1) {
+        if (idx == nullptr && d > 0)
+            return fail(UQ_EINVAL, "idx is NULL");
+        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    } else {
+        idx = nullptr;  // one scale: the index is not read
+    }
+    if (accumulate != 0 && accumulate != 1)
+        return fail(UQ_EINVAL, "accumulate must be 0 or 1");
+    UQ_TRY(check_vec(sum, d, "sum"));
+    if (out != nullptr) {
+        uq::ScaleSet S2;
+        UQ_TRY(check_reconstruction(d, M, w, scales, K, idx, out, &S2));
+    }
+    return launched(uq::launch_quant_sum(g, d, rows, ldg, worker0, w, S, idx, seed, accumulate, sum, M, out,
+                                         static_cast<hipStream_t>(stream)));
+}
+
 size_t uq_randk_workspace_bytes(int64_t d, int64_t K)
 {
     (void)d;

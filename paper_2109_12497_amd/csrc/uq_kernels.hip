@@ -1167,6 +1167,255 @@ __global__ __launch_bounds__(kBlock) void k_dequant(const int32_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// Quantise and sum in one pass (Eq. (8)/(12) and the all-reduce of Algorithm
+// 1/2): the rows' codes, exactly those k_quantise would store, are added into
+// the int32 sums in registers and never stored.  A wave takes one
+// 512-coordinate tile (the lane layout of k_quantise: quads A = 4t .. 4t+3
+// and B = 256+4t .. 256+4t+3) of every row in turn, so the shared index and
+// the tables are looked up once per tile; the next row's loads go out before
+// the current row is coded.  The tile's sums are then stored once (the old
+// sums added first when accumulating) and, with DEQ, so is the reconstruction
+// of those sums, RN32(sum * deq_k).  Per streamed row this moves 4 + 1 bytes
+// in and 4 (+ 4 read when accumulating) per coordinate, against 6 + 9 for the
+// quantiser followed by the sum.
+// ---------------------------------------------------------------------------
+
+// The codes of up to kPairRows rows are summed in the 16-bit lanes of the
+// pair registers (|sum| <= 256 * 127 < 2^15, so the wrapped 16-bit sums are
+// exact), then widened to int32.
+constexpr int32_t kPairRows = 256;
+
+template <bool NT>
+__device__ __forceinline__ i32x4 load_sum4(const int32_t* p)
+{
+    if (NT)
+        return __builtin_nontemporal_load(reinterpret_cast<const i32x4*>(p));
+    return *reinterpret_cast<const i32x4*>(p);
+}
+
+template <bool NT>
+__device__ __forceinline__ void store_sum4(int32_t* p, i32x4 v)
+{
+    if (NT)
+        __builtin_nontemporal_store(v, reinterpret_cast<i32x4*>(p));
+    else
+        *reinterpret_cast<i32x4*>(p) = v;
+}
+
+// Adds the 16-bit lane sums of h[4] (codes A0 A1, A2 A3, B0 B1, B2 B3) to the
+// int32 sums acc[8] and clears h.
+__device__ __forceinline__ void widen_pairs(uint32_t h[4], int32_t acc[8])
+{
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        acc[2 * j] += __builtin_amdgcn_sbfe(static_cast<int32_t>(h[j]), 0, 16);
+        acc[2 * j + 1] += __builtin_amdgcn_sbfe(static_cast<int32_t>(h[j]), 16, 16);
+        h[j] = 0u;
+    }
+}
+
+// One tile of every row: `in` holds row 0's quads and the tile's index words,
+// oldA / oldB the sums already stored (when ACC).  inv_t / inv0 / s0x as for
+// code_tile.
+template <bool MULTI, bool PRE, bool ACC, bool DEQ, bool NT, bool ROW1>
+__device__ __forceinline__ void quant_sum_tile(const float* __restrict__ g, int64_t ldg, int32_t rows,
+                                               uint32_t worker0, int64_t T, TileIn in, i32x4 oldA, i32x4 oldB,
+                                               const float* inv_t, float inv0, float s0x, uint32_t kmax,
+                                               uint32_t key0, uint32_t key1, uint32_t one2,
+                                               int32_t* __restrict__ sum, const float* deq_t,
+                                               float* __restrict__ out)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t a_off = (T << 9) + 4 * lane;
+    float inv[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        inv[j] = MULTI ? inv_t[min((in.ka >> (8 * j)) & 0xFFu, kmax)] : inv0;
+        inv[j + 4] = MULTI ? inv_t[min((in.kb >> (8 * j)) & 0xFFu, kmax)] : inv0;
+    }
+    int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+    int32_t pending = 0;
+    f32x4 A = in.A, B = in.B;
+    const int32_t nrows = ROW1 ? 1 : rows;
+    for (int32_t r = 0; r < nrows; ++r) {
+        f32x4 nA = A, nB = B;
+        if (!ROW1 && r + 1 < nrows) {
+            const float* nrow = g + static_cast<int64_t>(r + 1) * ldg;
+            nA = load_nt(nrow + a_off);
+            nB = load_nt(nrow + a_off + 256);
+        }
+        const float v[8] = {A.x, A.y, A.z, A.w, B.x, B.y, B.z, B.w};
+        uint32_t p[4];
+        tile_codes<PRE>(v, inv, s0x, T, worker0 + static_cast<uint32_t>(r), key0, key1, one2, p);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            h[j] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, h[j]) + __builtin_bit_cast(u16x2, p[j]));
+        if (++pending == kPairRows) {
+            widen_pairs(h, acc);
+            pending = 0;
+        }
+        A = nA;
+        B = nB;
+    }
+    widen_pairs(h, acc);
+    i32x4 sa = {acc[0], acc[1], acc[2], acc[3]};
+    i32x4 sb = {acc[4], acc[5], acc[6], acc[7]};
+    if (ACC) {
+        sa += oldA;
+        sb += oldB;
+    }
+    store_sum4<NT>(sum + a_off, sa);
+    store_sum4<NT>(sum + a_off + 256, sb);
+    if (DEQ) {
+        // the index words again (two registers live instead of eight indices)
+        const auto k = [&](uint32_t word, int j) { return MULTI ? min((word >> (8 * j)) & 0xFFu, kmax) : 0u; };
+        f32x4 oa, ob;
+        oa.x = static_cast<float>(sa.x) * deq_t[k(in.ka, 0)];
+        oa.y = static_cast<float>(sa.y) * deq_t[k(in.ka, 1)];
+        oa.z = static_cast<float>(sa.z) * deq_t[k(in.ka, 2)];
+        oa.w = static_cast<float>(sa.w) * deq_t[k(in.ka, 3)];
+        ob.x = static_cast<float>(sb.x) * deq_t[k(in.kb, 0)];
+        ob.y = static_cast<float>(sb.y) * deq_t[k(in.kb, 1)];
+        ob.z = static_cast<float>(sb.z) * deq_t[k(in.kb, 2)];
+        ob.w = static_cast<float>(sb.w) * deq_t[k(in.kb, 3)];
+        store_nt(out + a_off, oa);
+        store_nt(out + a_off + 256, ob);
+    }
+}
+
+// The coordinates past the last whole tile (fewer than 512): lane t of one
+// wave takes the 8 contiguous coordinates of group ntiles * 64 + t for every
+// row, then stores their sums (and reconstruction).  inv_s holds s_k / W (not
+// scaled).
+template <bool MULTI, bool ACC, bool DEQ>
+__device__ __forceinline__ void quant_sum_tail(const float* __restrict__ g, int64_t d, int64_t ldg, int32_t rows,
+                                               uint32_t worker0, const uint8_t* __restrict__ idx, int64_t ntiles,
+                                               const float* inv_s, float inv0, float s0, uint32_t kmax,
+                                               uint32_t key0, uint32_t key1, int32_t* __restrict__ sum,
+                                               const float* deq_t, float* __restrict__ out)
+{
+    const int64_t q = (ntiles << 6) + (threadIdx.x & 63);
+    const int64_t base = q << 3;
+    if (base >= d)
+        return;
+    float inv[8];
+    uint32_t kk[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        kk[j] = MULTI ? min(static_cast<uint32_t>(base + j < d ? idx[base + j] : 0), kmax) : 0u;
+        inv[j] = MULTI ? inv_s[kk[j]] : inv0;
+    }
+    int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int32_t r = 0; r < rows; ++r) {
+        const float* row = g + static_cast<int64_t>(r) * ldg;
+        float v[8];
+        int32_t code[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            v[j] = base + j < d ? row[base + j] : 0.0f;
+        quantise_group(v, inv, s0, static_cast<uint64_t>(q), worker0 + static_cast<uint32_t>(r), key0, key1, code);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc[j] += code[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (base + j < d) {
+            const int32_t s = acc[j] + (ACC ? sum[base + j] : 0);
+            sum[base + j] = s;
+            if (DEQ)
+                out[base + j] = static_cast<float>(s) * deq_t[kk[j]];
+        }
+    }
+}
+
+// ROW1: the one-row form (a streamed worker), compiled apart so that it does
+// not carry the row loop's registers.
+template <bool MULTI, bool ACC, bool DEQ, bool NT, bool ROW1>
+__global__ __launch_bounds__(kBlock) void k_quant_sum(const float* __restrict__ g, int64_t d, int32_t rows,
+                                                      int64_t ldg, int32_t worker0, const float* __restrict__ wptr,
+                                                      ScaleSet S, const uint8_t* __restrict__ idx, uint32_t key0,
+                                                      uint32_t key1, int32_t* __restrict__ sum, int32_t M,
+                                                      float* __restrict__ out)
+{
+    __shared__ float inv_s[kMaxScales];  // s_k / W
+    __shared__ float inv_p[kMaxScales];  // s_k / W * 2^16 when pre
+    __shared__ float deq_s[kMaxScales];  // RN32(W / (M s_k))
+    const int lane = threadIdx.x & 63;
+    const int64_t ntiles = d >> 9;
+    const int32_t wave_in_block = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave_in_block;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
+    const uint32_t w0 = static_cast<uint32_t>(worker0);
+
+    // the first tile's loads (row 0, its index words, the old sums) go out
+    // before W is read and the tables are formed
+    TileIn in0 = {};
+    i32x4 oldA0 = {0, 0, 0, 0}, oldB0 = {0, 0, 0, 0};
+    if (first < ntiles) {
+        const int64_t a_off = (first << 9) + 4 * lane;
+        in0 = load_tile<MULTI>(g, idx, a_off);
+        if (ACC) {
+            oldA0 = load_sum4<NT>(sum + a_off);
+            oldB0 = load_sum4<NT>(sum + a_off + 256);
+        }
+    }
+
+    const float W = *wptr;
+    const float q0 = div_rn32(S.s[0], W);
+    const bool zero = zero_path(W, q0);
+    const bool pre = zero || (MULTI ? div_rn32(S.s_last, W) : q0) <= 0x1p100f;
+    if (threadIdx.x < S.K) {
+        const float inv = zero ? 0.0f : div_rn32(S.s[threadIdx.x], W);
+        inv_s[threadIdx.x] = inv;
+        inv_p[threadIdx.x] = pre ? inv * 65536.0f : inv;
+        if (DEQ) {
+            const float denom = static_cast<float>(static_cast<double>(M) * static_cast<double>(S.s[threadIdx.x]));
+            deq_s[threadIdx.x] = zero ? 0.0f : div_rn32(W, denom);
+        }
+    }
+    __syncthreads();
+    const float inv0 = zero ? 0.0f : q0;
+    const float s0 = S.s[0];
+    const uint32_t kmax = static_cast<uint32_t>(S.K - 1);
+    uint32_t one2 = 0x00010001u;
+    asm("" : "+s"(one2));
+
+    // the preloaded tile, then (on a grid capped below one tile per wave)
+    // every stride-th tile after it
+    if (first < ntiles) {
+        if (pre)
+            quant_sum_tile<MULTI, true, ACC, DEQ, NT, ROW1>(g, ldg, rows, w0, first, in0, oldA0, oldB0, inv_p,
+                                                      inv0 * 65536.0f, s0 * 65536.0f, kmax, key0, key1, one2, sum,
+                                                      deq_s, out);
+        else
+            quant_sum_tile<MULTI, false, ACC, DEQ, NT, ROW1>(g, ldg, rows, w0, first, in0, oldA0, oldB0, inv_p, inv0, s0,
+                                                       kmax, key0, key1, one2, sum, deq_s, out);
+    }
+    if (stride < ntiles) {
+        for (int64_t T = first + stride; T < ntiles; T += stride) {
+            const int64_t a_off = (T << 9) + 4 * lane;
+            const TileIn in = load_tile<MULTI>(g, idx, a_off);
+            i32x4 oldA = {0, 0, 0, 0}, oldB = {0, 0, 0, 0};
+            if (ACC) {
+                oldA = load_sum4<NT>(sum + a_off);
+                oldB = load_sum4<NT>(sum + a_off + 256);
+            }
+            if (pre)
+                quant_sum_tile<MULTI, true, ACC, DEQ, NT, ROW1>(g, ldg, rows, w0, T, in, oldA, oldB, inv_p, inv0 * 65536.0f,
+                                                          s0 * 65536.0f, kmax, key0, key1, one2, sum, deq_s, out);
+            else
+                quant_sum_tile<MULTI, false, ACC, DEQ, NT, ROW1>(g, ldg, rows, w0, T, in, oldA, oldB, inv_p, inv0, s0,
+                                                           kmax, key0, key1, one2, sum, deq_s, out);
+        }
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 64)
+        quant_sum_tail<MULTI, ACC, DEQ>(g, d, ldg, rows, w0, idx, ntiles, inv_s, inv0, s0, kmax, key0, key1, sum,
+                                        deq_s, out);
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers (called by the ABI layer after validation).
 // ---------------------------------------------------------------------------
 // Tiles per wave for the quantiser.  Launch-shape sweeps on MI355X with cold
@@ -1310,6 +1559,55 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
         if (multi) UQ_LAUNCH_QUANTISE(true, 2); else UQ_LAUNCH_QUANTISE(false, 2);
     }
 #undef UQ_LAUNCH_QUANTISE
+    return hipGetLastError();
+}
+
+hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                            const ScaleSet& S, const uint8_t* idx, uint64_t seed, int32_t accumulate, int32_t* sum,
+                            int32_t M, float* out, hipStream_t stream)
+{
+    if (d == 0)
+        return hipSuccess;
+    const uint32_t key0 = static_cast<uint32_t>(seed);
+    const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
+    // one wave per 512-coordinate tile (at least one block for the tail)
+    const dim3 grid(one_shot(d >> 9, kBlock / 64));
+    // sums beyond 64 MiB are loaded and stored nontemporally, as in the fused sum
+    const bool nt = 4 * d > kSumNontemporalBytes;
+    const bool multi = S.K > 1;
+    const bool acc = accumulate != 0;
+    const bool deq = out != nullptr;
+#define UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, NT)                                                                        \
+    do {                                                                                                           \
+        if (rows == 1)                                                                                             \
+            hipLaunchKernelGGL((k_quant_sum<MULTI, ACC, DEQ, NT, true>), grid, dim3(kBlock), 0, stream, g, d, rows, \
+                               ldg, worker0, w, S, idx, key0, key1, sum, M, out);                                  \
+        else                                                                                                       \
+            hipLaunchKernelGGL((k_quant_sum<MULTI, ACC, DEQ, NT, false>), grid, dim3(kBlock), 0, stream, g, d,      \
+                               rows, ldg, worker0, w, S, idx, key0, key1, sum, M, out);                            \
+    } while (0)
+#define UQ_LAUNCH_QSUM_NT(MULTI, ACC, DEQ)  \
+    do {                                    \
+        if (nt)                             \
+            UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, true);  \
+        else                                \
+            UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, false); \
+    } while (0)
+#define UQ_LAUNCH_QSUM_DEQ(MULTI, ACC)           \
+    do {                                         \
+        if (deq)                                 \
+            UQ_LAUNCH_QSUM_NT(MULTI, ACC, true); \
+        else                                     \
+            UQ_LAUNCH_QSUM_NT(MULTI, ACC, false);\
+    } while (0)
+    if (multi) {
+        if (acc) UQ_LAUNCH_QSUM_DEQ(true, true); else UQ_LAUNCH_QSUM_DEQ(true, false);
+    } else {
+        if (acc) UQ_LAUNCH_QSUM_DEQ(false, true); else UQ_LAUNCH_QSUM_DEQ(false, false);
+    }
+#undef UQ_LAUNCH_QSUM_DEQ
+#undef UQ_LAUNCH_QSUM_NT
+#undef UQ_LAUNCH_QSUM
     return hipGetLastError();
 }
 

@@ -11,8 +11,8 @@ from __future__ import annotations
 import torch
 
 from . import (_stream, uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_packed, uq_quantize_single,
-               uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale, uq_sum_codes,
-               uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
+               uq_quantize_sum, uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale,
+               uq_sum_codes, uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
 
 
 def round_up(x: int, m: int) -> int:
@@ -28,12 +28,18 @@ class Step:
     bits = 4 or 2: the codes are held packed ([M, ldc] bytes, ldc >= d*bits/8).
     fused=True: the last sum call also reconstructs (uq_sum_dequantize);
     False: uq_sum_codes / uq_sum_packed, then uq_dequantize.
+    quant_sum=True: the codes are added into the sum as they are formed
+    (uq_quantize_sum) and never stored: one call per worker when streamed
+    (the last one also reconstructs), one call for all workers otherwise.
+    The default is True for a streamed step with fused=True, else False.
     """
 
     def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None,
-                 bits: int = 8, fused: bool = True):
+                 bits: int = 8, fused: bool = True, quant_sum: bool | None = None):
         self.d, self.M = d, M
         self.fused = fused
+        self.quant_sum = (streamed and fused) if quant_sum is None else quant_sum
+        assert not (self.quant_sum and not fused), "quant_sum reconstructs in the same pass (fused)"
         self.scales = [float(s) for s in scales]
         self.K = len(self.scales)
         self.streamed = streamed
@@ -48,7 +54,8 @@ class Step:
         self.ws_bytes = uq_workspace_bytes(d, M)
         self.ws = torch.zeros(self.ws_bytes // 8, dtype=torch.float64, device=device)
         rows = 1 if streamed else M
-        self.codes = torch.zeros((rows, self.ldc), dtype=torch.int8, device=device)
+        # the fused quantise-and-sum stores no codes
+        self.codes = None if self.quant_sum else torch.zeros((rows, self.ldc), dtype=torch.int8, device=device)
         self.sum = torch.zeros(round_up(max(d, 1), 64), dtype=torch.int32, device=device)
         self.out = torch.zeros(round_up(max(d, 1), 64), dtype=torch.float32, device=device)
 
@@ -78,6 +85,12 @@ class Step:
         else:
             uq_sum_codes(codes, self.d, rows, codes.stride(0), accumulate, self.sum, stream)
 
+    def quantize_sum(self, g, seed: int, rows: int | None = None, worker0: int = 0, accumulate: int = 0,
+                     reconstruct: bool = True, stream=None):
+        rows = self.M if rows is None else rows
+        uq_quantize_sum(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed,
+                        accumulate, self.sum, self.M, self.out if reconstruct else None, stream)
+
     def dequantize(self, stream=None):
         uq_dequantize(self.sum, self.d, self.M, self.w, self.scales, self.K, self.idx, self.out, stream)
 
@@ -94,7 +107,13 @@ class Step:
         assert g.stride(1) == 1 and g.shape[1] >= self.d
         stream = _stream(stream)  # resolved once for the step's calls
         self.shared_scale(g, stream)
-        if self.streamed:
+        if self.quant_sum and self.streamed:
+            for m in range(self.M):
+                self.quantize_sum(g[m:m + 1], seed, rows=1, worker0=m, accumulate=1 if m > 0 else 0,
+                                  reconstruct=m == self.M - 1, stream=stream)
+        elif self.quant_sum:
+            self.quantize_sum(g, seed, stream=stream)
+        elif self.streamed:
             for m in range(self.M):
                 self.quantize(g[m:m + 1], seed, rows=1, worker0=m, stream=stream)
                 acc = 1 if m > 0 else 0

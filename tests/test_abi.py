@@ -194,6 +194,40 @@ def test_sum_dequantize_rejects(kw, want):
     assert status_sumdeq(**kw) == E[want]
 
 
+def status_qsum(g=A, d=100, rows=2, ldg=128, worker0=0, w=A, scales=S4, K=4, idx=A, seed=1, acc=0, sum_=A,
+                M=2, out=A):
+    hs = uq._HostScales(scales)
+    return L.uq_quantize_sum(g, d, rows, ldg, worker0, w, hs.ptr, K, idx, seed, acc, sum_, M, out, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    # the quantiser's checks
+    (dict(g=None), "inval"), (dict(w=None), "inval"), (dict(w=A + 2), "align"), (dict(d=-1), "inval"),
+    (dict(rows=0), "inval"), (dict(rows=65536), "range"), (dict(ldg=96), "inval"), (dict(ldg=102), "align"),
+    (dict(g=A + 8), "align"), (dict(worker0=-1), "range"), (dict(worker0=2 ** 31 - 1, rows=2), "range"),
+    (dict(idx=None), "inval"), (dict(idx=A + 4), "align"), (dict(K=0), "range"), (dict(scales=None), "inval"),
+    (dict(scales=[127.0, 100.0, 200.0, 300.0]), "range"), (dict(K=1, scales=[128.0]), "range"),
+    # the sum's checks
+    (dict(sum_=None), "inval"), (dict(sum_=A + 4), "align"), (dict(acc=2), "inval"), (dict(acc=-1), "inval"),
+    # the reconstruction's checks, only when out is given
+    (dict(M=0), "inval"), (dict(out=A + 4), "align"), (dict(M=20_000_000, K=1, scales=[127.0]), "range"),
+    (dict(M=3, K=2, scales=[7.0, 11184811.0]), "range"),
+])
+def test_quantize_sum_rejects(kw, want):
+    assert status_qsum(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
+def test_quantize_sum_reconstruction_checks_only_with_out():
+    """Without an output the worker count is not read, and one scale does not
+    read the index: such calls pass every check.  d = 0 makes them valid
+    no-ops that launch nothing, so this holds on any host."""
+    for kw in (dict(out=None, M=0), dict(out=None, M=20_000_000, K=1, scales=[127.0]),
+               dict(K=1, scales=[127.0], idx=None), dict(K=1, scales=[127.0], idx=A + 1)):
+        assert status_qsum(d=0, **kw) == uq.UQ_OK, kw
+    assert status_qsum(d=0, M=0) == uq.UQ_EINVAL
+
+
 def test_binding_raises_with_detail():
     with pytest.raises(uq.UQError) as e:
         uq.uq_quantize_single(A, 100, 2, 128, 0, A, 200, 1, A, 128, stream=0)

@@ -13,8 +13,8 @@ sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
 
-def per_coord(M, K, streamed=False, bits=8, d=1 << 20):
-    b = bench.algorithmic_bytes(d, M, K, streamed, bits)
+def per_coord(M, K, streamed=False, bits=8, d=1 << 20, quant_sum=False):
+    b = bench.algorithmic_bytes(d, M, K, streamed, bits, quant_sum)
     assert b["total"] % d == 0
     return b["total"] // d
 
@@ -29,20 +29,47 @@ def test_step_bytes_per_coordinate(M):
     # row maxima the index pass reads
     want = 10 * M + 19 if 2 <= M <= bench.FUSED_MAX_ROWS else 14 * M + 11
     assert per_coord(M, 4) == want
+    # all rows quantised and summed in one fused call: the gradients and the
+    # index in, the sums and the output out
+    assert per_coord(M, 1, quant_sum=True) - 4 * M == 4 * M + 8
+    assert per_coord(M, 4, quant_sum=True) == want - (10 * M + 19 - (8 * M + 18) if 2 <= M <= 16 else
+                                                      14 * M + 11 - (12 * M + 10))
 
 
-def test_streamed_and_packed_bytes():
+def test_streamed_bytes():
     d, M, K = 1 << 20, 16, 8
+    # codes stored, then summed: the quantiser row by row (the index read by
+    # every launch), the sum set for the first row and += after, the last
+    # call with the output and the index for the reconstruction
     b = bench.algorithmic_bytes(d, M, K, True)
-    # quantise row by row (the index read by every launch), accumulate into
-    # the int32 sum (set for the first row, += after)
     assert b["quantize"] == M * (5 * d + d)
-    # (and in the last call the output and the index for the reconstruction)
-    assert b["sum_dequantize"] == (d + 4 * d) + (M - 1) * (d + 8 * d) + 4 * d + d
-    # 4-bit codes: half a byte per code written and read back
+    assert b["sum_first"] + b["sum"] + b["sum_dequantize"] == (d + 4 * d) + (M - 1) * (d + 8 * d) + 4 * d + d
+    # fused: the first worker 4 + 1 in, 4 out; the others also read the old
+    # sums; the last also writes the output
+    f = bench.algorithmic_bytes(d, M, K, True, quant_sum=True)
+    assert f["quant_sum_first"] == 9 * d and f["quant_sum"] == (M - 2) * 13 * d and f["quant_sum_last"] == 17 * d
+    # the whole step: norm + maxima 4M + 4, index 4 + 1, then 9 + 13 (M - 2) + 17
+    assert per_coord(M, K, True, quant_sum=True) == 17 * M + 9
+    assert per_coord(1, K, True, quant_sum=True) == per_coord(1, K, False, quant_sum=True)
+
+
+def test_packed_bytes():
     assert bench.code_bytes(1001, 4) == 501 and bench.code_bytes(1001, 2) == 251
     assert bench.quantize_bytes_per_launch(1000, 3, 1, 4) == 3 * (4000 + 500)
     assert bench.quantize_bytes_per_launch(1000, 3, 2, 8) == 3 * 5000 + 1000
+
+
+def test_stage_plan_names_the_kernels():
+    st = bench.plan_stages(1 << 20, 16, 8, 8, True, True)
+    assert [s["name"] for s in st] == ["shared_scale", "quant_sum_first", "quant_sum", "quant_sum_last"]
+    assert st[0]["kernels"] == ["k_norm_max", "k_rowsum", "k_index_max"]
+    assert [s["calls"] for s in st] == [1, 1, 14, 1]
+    assert bench.plan_stages(100, 8, 1)[1]["kernels"] == ["k_quantise_single"]
+    assert bench.plan_stages(100, 16, 4, 4)[1]["kernels"] == ["k_quantise_multi_4bit"]
+    assert bench.plan_stages(100, 17, 4)[0]["kernels"] == ["k_sumsq", "k_finish", "k_index"]
+    for M in (1, 2, 3):
+        st = bench.plan_stages(100, M, 2, 8, True, True)
+        assert sum(s["calls"] for s in st[1:]) == M
 
 
 def test_stage_reps():
@@ -80,7 +107,60 @@ def test_counter_traffic_follows_the_sources(tmp_path, monkeypatch):
 def test_cpu_baseline_on_a_small_sample():
     torch = pytest.importorskip("torch")
     g = torch.from_numpy(np.random.default_rng(0).standard_normal((2, 5000)).astype(np.float32) * 1e-3)
-    base, ref, dn = bench.cpu_baseline(g, dict(d=5000, M=2, scales=[127.0], seed=3), 0.2)
-    assert dn == 5000 and base["kind"] == "oracle" and base["cores"] == 1 and base["value"] > 0
+    base, ref, dn = bench.cpu_baseline(g, dict(d=5000, M=2, scales=[127.0], seed=3), 0.2, threads=3)
+    assert dn == 5000 and base["kind"] == "oracle" and base["cores"] == 3 and base["value"] > 0
+    assert base["one_core"]["cores"] == 1 and base["one_core"]["value"] > 0
     assert base["sample"].startswith("full workload")
     assert ref["codes"].shape == (2, 5000)
+
+
+class FakeStep:
+    """The buffers bench.py reads back from a step, as host tensors."""
+
+    def __init__(self, torch, ref, M, d, bits, streamed=False):
+        from oracle import oracle
+
+        self.w = torch.tensor([float(ref["W"])], dtype=torch.float32)
+        self.idx = None if ref["idx"] is None else torch.from_numpy(ref["idx"].copy())
+        self.sum = torch.from_numpy(ref["sum"].copy())
+        self.out = torch.from_numpy(ref["out"].copy())
+        self.streamed = streamed
+        if streamed:
+            self.codes = None
+        elif bits == 8:
+            self.codes = torch.from_numpy(ref["codes"].copy())
+        else:
+            ld = ((d * bits + 7) // 8 + 255) // 256 * 256
+            packed = np.zeros((M, ld), dtype=np.uint8)
+            for m in range(M):
+                p = oracle.pack_codes(ref["codes"][m], bits)
+                packed[m, :p.size] = p
+            self.codes = torch.from_numpy(packed)
+
+
+@pytest.mark.parametrize("bits,scales", [(8, [127.0]), (8, [127.0, 2032.0]), (4, [7.0]), (4, [7.0, 112.0]),
+                                         (2, [1.0])])
+@pytest.mark.parametrize("streamed", [False, True])
+def test_parity_on_sample_reads_every_code_width(bits, scales, streamed):
+    """The bench's parity check unpacks packed codes before comparing them
+    with the oracle's int8 codes; a changed code, sum or output is caught."""
+    torch = pytest.importorskip("torch")
+    from oracle import oracle
+
+    M, d = 3, 1001
+    g = np.random.default_rng(bits).standard_normal((M, d)).astype(np.float32) * 1e-3
+    ref = oracle.pipeline(g, scales, 9, d=d)
+    st = FakeStep(torch, ref, M, d, bits, streamed)
+    assert bench.parity_on_sample(st, ref, d, d, bits) == "bit-exact"
+    st.sum[5] += 1
+    assert bench.parity_on_sample(st, ref, d, d, bits) == "MISMATCH"
+    st = FakeStep(torch, ref, M, d, bits, streamed)
+    st.out[7] = -st.out[7] + 1.0
+    assert bench.parity_on_sample(st, ref, d, d, bits) == "MISMATCH"
+    if not streamed:
+        st = FakeStep(torch, ref, M, d, bits, streamed)
+        if bits == 8:
+            st.codes[1, 3] += 1
+        else:
+            st.codes[1, 0] ^= 1
+        assert bench.parity_on_sample(st, ref, d, d, bits) == "MISMATCH"

@@ -1,8 +1,10 @@
 """bench.py end to end on the GPU at the small workload (d = 2^20, 4 workers,
-one scale s = 127): one JSON line carrying the throughput, the dominant
-kernel's roofline and the oracle's rate on the same input, with the device's
-step bit-exact against that oracle run; host launches and HIP-graph replays.
-Also the GlobalRandK line at the ResNet-18 shape."""
+one scale s = 127): one JSON line carrying the throughput, the roofline of
+the stage with the largest share of the step and the oracle's rate on one and
+on several cores over the same input, with the device's step bit-exact
+against that oracle run; host launches and HIP-graph replays.  Also the
+default line (2^30 coordinates, 16 streamed workers, eight scales) in a
+short run, and the GlobalRandK line at the ResNet-18 shape."""
 import json
 import os
 import subprocess
@@ -16,10 +18,12 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 D, M = 1 << 20, 4
 
 
-def run_bench(*extra, workload="small-gaussian"):
-    cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", workload, "--steps", "20",
-           "--warmup", "5", "--cpu-budget", "1", *extra]
-    r = subprocess.run(cmd, capture_output=True, text=True, timeout=240, cwd=ROOT)
+def run_bench(*extra, workload="small-gaussian", steps=20, warmup=5):
+    cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--steps", str(steps), "--warmup", str(warmup),
+           "--cpu-budget", "1", *extra]
+    if workload:
+        cmd += ["--workload", workload]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=300, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
     assert len(lines) == 1, r.stdout
@@ -40,16 +44,41 @@ def test_bench_line(extra):
     # M·d worker-coordinates per step, in G elements/s
     assert j["value"] == pytest.approx(M * D / (j["ms_per_step"] * 1e-3) / 1e9, rel=0.02)
 
+    check_roofline(j)
+    base = j["cpu_baseline"]
+    assert base["kind"] == "oracle" and base["cores"] >= 1 and base["value"] > 0 and base["sample"]
+    assert base["one_core"]["cores"] == 1 and base["one_core"]["value"] > 0
+    assert j["parity_vs_oracle"] == "bit-exact"
+
+
+def check_roofline(j, share_lo=0.4, share_hi=1.3):
     roof = j["roofline"]
     assert (roof["bound"], roof["peak"], roof["unit"]) == ("hbm", 8000.0, "GB/s")
-    # one quantiser launch over all rows: 4 bytes read and 1 written per coordinate
-    assert roof["algorithmic_bytes_per_launch"] == M * D * 5
+    share = j["stage_share"]
+    # the roofline is the stage with the largest share of the step
+    assert roof["stage"] == max(share, key=share.get)
     assert roof["achieved"] == pytest.approx(roof["algorithmic_bytes_per_launch"] / (roof["avg_launch_us"] * 1e3),
                                              rel=0.01)
     assert roof["frac"] == pytest.approx(roof["achieved"] / roof["peak"], rel=1e-3)
+    # stage_ms carries four decimals of a millisecond
+    assert roof["avg_launch_us"] == pytest.approx(j["stage_ms"][roof["stage"]] * 1e3, abs=0.06)
+    # the stages run back to back take about the step's time (less where the
+    # step is bound by host launches)
+    assert share_lo < sum(share.values()) < share_hi
 
-    base = j["cpu_baseline"]
-    assert base["kind"] == "oracle" and base["cores"] >= 1 and base["value"] > 0 and base["sample"]
+
+def test_default_bench_line():
+    """`python bench.py` with no workload: 2^30 coordinates, 16 workers
+    streamed through the fused quantise-and-sum, eight scales."""
+    j = run_bench(workload=None, steps=3, warmup=1)
+    cfg = j["config"]
+    assert (cfg["workload"], cfg["d"], cfg["M"], len(cfg["scales"]), cfg["streamed"]) == \
+        ("student-t", 1 << 30, 16, 8, True)
+    assert cfg["path"] == "quantise-and-sum fused"
+    assert j["step_bytes"] == (17 * 16 + 9) * (1 << 30)
+    check_roofline(j, 0.85, 1.15)
+    assert j["roofline"]["stage"] == "quant_sum" and j["roofline"]["launches_per_step"] == 14
+    assert j["cpu_baseline"]["one_core"]["value"] > 0
     assert j["parity_vs_oracle"] == "bit-exact"
 
 

@@ -33,16 +33,16 @@ def ulps(a, b) -> int:
     return abs(int(np.float32(a).view(np.int32)) - int(np.float32(b).view(np.int32)))
 
 
-def gpu_step(host_g, d, scales, seed, streamed=False):
+def gpu_step(host_g, d, scales, seed, streamed=False, quant_sum=None):
     g = torch.from_numpy(np.ascontiguousarray(host_g)).to(DEV)
     M = host_g.shape[0]
-    step = Step(d, M, scales, device=DEV, streamed=streamed)
+    step = Step(d, M, scales, device=DEV, streamed=streamed, quant_sum=quant_sum)
     step.run(g, seed)
     torch.cuda.synchronize()
     res = dict(W=np.float32(step.w[0].item()), sum=step.sum[:d].cpu().numpy(),
                out=step.out[:d].cpu().numpy(),
                idx=None if step.idx is None else step.idx[:d].cpu().numpy())
-    if not streamed:
+    if step.codes is not None and not streamed:
         res["codes"] = step.codes[:, :d].cpu().numpy()
     return res, step, g
 
@@ -163,9 +163,11 @@ def test_capped_grids(cap, M):
         for scales in (S_SINGLE, S_MULTI4):
             res, _, _ = gpu_step(host, d, scales, seed=cap + M)
             assert_matches_oracle(res, host, d, scales, seed=cap + M)
-            # one row at a time into the running sum, the last call with the reconstruction
-            res, _, _ = gpu_step(host, d, scales, seed=cap + M, streamed=True)
-            assert_matches_oracle(res, host, d, scales, seed=cap + M)
+            # one row at a time into the running sum, the last call with the
+            # reconstruction: fused quantise-and-sum, and codes stored then summed
+            for qs in (True, False):
+                res, _, _ = gpu_step(host, d, scales, seed=cap + M, streamed=True, quant_sum=qs)
+                assert_matches_oracle(res, host, d, scales, seed=cap + M)
     finally:
         uq.uq_set_grid_cap(0)
 
@@ -241,9 +243,10 @@ def test_accumulate_equals_set():
     d, M = 40_000, 5
     host = synth.gaussian_rows(M, d, seed=8, ldg=40_000)
     res, step, g = gpu_step(host, d, S_MULTI4, seed=4)
-    res_s, _, _ = gpu_step(host, d, S_MULTI4, seed=4, streamed=True)
-    assert np.array_equal(res["sum"], res_s["sum"])
-    assert np.array_equal(res["out"].view(np.int32), res_s["out"].view(np.int32))
+    for qs in (True, False):
+        res_s, _, _ = gpu_step(host, d, S_MULTI4, seed=4, streamed=True, quant_sum=qs)
+        assert np.array_equal(res["sum"], res_s["sum"])
+        assert np.array_equal(res["out"].view(np.int32), res_s["out"].view(np.int32))
 
 
 def test_repeatable():

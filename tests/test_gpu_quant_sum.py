@@ -1,0 +1,160 @@
+"""GPU parity of the fused quantise-and-sum (uq_quantize_sum) through the C ABI.
+
+Its sums and reconstruction must equal, bit for bit, the oracle's integer sum
+of the workers' codes (Eq. (8)/(12) and the all-reduce of Algorithm 1/2) and
+its reconstruction (Eq. (9)/(13)), and the composed calls uq_quantize_* ->
+uq_sum_codes -> uq_dequantize: one row per call into a running sum (a worker
+streamed through a resident accumulator), all rows in one call, accumulating
+onto sums already stored, on capped grids and past the 16-bit lane sums'
+flush at 256 rows.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import synth  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+import paper_2109_12497_amd as uq  # noqa: E402
+from paper_2109_12497_amd.step import Step  # noqa: E402
+
+DEV = torch.device("cuda:0")
+SCALE_SETS = {"s127": [127.0], "s7": [7.0], "s1": [1.0], "K4": synth.scales_for(8, 4), "K2": [7.0, 112.0],
+              "K8": synth.scales_for(8, 8)}
+
+
+def ulps(a, b) -> int:
+    return abs(int(np.float32(a).view(np.int32)) - int(np.float32(b).view(np.int32)))
+
+
+def run_step(host, d, scales, seed, **kw):
+    g = torch.from_numpy(np.ascontiguousarray(host)).to(DEV)
+    st = Step(d, host.shape[0], scales, device=DEV, **kw)
+    st.run(g, seed)
+    torch.cuda.synchronize()
+    return st, g
+
+
+def check_oracle(st, host, d, scales, seed):
+    W = np.float32(st.w[0].item())
+    ref = O.pipeline(host, scales, seed, d=d, W=W)
+    assert ulps(W, ref["W_oracle"]) <= 1
+    if len(scales) > 1:
+        assert np.array_equal(st.idx[:d].cpu().numpy(), ref["idx"]), "scale index differs"
+    got = st.sum[:d].cpu().numpy()
+    bad = np.flatnonzero(got != ref["sum"])
+    assert bad.size == 0, f"sums differ at {bad[:8].tolist()}"
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32)), "outputs differ"
+
+
+@pytest.mark.parametrize("d", [1, 5, 8, 9, 511, 512, 513, 1000, 4097, 10_007, 65_539, 200_003])
+@pytest.mark.parametrize("name", list(SCALE_SETS))
+@pytest.mark.parametrize("streamed", [True, False], ids=["per-worker", "all-rows"])
+def test_quant_sum_matches_oracle(d, name, streamed):
+    scales = SCALE_SETS[name]
+    M = 5
+    host = synth.mixed_rows(M, d, seed=d + 3, ldg=synth.round_up(d, 64))
+    st, _ = run_step(host, d, scales, seed=900 + d, streamed=streamed, quant_sum=True)
+    assert st.codes is None  # no code row is kept
+    check_oracle(st, host, d, scales, seed=900 + d)
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 16, 17])
+@pytest.mark.parametrize("name", ["s127", "K4"])
+def test_quant_sum_equals_composed_calls(M, name):
+    """Per-worker calls, one call for all rows, and the composed quantise /
+    sum / reconstruction calls give the same sums and outputs."""
+    scales = SCALE_SETS[name]
+    d = 123_457
+    host = synth.mixed_rows(M, d, seed=M, ldg=synth.round_up(d, 64))
+    a, _ = run_step(host, d, scales, seed=11, streamed=True, quant_sum=True)
+    b, _ = run_step(host, d, scales, seed=11, streamed=False, quant_sum=True)
+    c, _ = run_step(host, d, scales, seed=11, streamed=True, quant_sum=False)
+    e, _ = run_step(host, d, scales, seed=11, streamed=False, fused=False)
+    for st in (b, c, e):
+        assert torch.equal(a.sum[:d], st.sum[:d])
+        assert torch.equal(a.out[:d].view(torch.int32), st.out[:d].view(torch.int32))
+
+
+def test_accumulates_onto_stored_sums():
+    """accumulate = 1 adds to whatever the sums hold; without an output the
+    reconstruction is not written."""
+    d, M = 70_001, 3
+    scales = SCALE_SETS["K4"]
+    host = synth.gaussian_rows(M, d, seed=5, ldg=synth.round_up(d, 64))
+    st, g = run_step(host, d, scales, seed=6, streamed=False, fused=False)
+    W = np.float32(st.w[0].item())
+    ref = O.pipeline(host, scales, 6, d=d, W=W)
+    base = np.random.default_rng(1).integers(-10 ** 6, 10 ** 6, size=d).astype(np.int32)
+    st.sum[:d].copy_(torch.from_numpy(base))
+    st.out.fill_(-7.0)
+    uq.uq_quantize_sum(g, d, M, g.stride(0), 0, st.w, scales, len(scales), st.idx, 6, 1, st.sum, M, None)
+    torch.cuda.synchronize()
+    assert np.array_equal(st.sum[:d].cpu().numpy(), base + ref["sum"])
+    assert bool((st.out[:d] == -7.0).all())
+    # the last worker alone, onto the first M - 1 workers' sum, with the reconstruction
+    first = O.sum_codes(ref["codes"][:M - 1])
+    st.sum[:d].copy_(torch.from_numpy(first))
+    uq.uq_quantize_sum(g[M - 1:], d, 1, g.stride(0), M - 1, st.w, scales, len(scales), st.idx, 6, 1, st.sum, M,
+                       st.out)
+    torch.cuda.synchronize()
+    assert np.array_equal(st.sum[:d].cpu().numpy(), ref["sum"])
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32))
+
+
+@pytest.mark.parametrize("cap", [8, 24])
+@pytest.mark.parametrize("streamed", [True, False], ids=["per-worker", "all-rows"])
+def test_quant_sum_capped_grids(cap, streamed):
+    """Waves striding over several tiles (the grid capped far below one tile
+    per wave); the results must not depend on the grid."""
+    d, M = 100_003, 4
+    host = synth.mixed_rows(M, d, seed=cap, ldg=synth.round_up(d, 64))
+    uq.uq_set_grid_cap(cap)
+    try:
+        for scales in (SCALE_SETS["s127"], SCALE_SETS["K4"]):
+            st, _ = run_step(host, d, scales, seed=cap, streamed=streamed, quant_sum=True)
+            check_oracle(st, host, d, scales, seed=cap)
+    finally:
+        uq.uq_set_grid_cap(0)
+
+
+@pytest.mark.parametrize("M", [256, 257, 300])
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_more_rows_than_the_16_bit_lane_sums_hold(M, sign):
+    """All rows in one call: the codes are summed in 16-bit lanes for up to
+    256 rows, then widened.  Every row is one-hot at coordinate 0 (plus
+    values too small to move its norm off 1), so that coordinate takes code
+    +-127 in every row and its sum passes +-2^15 from 258 rows on."""
+    d = 3_001
+    scales = [127.0]
+    host = np.zeros((M, synth.round_up(d, 64)), dtype=np.float32)
+    host[:, 0] = sign
+    host[:, 100:200] = synth.gaussian_rows(M, 100, seed=M, sigma=1e-6)
+    st, _ = run_step(host, d, scales, seed=3, streamed=False, quant_sum=True)
+    assert st.w[0].item() == 1.0
+    assert int(st.sum[0].item()) == int(sign) * 127 * M
+    check_oracle(st, host, d, scales, seed=3)
+
+
+@pytest.mark.parametrize("W", [0.0, -1.0, float("inf"), float("nan"), 1e-45])
+def test_forced_scale_values(W):
+    """A W that is zero, negative, non-finite or so small that s_0 / W
+    overflows selects the zero path: every sum and output 0."""
+    d, M = 5_000, 3
+    scales = SCALE_SETS["K4"]
+    host = synth.gaussian_rows(M, d, seed=2, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(host).to(DEV)
+    st = Step(d, M, scales, device=DEV, streamed=True)
+    st.shared_scale(g)
+    st.w.fill_(W)
+    st.sum.fill_(5)
+    for m in range(M):
+        st.quantize_sum(g[m:m + 1], 1, rows=1, worker0=m, accumulate=1 if m else 0, reconstruct=m == M - 1)
+    torch.cuda.synchronize()
+    assert int(st.sum[:d].abs().max()) == 0
+    assert int(st.out[:d].view(torch.int32).abs().max()) == 0
