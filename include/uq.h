@@ -95,6 +95,30 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg,
                     const float* scales, int32_t K, float* w, uint8_t* idx,
                     void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * uq_shared_scale for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same checks, kernels and results, bit for bit, with the scratch taken
+ * from a static device buffer of UQ_NOALLOC_SCRATCH_BYTES bytes that the
+ * library holds on each device it runs on until the process ends.  The call
+ * itself allocates nothing; its first call on a device looks up that
+ * device's buffer (the current device, which the stream must belong to).
+ *   Limit: the scratch the kernels need must fit the buffer.  With one
+ *   scale, or more than 16 rows, or one row, that is 8 * M * ceil(d / c)
+ *   bytes with c >= 8192 chunks of at most 1024 per row: any d for
+ *   M <= 8192.  With several scales and 2 to 16 rows the row maxima take
+ *   4 * d bytes more: d up to about 16.7 million.  A call beyond the limit
+ *   returns UQ_EWORKSPACE and launches nothing.
+ *   Every call on one device shares that device's buffer (nothing in it
+ *   needs to start at zero): calls that overlap on one device, on different
+ *   streams or threads, race and give undefined results.
+ * Arguments as for uq_shared_scale, without ws and ws_bytes.
+ */
+#define UQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int uq_shared_scale_noalloc(const float* g, int64_t d, int32_t M, int64_t ldg,
+                            const float* scales, int32_t K, float* w, uint8_t* idx,
+                            void* stream);
+
 /* Workspace bytes uq_shared_scale needs for (d, M) and any K; 0 never
  * returned.  With 2 <= M <= 16 this includes 4 * d bytes: with several scales the
  * norm pass also keeps the largest |g| over the rows at every coordinate, so

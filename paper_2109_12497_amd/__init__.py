@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(HERE, "libuq.so")
 
 UQ_OK, UQ_EINVAL, UQ_ERANGE, UQ_EALIGN, UQ_EWORKSPACE, UQ_EHIP = 0, -1, -2, -3, -4, -5
 UQ_MAX_SCALES = 16
+UQ_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class UQError(RuntimeError):
@@ -51,6 +52,7 @@ def _load() -> ctypes.CDLL:
         raise ImportError(f"two HIP runtimes are mapped in this process: {sorted(runtimes)}")
     P, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
     L.uq_shared_scale.argtypes = [P, i64, i32, i64, P, i32, P, P, P, sz, P]
+    L.uq_shared_scale_noalloc.argtypes = [P, i64, i32, i64, P, i32, P, P, P]
     L.uq_workspace_bytes.argtypes = [i64, i32]
     L.uq_workspace_bytes.restype = sz
     L.uq_quantize_single.argtypes = [P, i64, i32, i64, i32, P, i32, u64, P, i64, P]
@@ -72,7 +74,7 @@ def _load() -> ctypes.CDLL:
     L.uq_strerror.restype = ctypes.c_char_p
     L.uq_last_error.argtypes = []
     L.uq_last_error.restype = ctypes.c_char_p
-    for name in ("uq_shared_scale", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
+    for name in ("uq_shared_scale", "uq_shared_scale_noalloc", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
                  "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_quantize_sum",
                  "uq_randk_select", "uq_gather",
                  "uq_scatter", "uq_set_grid_cap", "uq_set_randk_mode"):
@@ -154,6 +156,11 @@ def uq_shared_scale(g, d, M, ldg, scales, K, w, idx, ws, ws_bytes, stream=None) 
     hs = _host_scales(scales)
     _check(lib.uq_shared_scale(_ptr(g), d, M, ldg, hs.ptr, K, _ptr(w), _ptr(idx), _ptr(ws), ws_bytes,
                                _stream(stream)))
+
+
+def uq_shared_scale_noalloc(g, d, M, ldg, scales, K, w, idx, stream=None) -> None:
+    hs = _host_scales(scales)
+    _check(lib.uq_shared_scale_noalloc(_ptr(g), d, M, ldg, hs.ptr, K, _ptr(w), _ptr(idx), _stream(stream)))
 
 
 def uq_quantize_single(g, d, rows, ldg, worker0, w, s, seed, codes, ldc, stream=None) -> None:

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "uq.h"
 #include "uq_launch.hpp"
@@ -207,6 +208,56 @@ int64_t grid_cap()
 
 }  // namespace uq
 
+namespace {
+
+// Scratch of uq_shared_scale_noalloc: the norm's partial sums (and, with
+// several scales and 2 to 16 rows, the rows' maxima) live in this array
+// instead of a caller's workspace.  Each device holds its own copy, at its
+// own address, until the process ends.  In host code `scratch` names a
+// host-side stand-in, never the device memory: kernels get the address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[UQ_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch` (looked up on the first call on
+// that device); nullptr with *err set when the runtime refuses.
+void* device_scratch(hipError_t* err)
+{
+    int dev = -1;
+    *err = hipGetDevice(&dev);
+    if (*err != hipSuccess)
+        return nullptr;
+    if (dev < 0 || dev >= kMaxDevices) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (*err != hipSuccess)
+            return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+// Scratch bytes uq_shared_scale's kernels use for (d, M, K): the norm's
+// partials, or the fused pass's layout.
+size_t scratch_bytes_for(int64_t d, int32_t M, int32_t K)
+{
+    if (uq::use_fused(d, M, K))
+        return uq::fused_layout(d, M).bytes;
+    const uq::NormPlan p = uq::norm_plan(d);
+    const int64_t chunks = p.nchunks < 1 ? 1 : p.nchunks;
+    return uq::align256(static_cast<size_t>(M) * static_cast<size_t>(chunks) * sizeof(double));
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t uq_workspace_bytes(int64_t d, int32_t M)
@@ -246,6 +297,32 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const flo
     if (ws_bytes < uq_workspace_bytes(d, M))
         return fail(UQ_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", ws_bytes,
                     uq_workspace_bytes(d, M));
+    return launched(uq::launch_shared_scale(g, d, M, ldg, S, w, idx, ws, static_cast<hipStream_t>(stream)));
+}
+
+int uq_shared_scale_noalloc(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
+                            float* w, uint8_t* idx, void* stream)
+{
+    UQ_TRY(check_dims(d, M, "M"));
+    UQ_TRY(check_rows(g, d, M, ldg, 4, "g"));
+    UQ_TRY(check_w(w));
+    uq::ScaleSet S;
+    if (K == 1 && scales == nullptr) {
+        S = one_scale(1.0f);
+    } else {
+        UQ_TRY(check_scales(scales, K, &S));
+    }
+    if (K > 1)
+        UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    const size_t need = scratch_bytes_for(d, M, K);
+    if (need > UQ_NOALLOC_SCRATCH_BYTES)
+        return fail(UQ_EWORKSPACE, "d = %lld, M = %d, K = %d needs %zu bytes of scratch, more than the %zu of the "
+                    "static buffer (use uq_shared_scale with a workspace)", (long long)d, M, K, need,
+                    (size_t)UQ_NOALLOC_SCRATCH_BYTES);
+    hipError_t e = hipSuccess;
+    void* ws = device_scratch(&e);
+    if (ws == nullptr)
+        return fail(UQ_EHIP, "static scratch of the current device: %s", hipGetErrorString(e));
     return launched(uq::launch_shared_scale(g, d, M, ldg, S, w, idx, ws, static_cast<hipStream_t>(stream)));
 }
 

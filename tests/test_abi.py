@@ -120,6 +120,37 @@ def test_shared_scale_rejects(kw, want):
     assert uq.uq_last_error() != ""
 
 
+def status_noalloc(g=A, d=100, M=2, ldg=128, scales=S127, K=1, w=A, idx=A):
+    hs = uq._HostScales(scales)
+    return L.uq_shared_scale_noalloc(g, d, M, ldg, hs.ptr, K, w, idx, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(g=None), "inval"), (dict(d=-1), "inval"), (dict(M=0), "inval"), (dict(M=70000), "range"),
+    (dict(ldg=64), "inval"), (dict(ldg=130), "align"), (dict(g=A + 4), "align"), (dict(w=None), "inval"),
+    (dict(w=A + 2), "align"), (dict(K=0), "range"), (dict(K=2, scales=[3.0, 3.0]), "range"),
+    (dict(K=2, scales=S4[:2], idx=None), "inval"), (dict(K=2, scales=S4[:2], idx=A + 1), "align"),
+    (dict(K=2, scales=None), "inval"),
+    # beyond the static scratch: the row maxima of 20 million coordinates
+    # (several scales, 8 rows), or 8 KiB of norm partials for each of 9000 rows
+    (dict(d=20_000_000, ldg=20_000_000, M=8, K=4, scales=S4), "ws"),
+    (dict(d=1 << 30, ldg=1 << 30, M=9000), "ws"),
+])
+def test_shared_scale_noalloc_rejects(kw, want):
+    assert status_noalloc(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
+def test_shared_scale_noalloc_limit_is_the_header_s():
+    import re
+
+    m = re.search(r"#define UQ_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == uq.UQ_NOALLOC_SCRATCH_BYTES == 64 << 20
+    # the same sizes with a workspace argument are accepted by the checks
+    need = uq.uq_workspace_bytes(20_000_000, 8)
+    assert need > uq.UQ_NOALLOC_SCRATCH_BYTES
+
+
 @pytest.mark.parametrize("M", [1, 2, 8, 16, 17])
 def test_shared_scale_needs_the_full_workspace(M):
     """The workspace of uq_workspace_bytes(d, M) covers any K; one 256-byte
