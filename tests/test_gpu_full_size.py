@@ -1,0 +1,127 @@
+"""GPU parity at full size, every coordinate, against the oracle.
+
+The VGG-16-shaped workload (d = 138,357,544, 16 workers; one scale s = 7, and
+four scales 7 * 16^k) and the 2^30-coordinate workload (16 workers streamed
+through the fused quantise-and-sum, eight scales) in the launch configuration
+the benchmark times.  Each is compared with the oracle (Eq. (7)-(13),
+Algorithms 1-2) over all of d, in coordinate chunks of 2^24 (every worker's
+chunk copied to the host, the oracle on the host's threads, given the
+device's W): the scale index, every worker's codes where the step keeps them,
+the sums and the reconstruction, bit for bit.  The 4-bit packed runs of the
+VGG-16 workload are compared in full with the int8 run's codes, sums and
+outputs.  W is checked within one binary32 ulp of a float64 norm.
+"""
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import synth  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+from paper_2109_12497_amd.step import Step  # noqa: E402
+
+DEV = torch.device("cuda:0")
+CHUNK = 1 << 24
+
+
+def ulps(a, b) -> int:
+    return abs(int(np.float32(a).view(np.int32)) - int(np.float32(b).view(np.int32)))
+
+
+def check_norm(g, d, W):
+    """W within one ulp of RN32(sqrt(max_m sum g^2)), the sums in float64 on the device."""
+    best = 0.0
+    for m in range(g.shape[0]):
+        s = 0.0
+        for c in range(0, d, 1 << 26):
+            x = g[m, c:min(d, c + (1 << 26))].double()
+            s += float(torch.dot(x, x))
+        best = max(best, s)
+    assert ulps(W, np.float32(math.sqrt(best))) <= 1
+
+
+def compare_in_chunks(step, g, d, scales, seed, with_codes):
+    W = np.float32(step.w[0].item())
+    threads = O.default_threads()
+    for c0 in range(0, d, CHUNK):
+        c1 = min(d, c0 + CHUNK)
+        host = g[:, c0:c1].cpu().numpy()
+        ref = O.window(host, W, scales, seed, i0=c0, threads=threads)
+        if ref["idx"] is not None:
+            got = step.idx[c0:c1].cpu().numpy()
+            bad = np.flatnonzero(got != ref["idx"])
+            assert bad.size == 0, f"scale index differs at {(c0 + bad[:5]).tolist()}"
+        if with_codes:
+            got = step.codes[:, c0:c1].cpu().numpy()
+            bad = np.argwhere(got != ref["codes"])
+            assert bad.size == 0, f"codes differ at (worker, coordinate) {[(int(m), c0 + int(i)) for m, i in bad[:5]]}"
+        got = step.sum[c0:c1].cpu().numpy()
+        bad = np.flatnonzero(got != ref["sum"])
+        assert bad.size == 0, f"sums differ at {(c0 + bad[:5]).tolist()}"
+        got = step.out[c0:c1].cpu().numpy().view(np.int32)
+        bad = np.flatnonzero(got != ref["out"].view(np.int32))
+        assert bad.size == 0, f"outputs differ at {(c0 + bad[:5]).tolist()}"
+
+
+@pytest.mark.parametrize("name", ["vgg16-single", "vgg16-multi"])
+def test_vgg16_every_coordinate(name):
+    g, cfg = synth.make_gradients(name, device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    step = Step(d, M, scales, device=DEV)
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    check_norm(g, d, np.float32(step.w[0].item()))
+    compare_in_chunks(step, g, d, scales, seed, with_codes=True)
+
+
+def unpack_rows(packed, d, bits):
+    """[rows, >= d*bits/8] packed bytes -> [rows, d] int8 codes (two's
+    complement fields, low bits first), on the device."""
+    per = 8 // bits
+    x = packed[:, :(d + per - 1) // per].to(torch.int16)
+    fields = torch.stack([(x >> (bits * j)) & ((1 << bits) - 1) for j in range(per)], dim=2)
+    fields = torch.where(fields >= (1 << (bits - 1)), fields - (1 << bits), fields)
+    return fields.reshape(x.shape[0], -1)[:, :d].to(torch.int8)
+
+
+@pytest.mark.parametrize("name", ["vgg16-single", "vgg16-multi"])
+def test_vgg16_4bit_every_coordinate_equals_int8(name):
+    """The 4-bit workloads hold the same codes as the int8 run, unpacked, at
+    every coordinate of every worker; their sums and outputs are the same."""
+    g, cfg = synth.make_gradients(name, device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    a = Step(d, M, scales, device=DEV)
+    a.run(g, seed)
+    b = Step(d, M, scales, device=DEV, bits=4)
+    b.run(g, seed)
+    torch.cuda.synchronize()
+    assert torch.equal(a.w, b.w)
+    if a.idx is not None:
+        assert torch.equal(a.idx[:d], b.idx[:d])
+    for m in range(M):
+        assert torch.equal(unpack_rows(b.codes[m:m + 1], d, 4), a.codes[m:m + 1, :d]), f"worker {m}"
+    assert torch.equal(a.sum[:d], b.sum[:d])
+    assert torch.equal(a.out[:d].view(torch.int32), b.out[:d].view(torch.int32))
+
+
+def test_student_t_every_coordinate():
+    """2^30 coordinates, 16 workers streamed through the fused
+    quantise-and-sum (no code rows), eight scales: the index, the sums and
+    the reconstruction at every coordinate."""
+    g, cfg = synth.make_gradients("student-t", device=DEV)
+    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
+    step = Step(d, M, scales, device=DEV, streamed=True)
+    assert step.quant_sum
+    step.run(g, seed)
+    torch.cuda.synchronize()
+    check_norm(g, d, np.float32(step.w[0].item()))
+    compare_in_chunks(step, g, d, scales, seed, with_codes=False)
+    del g, step
+    torch.cuda.empty_cache()

@@ -471,25 +471,14 @@ def test_workload_full_parity(name):
     assert_matches_oracle(res, host, d, scales, seed)
 
 
-@pytest.mark.parametrize("name", ["vgg16-single", "vgg16-multi"])
-def test_workload_sampled_parity(name):
-    g, cfg = synth.make_gradients(name, device=DEV)
-    d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
-    step = Step(d, M, scales, device=DEV)
-    step.run(g, seed)
-    torch.cuda.synchronize()
-    device_norm_check(g, d, np.float32(step.w[0].item()))
-    check_windows(step, g, d, scales, seed, sample_windows(d, seed=d), streamed=False)
-    # properties over every coordinate: sum = integer sum of the rows' codes
-    assert torch.equal(step.codes[:, :d].to(torch.int32).sum(dim=0), step.sum[:d])
-    assert int(step.codes[:, :d].abs().max()) <= scales[0]
-
-
-def test_student_t_streamed_sampled_parity():
-    cfg = synth.WORKLOADS["student-t"]
+def test_student_t_streamed_composed_sampled_parity():
+    """The 2^30-coordinate workload with each streamed worker's codes stored
+    and then summed (two calls per worker; the fused quantise-and-sum the
+    benchmark times is compared at every coordinate elsewhere): windows
+    against the oracle."""
     g, cfg = synth.make_gradients("student-t", device=DEV)
     d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
-    step = Step(d, M, scales, device=DEV, streamed=True)
+    step = Step(d, M, scales, device=DEV, streamed=True, quant_sum=False)
     step.run(g, seed)
     torch.cuda.synchronize()
     device_norm_check(g, d, np.float32(step.w[0].item()))
