@@ -230,19 +230,7 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 //   k_rowsum     block m: S_m = fixed-order sum of row m's chunk partials
 //   k_index_max  W from the S_m (the rule of k_finish; block 0 stores it),
 //                then the index of every coordinate from amax
-// Measured on MI355X, the amax stores cost far more than their bytes when
-// mixed into the sixteen concurrent row streams (the pass runs 25-30% slower
-// than without them); a variant that walked the rows one at a time and
-// stored each window's maxima once was slower still.
 // ---------------------------------------------------------------------------
-// Block c covers chunk c of every row in tiles of 1024 coordinates (256
-// quads).  Wave w owns rows w, w + 4, ... (ROWS / 4 of them; rows past M
-// re-read row M - 1, a cache hit, and are not accumulated): lane l loads quads
-// l, l + 64, l + 128, l + 192 of the tile from each of its rows, so each row
-// is read 4 KiB at a time per wave, and keeps one fp64 accumulator per row.
-// The waves' maxima meet in LDS and leave as one coalesced amax store, issued
-// after the next tile's loads: one counter tracks a wave's loads and stores in
-// issue order, so a store issued first would hold up the wait for the loads.
 // Barrier for LDS traffic only: the block's LDS writes are complete and
 // visible, while its global loads and stores stay in flight (__syncthreads
 // would also wait for those).
@@ -251,146 +239,173 @@ __device__ __forceinline__ void sync_lds()
     __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Loads of one tile; quads past q_end re-read quad q_end - 1 (so that the
-// loads carry no branch) and are zeroed by the caller.
+// Tile t = the whole quads [256 t, 256 t + 256) (coordinates 1024 t ..) of
+// every row; one block per tile, and one more block for the d % 4 trailing
+// coordinates, which have a partial of their own (on a grid capped below
+// that, blocks stride over the tiles, each tile still with its own partials,
+// so the reduction tree does not depend on the grid).  Wave w owns rows
+// w, w + 4, ... (ROWS / 4 of them; rows past M re-read row M - 1 and are not
+// accumulated): lane l loads quads l, l + 64, l + 128, l + 192 of the tile from
+// each of its rows (4 KiB per row per wave), all loads issued at once.  The
+// waves' maxima meet in LDS and leave as one coalesced store; each row's
+// squares leave as one fp64 partial per tile.  Measured at 2^30 coordinates
+// and 16 rows (MI355X): 12.3 ms (0.74 of 8 TB/s) in a probe of this form,
+// against 13.8 ms for blocks that loop over 16 tiles with the next tile's
+// loads issued before the current tile's store, and 12.8-13.8 ms for every
+// looping form tried (double-buffered, no prefetch, 8 waves of 2 rows,
+// straight-line runs of 2 to 16 tiles): in them the maxima stores cost about
+// 3.7 ms over a pass without them, here 1.3 ms.  The trailing coordinates
+// have their own block so that their code adds no registers to the tiles'
+// (102 registers with it, four waves per SIMD instead of five).
+// The d % 4 trailing coordinates of every row (partial t = ntiles): each
+// wave adds its own rows' squares; wave 0 forms the maximum over all rows.
 template <int ROWS>
-__device__ __forceinline__ void norm_max_load(const float* const rowp[ROWS / 4], int64_t t0, int64_t q_end,
-                                              int lane, f32x4 v[ROWS / 4][4])
+__device__ __forceinline__ void norm_max_tail(const float* __restrict__ g, int64_t d, int32_t M, int64_t ldg,
+                                              int64_t ntiles, double* __restrict__ part, float* __restrict__ amax)
 {
-#pragma unroll
-    for (int r = 0; r < ROWS / 4; ++r)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t q = t0 + lane + 64 * j;
-            v[r][j] = load_nt(rowp[r] + ((q < q_end ? q : q_end - 1) << 2));
-        }
-}
-
-template <int ROWS, bool NT>
-__global__ __launch_bounds__(kBlock) void k_norm_max(const float* __restrict__ g, int64_t d, int32_t M,
-                                                     int64_t ldg, int64_t chunk, int32_t nchunks,
-                                                     double* __restrict__ part, float* __restrict__ amax)
-{
-    constexpr int RPW = ROWS / 4;  // rows per wave
-    __shared__ f32x4 wave_max[4][kBlock];
+    constexpr int RPW = ROWS / 4;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int32_t c = blockIdx.x;
-    const int64_t begin = static_cast<int64_t>(c) * chunk;
-    const int64_t end = begin + chunk < d ? begin + chunk : d;
-    const int64_t q_end = end >> 2;  // chunk starts are multiples of 4: whole quads below end
-    const int64_t spare_quad = (d + 3) >> 2;
-    const float* rowp[RPW];
+    const int64_t tail = ((d >> 2) << 2) + lane;
+    const int64_t nparts = ntiles + 1;
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
         const int m = wave + 4 * r;
-        rowp[r] = g + static_cast<int64_t>(m < M ? m : M - 1) * ldg;
+        const double x = tail < d ? g[static_cast<int64_t>(m < M ? m : M - 1) * ldg + tail] : 0.0;
+        const double sum = wave_sum(x * x);
+        if (lane == 0 && m < M)
+            part[static_cast<int64_t>(m) * nparts + ntiles] = sum;
+    }
+    if (wave == 0 && tail < d) {
+        float mt = 0.0f;
+        for (int32_t m = 0; m < M; ++m)
+            mt = fmaxf(mt, usable_or_zero(g[static_cast<int64_t>(m) * ldg + tail]));
+        amax[tail] = mt;
+    }
+}
+
+// Tile t < ntiles: its maxima and the rows' partials t.
+template <int ROWS, bool NT>
+__device__ __forceinline__ void norm_max_tile(const float* __restrict__ g, int64_t d, int32_t M, int64_t ldg,
+                                              int64_t ntiles, int64_t t, double* __restrict__ part,
+                                              float* __restrict__ amax, f32x4 (*wave_max)[kBlock])
+{
+    constexpr int RPW = ROWS / 4;  // rows per wave
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int64_t nquad = d >> 2;
+    const int64_t q0 = t * kBlock;  // first quad of the tile
+    const int64_t qe = q0 + kBlock < nquad ? q0 + kBlock : nquad;  // > q0
+    // quads past qe re-read quad qe - 1 (the loads carry no branch) and are
+    // zeroed below
+    f32x4 v[RPW][4];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+        const int m = wave + 4 * r;
+        const float* row = g + static_cast<int64_t>(m < M ? m : M - 1) * ldg;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t q = q0 + lane + 64 * j;
+            v[r][j] = load_nt(row + ((q < qe ? q : qe - 1) << 2));
+        }
+    }
+    f32x4 mx[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        mx[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (q0 + lane + 64 * j >= qe) {
+#pragma unroll
+            for (int r = 0; r < RPW; ++r)
+                v[r][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
     }
     double acc[RPW];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r)
-        acc[r] = 0.0;
-    f32x4 v[RPW][4];
-    int64_t t0 = begin >> 2;
-    if (t0 < q_end) {
-        norm_max_load<ROWS>(rowp, t0, q_end, lane, v);
-        // a store after the first loads as after every later batch, so the
-        // loop entry and the back edge agree on the wait for the loads
-        __asm__ volatile("" ::: "memory");
-        *reinterpret_cast<f32x4*>(amax + (spare_quad << 2)) = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-    for (; t0 < q_end; t0 += kBlock) {
-        f32x4 mx[4];
+    for (int r = 0; r < RPW; ++r) {
+        double a = 0.0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            mx[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (t0 + lane + 64 * j >= q_end) {
-#pragma unroll
-                for (int r = 0; r < RPW; ++r)
-                    v[r][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            }
+            a = fma((double)v[r][j].x, (double)v[r][j].x, a);
+            a = fma((double)v[r][j].y, (double)v[r][j].y, a);
+            a = fma((double)v[r][j].z, (double)v[r][j].z, a);
+            a = fma((double)v[r][j].w, (double)v[r][j].w, a);
+            mx[j].x = fmaxf(mx[j].x, usable_or_zero(v[r][j].x));
+            mx[j].y = fmaxf(mx[j].y, usable_or_zero(v[r][j].y));
+            mx[j].z = fmaxf(mx[j].z, usable_or_zero(v[r][j].z));
+            mx[j].w = fmaxf(mx[j].w, usable_or_zero(v[r][j].w));
         }
+        acc[r] = a;
+    }
 #pragma unroll
-        for (int r = 0; r < RPW; ++r) {
-            double a = acc[r];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                a = fma((double)v[r][j].x, (double)v[r][j].x, a);
-                a = fma((double)v[r][j].y, (double)v[r][j].y, a);
-                a = fma((double)v[r][j].z, (double)v[r][j].z, a);
-                a = fma((double)v[r][j].w, (double)v[r][j].w, a);
-                mx[j].x = fmaxf(mx[j].x, usable_or_zero(v[r][j].x));
-                mx[j].y = fmaxf(mx[j].y, usable_or_zero(v[r][j].y));
-                mx[j].z = fmaxf(mx[j].z, usable_or_zero(v[r][j].z));
-                mx[j].w = fmaxf(mx[j].w, usable_or_zero(v[r][j].w));
-            }
-            acc[r] = wave + 4 * r < M ? a : 0.0;
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            wave_max[wave][lane + 64 * j] = mx[j];
-        sync_lds();
-        const f32x4 m0 = wave_max[0][threadIdx.x], m1 = wave_max[1][threadIdx.x];
-        const f32x4 m2 = wave_max[2][threadIdx.x], m3 = wave_max[3][threadIdx.x];
-        sync_lds();  // wave_max is reused by the next tile
-        // the next tile's loads go out before this tile's store
-        if (t0 + kBlock < q_end)
-            norm_max_load<ROWS>(rowp, t0 + kBlock, q_end, lane, v);
-        __asm__ volatile("" ::: "memory");
-        // quads past q_end go to the spare quad after amax (an unconditional
-        // store keeps the wait counts exact)
-        const int64_t q = t0 + threadIdx.x;
+    for (int j = 0; j < 4; ++j)
+        wave_max[wave][lane + 64 * j] = mx[j];
+    sync_lds();
+    const f32x4 m0 = wave_max[0][threadIdx.x], m1 = wave_max[1][threadIdx.x];
+    const f32x4 m2 = wave_max[2][threadIdx.x], m3 = wave_max[3][threadIdx.x];
+    sync_lds();  // wave_max is reused by the block's next tile
+    const int64_t q = q0 + threadIdx.x;
+    if (q < qe) {
         f32x4 o;
         o.x = fmaxf(fmaxf(m0.x, m1.x), fmaxf(m2.x, m3.x));
         o.y = fmaxf(fmaxf(m0.y, m1.y), fmaxf(m2.y, m3.y));
         o.z = fmaxf(fmaxf(m0.z, m1.z), fmaxf(m2.z, m3.z));
         o.w = fmaxf(fmaxf(m0.w, m1.w), fmaxf(m2.w, m3.w));
-        f32x4* dst = reinterpret_cast<f32x4*>(amax + ((q < q_end ? q : spare_quad) << 2));
+        f32x4* dst = reinterpret_cast<f32x4*>(amax + (q << 2));
         if (NT)
             __builtin_nontemporal_store(o, dst);
         else
             *dst = o;
     }
-    // the trailing d % 4 coordinates (last chunk only): each wave adds its own
-    // rows' squares; wave 0 forms the maximum over all rows
-    const int64_t tail = (q_end << 2) + lane;
-    if (tail < end) {
-#pragma unroll
-        for (int r = 0; r < RPW; ++r) {
-            const double x = rowp[r][tail];
-            acc[r] = wave + 4 * r < M ? fma(x, x, acc[r]) : 0.0;
-        }
-        if (wave == 0) {
-            float mx = 0.0f;
-            for (int32_t m = 0; m < M; ++m)
-                mx = fmaxf(mx, usable_or_zero(g[static_cast<int64_t>(m) * ldg + tail]));
-            amax[tail] = mx;
-        }
-    }
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
-        const double s = wave_sum(acc[r]);
+        const double sum = wave_sum(acc[r]);
         const int m = wave + 4 * r;
         if (lane == 0 && m < M)
-            part[static_cast<int64_t>(m) * nchunks + c] = s;
+            part[static_cast<int64_t>(m) * (ntiles + 1) + t] = sum;
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ part, int32_t nchunks,
-                                                   double* __restrict__ rows)
+// ONE: one block per tile plus the trailing coordinates' block (no loop);
+// otherwise blocks stride over them.
+template <int ROWS, bool NT, bool ONE>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void k_norm_max(const float* __restrict__ g, int64_t d, int32_t M,
+                                                     int64_t ldg, int64_t ntiles, double* __restrict__ part,
+                                                     float* __restrict__ amax)
+{
+    __shared__ f32x4 wave_max[4][kBlock];
+    if (ONE) {
+        const int64_t t = blockIdx.x;
+        if (t < ntiles)
+            norm_max_tile<ROWS, NT>(g, d, M, ldg, ntiles, t, part, amax, wave_max);
+        else if (t == ntiles)
+            norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, amax);
+        return;
+    }
+    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x)
+        norm_max_tile<ROWS, NT>(g, d, M, ldg, ntiles, t, part, amax, wave_max);
+    if (blockIdx.x == gridDim.x - 1)
+        norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, amax);
+}
+
+// Block (b, m) sums part[m][b * span .. min(n, (b + 1) * span)) in a fixed
+// order (lane-strided sequential sums, 16 loads in flight per thread, then a
+// fixed butterfly and the four waves in order) into out[m * gridDim.x + b].
+__global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ part, int64_t n, int64_t span,
+                                                   double* __restrict__ out)
 {
     __shared__ double wave_part[kBlock / 64];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const double* p = part + static_cast<int64_t>(blockIdx.x) * nchunks;
-    // nchunks <= 65536: at most 256 partials per thread, 16 loads in flight at a time
+    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * span;
+    const int64_t b1 = b0 + span < n ? b0 + span : n;
+    const double* p = part + static_cast<int64_t>(blockIdx.y) * n;
     double s = 0.0;
-    for (int32_t j0 = 0; j0 < nchunks; j0 += 16 * kBlock) {
+    for (int64_t j0 = b0; j0 < b1; j0 += 16 * kBlock) {
         double x[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            const int32_t c = j0 + static_cast<int32_t>(threadIdx.x) + kBlock * j;
-            x[j] = c < nchunks ? p[c] : 0.0;
+            const int64_t c = j0 + static_cast<int64_t>(threadIdx.x) + kBlock * j;
+            x[j] = c < b1 ? p[c] : 0.0;
         }
 #pragma unroll
         for (int j = 0; j < 16; ++j)
@@ -401,7 +416,8 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
         wave_part[wave] = s;
     __syncthreads();
     if (threadIdx.x == 0)
-        rows[blockIdx.x] = (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
+        out[static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x] =
+            (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
 }
 
 // k_index_max: a block covers kIndexTile quads (8 per thread: quads t,
@@ -1474,23 +1490,32 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
                                float* w, uint8_t* idx, void* ws, hipStream_t stream)
 {
     if (use_fused(d, M, S.K)) {
-        const NormPlan plan = fused_plan(d);
+        const FusedPlan plan = fused_plan(d);
         const FusedLayout L = fused_layout(d, M);
         double* part = static_cast<double*>(ws);
+        double* sub = reinterpret_cast<double*>(static_cast<char*>(ws) + L.sub_off);
         double* rows = reinterpret_cast<double*>(static_cast<char*>(ws) + L.rows_off);
         float* amax = reinterpret_cast<float*>(static_cast<char*>(ws) + L.amax_off);
-        const dim3 grid(static_cast<unsigned>(plan.nchunks));
+        const dim3 grid(one_shot(plan.ntiles + 1, 1));
         // maxima beyond twice the 256 MB Infinity Cache are stored
         // nontemporally (the index pass cannot find them there anyway)
         const bool nt = 4 * d > kMaximaNontemporalBytes;
-#define UQ_LAUNCH_NORM_MAX(R)                                                                                     \
+        const bool one = static_cast<int64_t>(grid.x) >= plan.ntiles + 1;
+#define UQ_LAUNCH_NORM_MAX_(R, NT)                                                                                \
     do {                                                                                                          \
-        if (nt)                                                                                                   \
-            hipLaunchKernelGGL((k_norm_max<R, true>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,    \
-                               plan.nchunks, part, amax);                                                         \
+        if (one)                                                                                                  \
+            hipLaunchKernelGGL((k_norm_max<R, NT, true>), grid, dim3(kBlock), 0, stream, g, d, M, ldg,            \
+                               plan.ntiles, part, amax);                                                          \
         else                                                                                                      \
-            hipLaunchKernelGGL((k_norm_max<R, false>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, plan.chunk,   \
-                               plan.nchunks, part, amax);                                                         \
+            hipLaunchKernelGGL((k_norm_max<R, NT, false>), grid, dim3(kBlock), 0, stream, g, d, M, ldg,           \
+                               plan.ntiles, part, amax);                                                          \
+    } while (0)
+#define UQ_LAUNCH_NORM_MAX(R)              \
+    do {                                   \
+        if (nt)                            \
+            UQ_LAUNCH_NORM_MAX_(R, true);  \
+        else                               \
+            UQ_LAUNCH_NORM_MAX_(R, false); \
     } while (0)
         if (M <= 4)
             UQ_LAUNCH_NORM_MAX(4);
@@ -1499,8 +1524,12 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         else
             UQ_LAUNCH_NORM_MAX(kFuseRows);
 #undef UQ_LAUNCH_NORM_MAX
-        hipLaunchKernelGGL(k_rowsum, dim3(static_cast<unsigned>(M)), dim3(kBlock), 0, stream, part, plan.nchunks,
-                           rows);
+#undef UQ_LAUNCH_NORM_MAX_
+        // the rows' sums: kRowsumSpan tile partials at a time, then those sums
+        hipLaunchKernelGGL(k_rowsum, dim3(static_cast<unsigned>(plan.nsub), static_cast<unsigned>(M)), dim3(kBlock),
+                           0, stream, part, plan.ntiles + 1, kRowsumSpan, sub);
+        hipLaunchKernelGGL(k_rowsum, dim3(1, static_cast<unsigned>(M)), dim3(kBlock), 0, stream, sub, plan.nsub,
+                           plan.nsub, rows);
         const unsigned gx = one_shot((d + 3) / 4, kIndexTile);
         hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, amax, d, M, rows, w, S, idx);
         return hipGetLastError();

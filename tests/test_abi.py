@@ -66,9 +66,11 @@ def test_strerror_and_workspace():
         b = uq.uq_workspace_bytes(d, M)
         assert b % 256 == 0 and b >= 8 * M
         if 2 <= M <= 16:
-            # several scales with 2 to 16 rows: d fp32 row maxima, at most
-            # 65536 fp64 partials per row and M row sums
-            assert 4 * d <= b <= 4 * d + 8 * M * 65536 + 8 * M + 4 * 256
+            # several scales with 2 to 16 rows: d fp32 row maxima, one fp64
+            # partial per row and 1024 coordinates, their sums per 16384
+            # partials, and M row sums
+            tiles = -(-d // 1024)
+            assert 4 * d <= b <= 4 * d + 8 * M * (tiles + -(-tiles // 16384) + 1) + 5 * 256
         else:
             assert b <= 8 * M * 1024 + 256
     assert uq.uq_workspace_bytes(2 ** 30, 17) <= 17 * 1024 * 8 + 256
