@@ -271,10 +271,14 @@ size_t uq_randk_workspace_bytes(int64_t d, int64_t K);
  *   K      1 <= K <= d
  *   sel    [K] uint32 (written), 16-byte aligned
  *   ws     device workspace of uq_randk_workspace_bytes(d, K) bytes
- * The boundary search keeps at most 8192 keys that share the K-th key's top
- * 20 bits (about d / 2^20 are expected, at most 4096 with a standard
- * deviation of 64); more would make the result wrong, which pseudo-random
- * keys do not produce for any d < 2^32.
+ * The boundary search keeps the keys that share the K-th key's top 20 bits
+ * (about d / 2^20 are expected, at most 4096 with a standard deviation of
+ * 64); when more arrive than it keeps, the K-th key's whole 32-bit high word
+ * is found by one more histogram and only the keys with that high word are
+ * ranked, so the result stays exact.  Only if more than 1024 keys share
+ * that 32-bit high word (which pseudo-random keys do not produce for any
+ * d < 2^32) is the selection abandoned: then every entry of sel is
+ * 0xFFFFFFFF, an index >= d that uq_gather reads as 0 and uq_scatter skips.
  */
 int uq_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, size_t ws_bytes,
                     void* stream);
@@ -311,6 +315,10 @@ int uq_set_grid_cap(int64_t blocks);
  *      bracket misses (probability below 1e-20)
  *   0  the histogram passes (two histograms, then the collection pass)
  *   2  the bracket made to miss, so that the fallback always runs
+ *   3  as 0, keeping no boundary candidates, so that the exact refinement
+ *      by the 32-bit high word always runs
+ *   4  as 2, the fallback keeping no boundary candidates (the refinement
+ *      always runs there)
  * Every mode selects the same coordinates.  Process-wide: set it only while
  * no other thread issues library calls.  UQ_EINVAL for another value.
  */

@@ -501,7 +501,7 @@ int uq_scatter(const float* vals, const uint32_t* sel, int64_t K, float* out, in
 int uq_set_randk_mode(int32_t mode)
 {
     if (!uq::set_randk_mode(mode))
-        return fail(UQ_EINVAL, "GlobalRandK mode %d is not 0, 1 or 2", mode);
+        return fail(UQ_EINVAL, "GlobalRandK mode %d is not 0, 1, 2, 3 or 4", mode);
     return ok();
 }
 

@@ -120,13 +120,16 @@ hipError_t launch_sum_dequant(const uint8_t* codes, int64_t d, int32_t rows, int
                               const uint8_t* idx, float* out, hipStream_t stream);
 // GlobalRandK: at most kRandkCandidates keys sharing the threshold's 20-bit
 // prefix are kept (expected d / 2^20 <= 4096 for d < 2^32, standard deviation
-// 64 at most).
+// 64 at most); when more arrive, an exact refinement finds the threshold.
 constexpr int kRandkCandidates = 8192;
 
 size_t randk_workspace_bytes();
 // How the K-subset is found (test hook): the bracket with its exact
 // fallback (default), the multi-pass histograms, or the bracket made to miss.
+// The two NoCandidates modes keep no boundary candidates, so that the exact
+// refinement always runs (histogram route, and the bracket's fallback).
 constexpr int32_t kRandkBracket = 1, kRandkHistogram = 0, kRandkBracketMiss = 2;
+constexpr int32_t kRandkHistogramNoCandidates = 3, kRandkBracketMissNoCandidates = 4;
 bool set_randk_mode(int32_t mode);
 hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* sel, void* ws, hipStream_t stream);
 hipError_t launch_gather(const float* g, int64_t d, int32_t M, int64_t ldg, const uint32_t* sel, int64_t K,

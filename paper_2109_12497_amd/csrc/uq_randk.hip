@@ -60,10 +60,11 @@ constexpr int kRkShardCand = 256;  // bracket candidates per staging list
 
 struct RandkControl {
     uint32_t b1, need1, b2, need2;  // bins found by the two scans
-    uint32_t n_cand, pad0;          // candidate append counter
+    uint32_t n_cand, cand_cap;      // candidate append counter; candidates kept (<= kRandkCandidates)
     uint32_t thr_hi, thr_lo, thr_idx;
     uint32_t x_lo, x_hi;            // collection interval of hi (inclusive)
-    uint32_t pad[5];
+    uint32_t exact;                 // 1: the candidates overflowed, the sort takes the exact path
+    uint32_t pad[4];
 };
 
 constexpr int kRkMaxBlocks = 2048;  // ordered-compaction blocks
@@ -147,7 +148,8 @@ __device__ __forceinline__ void find_bin(const uint32_t* hist, uint32_t need, ui
 }
 
 static_assert(kRkCopies * kRkBins1 == kRkBins2, "one zeroing loop covers both histograms");
-__global__ __launch_bounds__(kBlock) void k_rk_init(RandkWorkspace* __restrict__ ws, uint32_t x_lo, uint32_t x_hi)
+__global__ __launch_bounds__(kBlock) void k_rk_init(RandkWorkspace* __restrict__ ws, uint32_t x_lo, uint32_t x_hi,
+                                                    uint32_t cand_cap)
 {
     for (int b = threadIdx.x; b < kRkBins2; b += kBlock) {
         reinterpret_cast<uint32_t*>(ws->hist1)[b] = 0u;  // kRkCopies * kRkBins1 == kRkBins2
@@ -159,6 +161,8 @@ __global__ __launch_bounds__(kBlock) void k_rk_init(RandkWorkspace* __restrict__
             v = x_lo;
         if (threadIdx.x == offsetof(RandkControl, x_hi) / 4)
             v = x_hi;
+        if (threadIdx.x == offsetof(RandkControl, cand_cap) / 4)
+            v = cand_cap;
         reinterpret_cast<uint32_t*>(&ws->ctl)[threadIdx.x] = v;
     }
     if (threadIdx.x < kRkShards) {
@@ -314,7 +318,7 @@ __global__ __launch_bounds__(kBlock) void k_rk_collect(int64_t d, uint32_t key0,
                         }
                     } else {
                         const uint32_t slot = atomicAdd(&ws->ctl.n_cand, 1u);
-                        if (slot < static_cast<uint32_t>(kRandkCandidates)) {
+                        if (slot < ws->ctl.cand_cap) {
                             ws->cand[slot][0] = word_of(w, j);
                             ws->cand[slot][1] = word_of(l, j);
                             ws->cand[slot][2] = static_cast<uint32_t>(i);
@@ -356,23 +360,127 @@ __device__ __forceinline__ bool key_less(uint32_t ah, uint32_t al, uint32_t ai, 
     return ah != bh ? ah < bh : (al != bl ? al < bl : ai < bi);
 }
 
+// One block, when the keys that share the K-th key's 20-bit prefix P did
+// not all fit the candidate list: the need-th smallest (hi, lo, index) among
+// them, exactly.  A histogram (in LDS, over every key) of the low 12 bits of
+// hi among the keys with prefix P gives the K-th key's whole hi h* and how
+// many keys with hi == h* are still needed; those keys (expected at most one
+// or two for d < 2^32) are collected in LDS and ranked.  False (nothing
+// written) only if more than `cap` keys share that 32-bit hi, which
+// pseudo-random keys do not produce.
+constexpr uint32_t kRkRefineCap = 1024;
+
+template <int T>
+__device__ bool refine_threshold(int64_t d, uint32_t key0, uint32_t key1, uint32_t P, uint32_t need, uint32_t* h,
+                                 uint32_t (*cand)[3], uint32_t cap, uint32_t* scratch, uint32_t* found,
+                                 uint32_t* th, uint32_t* tl, uint32_t* ti)
+{
+    const int64_t nq = (d + 3) >> 2;
+    const uint32_t t = threadIdx.x;
+    for (int b = t; b < kRkBins2; b += T)
+        h[b] = 0u;
+    __syncthreads();
+    for (int64_t q = t; q < nq; q += T) {
+        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t hi = word_of(w, j);
+            if ((q << 2) + j < d && (hi >> 12) == P)
+                atomicAdd(&h[hi & 0xFFFu], 1u);
+        }
+    }
+    __syncthreads();
+    find_bin<kRkBins2 / T, T>(h, need, scratch, &found[0], &found[1]);
+    __syncthreads();
+    const uint32_t hstar = (P << 12) | found[0], need3 = found[1];
+    __syncthreads();
+    if (t == 0)
+        found[0] = 0u;
+    __syncthreads();
+    for (int64_t q = t; q < nq; q += T) {
+        const uint4 w = selection_block(static_cast<uint32_t>(q), 2u, key0, key1);
+        bool any = false;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            any = any || (((q << 2) + j < d) && word_of(w, j) == hstar);
+        if (any) {
+            const uint4 l = selection_block(static_cast<uint32_t>(q), 3u, key0, key1);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (((q << 2) + j < d) && word_of(w, j) == hstar) {
+                    const uint32_t slot = atomicAdd(&found[0], 1u);
+                    if (slot < cap) {
+                        cand[slot][0] = hstar;
+                        cand[slot][1] = word_of(l, j);
+                        cand[slot][2] = static_cast<uint32_t>((q << 2) + j);
+                    }
+                }
+        }
+    }
+    __syncthreads();
+    const uint32_t n = found[0];
+    const bool ok = n <= cap;  // block-uniform
+    if (ok) {
+        for (uint32_t c = t; c < n; c += T) {
+            uint32_t rank = 0u;
+            for (uint32_t u = 0; u < n; ++u)
+                rank += key_less(cand[u][0], cand[u][1], cand[u][2], cand[c][0], cand[c][1], cand[c][2]) ? 1u : 0u;
+            if (rank == need3 - 1u) {
+                *th = cand[c][0];
+                *tl = cand[c][1];
+                *ti = cand[c][2];
+            }
+        }
+    }
+    __syncthreads();
+    return ok;
+}
+
 // One block: the candidate whose rank among the candidates (by hi, lo,
 // index; all distinct) is need2 - 1 is the threshold.  About d / 2^20
 // candidates are expected, so a direct count of smaller keys is cheapest.
 // With PICK the candidates of rank below need2 (the selected ones) are
-// appended to staging list 0.
+// appended to staging list 0.  If more candidates arrived than the list
+// keeps, the threshold comes from refine_threshold instead and (with PICK)
+// ctl.exact sends the sort to the exact path; should that fail too, every
+// output entry is 0xFFFFFFFF and the later passes select nothing.
 template <bool PICK>
-__global__ __launch_bounds__(kRkSortThreads) void k_rk_threshold(RandkWorkspace* __restrict__ ws, uint32_t K)
+__global__ __launch_bounds__(kRkSortThreads) void k_rk_threshold(RandkWorkspace* __restrict__ ws, uint32_t K,
+                                                                 int64_t d, uint32_t key0, uint32_t key1,
+                                                                 uint32_t* __restrict__ sel)
 {
-    const uint32_t n = min(ws->ctl.n_cand, static_cast<uint32_t>(kRandkCandidates));
+    __shared__ uint32_t h[kRkBins2];
+    __shared__ uint32_t cand[kRkRefineCap][3];
+    __shared__ uint32_t scratch[kRkSortThreads / 64];
+    __shared__ uint32_t found[2];
+    __shared__ uint32_t thr[3];
+    const uint32_t n_all = ws->ctl.n_cand;
     const uint32_t want = ws->ctl.need2 - 1u;
+    if (n_all > ws->ctl.cand_cap) {  // block-uniform
+        const uint32_t P = (ws->ctl.b1 << 12) | ws->ctl.b2;
+        const bool ok = refine_threshold<kRkSortThreads>(d, key0, key1, P, want + 1u, h, cand, kRkRefineCap,
+                                                         scratch, found, &thr[0], &thr[1], &thr[2]);
+        if (threadIdx.x == 0) {
+            ws->ctl.exact = 1u;
+            ws->ctl.thr_hi = ok ? thr[0] : 0u;
+            ws->ctl.thr_lo = ok ? thr[1] : 0u;
+            ws->ctl.thr_idx = ok ? thr[2] : 0u;
+            if (!ok)
+                ws->ctl.exact = 2u;
+        }
+        if (!ok)
+            for (uint32_t j = threadIdx.x; j < K; j += kRkSortThreads)
+                sel[j] = 0xFFFFFFFFu;
+        return;
+    }
+    const uint32_t n = n_all;
     for (uint32_t t = threadIdx.x; t < n; t += kRkSortThreads) {
-        const uint32_t h = ws->cand[t][0], l = ws->cand[t][1], i = ws->cand[t][2];
+        const uint32_t h0 = ws->cand[t][0], l = ws->cand[t][1], i = ws->cand[t][2];
         uint32_t rank = 0u;
         for (uint32_t u = 0; u < n; ++u)
-            rank += key_less(ws->cand[u][0], ws->cand[u][1], ws->cand[u][2], h, l, i) ? 1u : 0u;
+            rank += key_less(ws->cand[u][0], ws->cand[u][1], ws->cand[u][2], h0, l, i) ? 1u : 0u;
         if (rank == want) {
-            ws->ctl.thr_hi = h;
+            ws->ctl.thr_hi = h0;
             ws->ctl.thr_lo = l;
             ws->ctl.thr_idx = i;
         }
@@ -456,18 +564,70 @@ constexpr int kRkSliceBuckets = kRkBuckets / kRkSlices;
 static_assert(kRkSliceBuckets == 64, "one wave scans a slice's buckets");
 static_assert(kRkShards * 16 == kRkSortThreads, "16 threads per staging list");
 
+// The selections of one block's slice of the output, in index order, given
+// the threshold (th, tl, ti): one pass in index order that counts the
+// selections of earlier slices (the slice's offset) and writes the slice's
+// own at their places.
+__device__ void write_slice_in_order(int64_t d, uint32_t K, uint32_t key0, uint32_t key1, uint32_t* __restrict__ sel,
+                                     uint32_t th, uint32_t tl, uint32_t ti, uint32_t* scratch)
+{
+    constexpr int T = kRkSortThreads;
+    const int64_t nq = (d + 3) >> 2;
+    const uint32_t t = threadIdx.x;
+    const uint32_t slice = blockIdx.x;
+    const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
+    uint32_t below = 0u, mine = 0u;
+    for (int64_t qb = 0; qb < nq; qb += T) {
+        // past the slice: nothing more to write (the bucket map is monotone)
+        if (bucket_of(static_cast<uint32_t>(qb << 2), scale) / kRkSliceBuckets > slice)
+            break;
+        const int64_t q = qb + t;
+        const uint32_t mask = q < nq ? selected_mask(q, d, key0, key1, th, tl, ti) : 0u;
+        uint32_t mb = 0u, mm = 0u;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((mask >> j) & 1u) {
+                const uint32_t sl = bucket_of(static_cast<uint32_t>((q << 2) + j), scale) / kRkSliceBuckets;
+                mb |= sl < slice ? (1u << j) : 0u;
+                mm |= sl == slice ? (1u << j) : 0u;
+            }
+        const uint32_t nb = __builtin_popcount(mb), nm = __builtin_popcount(mm);
+        const uint32_t ib = block_inclusive_scan<T>(nb, scratch);
+        if (t == T - 1)
+            scratch[T / 64] = ib;
+        __syncthreads();
+        below += scratch[T / 64];  // earlier slices' selections have smaller indices
+        __syncthreads();
+        const uint32_t im = block_inclusive_scan<T>(nm, scratch);
+        uint32_t pos = below + mine + im - nm;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((mm >> j) & 1u) {
+                if (pos < K)
+                    sel[pos] = static_cast<uint32_t>((q << 2) + j);
+                ++pos;
+            }
+        if (t == T - 1)
+            scratch[T / 64] = im;
+        __syncthreads();
+        mine += scratch[T / 64];
+        __syncthreads();
+    }
+}
+
 // The exact selection, for one block's slice of the output (the bracket
 // missed): level-1 and level-2 histograms of hi in LDS, the candidates that
-// share the K-th key's 20-bit prefix ranked for the threshold (key, index),
-// then one pass in index order that counts the selections of earlier slices
-// (the slice's offset) and writes the slice's own at their places.
-// cand: LDS room for kRkSortMax / 3 candidates (about d / 2^20 are expected,
-// at most 4096 on average for d < 2^32).
+// share the K-th key's 20-bit prefix ranked for the threshold (key, index)
+// (if more than `cap` of them arrive, refine_threshold finds it instead),
+// then the slice written in order.  cand: LDS room for kRkSortMax / 3
+// candidates (about d / 2^20 are expected, at most 4096 on average for
+// d < 2^32).  Should refine_threshold fail, every output entry is 0xFFFFFFFF.
 __device__ void sort_exact_slice(int64_t d, uint32_t K, uint32_t key0, uint32_t key1, uint32_t* __restrict__ sel,
-                                 uint32_t* h, uint32_t (*cand)[3], uint32_t* scratch, uint32_t* found)
+                                 uint32_t* h, uint32_t (*cand)[3], uint32_t* scratch, uint32_t* found, uint32_t cap)
 {
     constexpr int T = kRkSortThreads;
     constexpr uint32_t kCap = kRkSortMax / 3;
+    cap = cap < kCap ? cap : kCap;
     const int64_t nq = (d + 3) >> 2;
     const uint32_t t = threadIdx.x;
     // level 1: hi >> 24
@@ -519,7 +679,7 @@ __device__ void sort_exact_slice(int64_t d, uint32_t K, uint32_t key0, uint32_t 
             for (int j = 0; j < 4; ++j)
                 if (((q << 2) + j < d) && (word_of(w, j) >> 12) == prefix) {
                     const uint32_t slot = atomicAdd(&found[0], 1u);
-                    if (slot < kCap) {
+                    if (slot < cap) {
                         cand[slot][0] = word_of(w, j);
                         cand[slot][1] = word_of(l, j);
                         cand[slot][2] = static_cast<uint32_t>((q << 2) + j);
@@ -528,60 +688,30 @@ __device__ void sort_exact_slice(int64_t d, uint32_t K, uint32_t key0, uint32_t 
         }
     }
     __syncthreads();
-    const uint32_t n = min(found[0], kCap);
-    for (uint32_t c = t; c < n; c += T) {
-        uint32_t rank = 0u;
-        for (uint32_t u = 0; u < n; ++u)
-            rank += key_less(cand[u][0], cand[u][1], cand[u][2], cand[c][0], cand[c][1], cand[c][2]) ? 1u : 0u;
-        if (rank == need2 - 1u) {
-            scratch[T / 64 + 1] = cand[c][0];
-            scratch[T / 64 + 2] = cand[c][1];
-            scratch[T / 64 + 3] = cand[c][2];
+    const uint32_t n = found[0];
+    __syncthreads();
+    __shared__ uint32_t thr[3];
+    if (n <= cap) {  // block-uniform
+        for (uint32_t c = t; c < n; c += T) {
+            uint32_t rank = 0u;
+            for (uint32_t u = 0; u < n; ++u)
+                rank += key_less(cand[u][0], cand[u][1], cand[u][2], cand[c][0], cand[c][1], cand[c][2]) ? 1u : 0u;
+            if (rank == need2 - 1u) {
+                thr[0] = cand[c][0];
+                thr[1] = cand[c][1];
+                thr[2] = cand[c][2];
+            }
         }
+        __syncthreads();
+    } else if (!refine_threshold<T>(d, key0, key1, prefix, need2, h, cand, kRkRefineCap, scratch, found, &thr[0],
+                                    &thr[1], &thr[2])) {
+        for (uint32_t j = t; j < K; j += T)
+            sel[j] = 0xFFFFFFFFu;
+        return;
     }
+    const uint32_t th = thr[0], tl = thr[1], ti = thr[2];
     __syncthreads();
-    const uint32_t th = scratch[T / 64 + 1], tl = scratch[T / 64 + 2], ti = scratch[T / 64 + 3];
-    __syncthreads();
-    // the slice's selections in index order, after those of earlier slices
-    const uint32_t slice = blockIdx.x;
-    const double scale = static_cast<double>(kRkBuckets) / static_cast<double>(d);
-    uint32_t below = 0u, mine = 0u;
-    for (int64_t qb = 0; qb < nq; qb += T) {
-        // past the slice: nothing more to write (the bucket map is monotone)
-        if (bucket_of(static_cast<uint32_t>(qb << 2), scale) / kRkSliceBuckets > slice)
-            break;
-        const int64_t q = qb + t;
-        const uint32_t mask = q < nq ? selected_mask(q, d, key0, key1, th, tl, ti) : 0u;
-        uint32_t mb = 0u, mm = 0u;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if ((mask >> j) & 1u) {
-                const uint32_t sl = bucket_of(static_cast<uint32_t>((q << 2) + j), scale) / kRkSliceBuckets;
-                mb |= sl < slice ? (1u << j) : 0u;
-                mm |= sl == slice ? (1u << j) : 0u;
-            }
-        const uint32_t nb = __builtin_popcount(mb), nm = __builtin_popcount(mm);
-        const uint32_t ib = block_inclusive_scan<T>(nb, scratch);
-        if (t == T - 1)
-            scratch[T / 64] = ib;
-        __syncthreads();
-        below += scratch[T / 64];  // earlier slices' selections have smaller indices
-        __syncthreads();
-        const uint32_t im = block_inclusive_scan<T>(nm, scratch);
-        uint32_t pos = below + mine + im - nm;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if ((mm >> j) & 1u) {
-                if (pos < K)
-                    sel[pos] = static_cast<uint32_t>((q << 2) + j);
-                ++pos;
-            }
-        if (t == T - 1)
-            scratch[T / 64] = im;
-        __syncthreads();
-        mine += scratch[T / 64];
-        __syncthreads();
-    }
+    write_slice_in_order(d, K, key0, key1, sel, th, tl, ti, scratch);
 }
 
 // The staged indices (and, with BRACKET, the picks this block makes among
@@ -683,7 +813,8 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
             valid = n_cross <= static_cast<uint32_t>(kRkCross);  // block-uniform
         }
         if (!valid) {
-            sort_exact_slice(d, K, key0, key1, sel, h, reinterpret_cast<uint32_t(*)[3]>(buf), scratch, found);
+            sort_exact_slice(d, K, key0, key1, sel, h, reinterpret_cast<uint32_t(*)[3]>(buf), scratch, found,
+                             ws->ctl.cand_cap);
             return;
         }
         // the picks, into h (the parts' counts are no longer needed)
@@ -707,6 +838,15 @@ __global__ __launch_bounds__(kRkSortThreads) void k_rk_sort(const RandkWorkspace
         npick = min(n_pick, static_cast<uint32_t>(kRkBins2));
     }
 
+    if (!BRACKET && ws->ctl.exact != 0u) {
+        // the histogram route's candidates overflowed: its threshold block
+        // found the threshold exactly (or, failing, wrote the sentinel), but
+        // the selected candidates were not staged, so the slice is written
+        // from the keys themselves
+        if (ws->ctl.exact == 1u)
+            write_slice_in_order(d, K, key0, key1, sel, ws->ctl.thr_hi, ws->ctl.thr_lo, ws->ctl.thr_idx, scratch);
+        return;
+    }
     if (t < kRkSliceBuckets)
         count[t] = 0u;
     __syncthreads();
@@ -803,8 +943,9 @@ __global__ __launch_bounds__(kBlock) void k_rk_count(int64_t d, int64_t chunk, u
 {
     __shared__ uint32_t wave_count[kBlock / 64];
     const uint32_t th = ws->ctl.thr_hi, tl = ws->ctl.thr_lo, ti = ws->ctl.thr_idx;
-    const int64_t q0 = (static_cast<int64_t>(blockIdx.x) * chunk) >> 2;
-    const int64_t q1 = min((static_cast<int64_t>(blockIdx.x) + 1) * chunk, d + 3) >> 2;
+    // the threshold could not be found (the output holds the sentinel): select nothing
+    const int64_t q0 = ws->ctl.exact == 2u ? 0 : (static_cast<int64_t>(blockIdx.x) * chunk) >> 2;
+    const int64_t q1 = ws->ctl.exact == 2u ? 0 : min((static_cast<int64_t>(blockIdx.x) + 1) * chunk, d + 3) >> 2;
     uint32_t count = 0u;
     for (int64_t q = q0 + threadIdx.x; q < q1; q += kBlock)
         count += __builtin_popcount(selected_mask(q, d, key0, key1, th, tl, ti));
@@ -852,8 +993,8 @@ __global__ __launch_bounds__(kBlock) void k_rk_write(int64_t d, int64_t chunk, u
     const int wave = threadIdx.x >> 6;
     const uint64_t below = (uint64_t(1) << lane) - 1u;
     uint32_t base = ws->block_offset[blockIdx.x];
-    const int64_t q0 = (static_cast<int64_t>(blockIdx.x) * chunk) >> 2;
-    const int64_t q1 = min((static_cast<int64_t>(blockIdx.x) + 1) * chunk, d + 3) >> 2;
+    const int64_t q0 = ws->ctl.exact == 2u ? 0 : (static_cast<int64_t>(blockIdx.x) * chunk) >> 2;
+    const int64_t q1 = ws->ctl.exact == 2u ? 0 : min((static_cast<int64_t>(blockIdx.x) + 1) * chunk, d + 3) >> 2;
     // sub-ranges of 1024 coordinates in order: thread t holds group qb + t
     for (int64_t qb = q0; qb < q1; qb += kBlock) {
         const int64_t q = qb + threadIdx.x;
@@ -942,7 +1083,7 @@ static std::atomic<int32_t> g_randk_mode{kRandkBracket};
 
 bool set_randk_mode(int32_t mode)
 {
-    if (mode != kRandkBracket && mode != kRandkHistogram && mode != kRandkBracketMiss)
+    if (mode < kRandkHistogram || mode > kRandkBracketMissNoCandidates)
         return false;
     g_randk_mode.store(mode, std::memory_order_relaxed);
     return true;
@@ -978,18 +1119,23 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
     const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
     const unsigned gx = key_grid(d);  // persistent grid for the key passes
     const int32_t mode = g_randk_mode.load(std::memory_order_relaxed);
+    // the test modes keep no candidates, so that the exact refinement runs
+    const uint32_t cand_cap = (mode == kRandkHistogramNoCandidates || mode == kRandkBracketMissNoCandidates)
+                                  ? 0u
+                                  : static_cast<uint32_t>(kRandkCandidates);
+    const bool histogram = mode == kRandkHistogram || mode == kRandkHistogramNoCandidates;
     uint32_t x_lo = 0u, x_hi = 0u;
-    if (K <= kRkSortMax && mode != kRandkHistogram && randk_bracket(d, K, &x_lo, &x_hi)) {
-        if (mode == kRandkBracketMiss)
+    if (K <= kRkSortMax && !histogram && randk_bracket(d, K, &x_lo, &x_hi)) {
+        if (mode == kRandkBracketMiss || mode == kRandkBracketMissNoCandidates)
             x_lo = x_hi = 0u;  // an interval that cannot hold the K-th key: the exact fallback runs
-        hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, x_lo, x_hi);
+        hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, x_lo, x_hi, cand_cap);
         hipLaunchKernelGGL((k_rk_collect<true, true>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
                            static_cast<uint32_t>(K));
         hipLaunchKernelGGL((k_rk_sort<true>), dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
                            static_cast<uint32_t>(K), d, key0, key1);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, 0u, 0u);
+    hipLaunchKernelGGL(k_rk_init, dim3(1), dim3(kBlock), 0, stream, ws, 0u, 0u, cand_cap);
     // the first histogram merges its LDS bins into global memory: few,
     // long-lived blocks keep those atomics to a few per bin
     int64_t hist_blocks = grid_cap() / 32;  // two blocks per compute unit
@@ -1004,7 +1150,7 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
         hipLaunchKernelGGL((k_rk_collect<true, false>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
                            static_cast<uint32_t>(K));
         hipLaunchKernelGGL(k_rk_threshold<true>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
-                           static_cast<uint32_t>(K));
+                           static_cast<uint32_t>(K), d, key0, key1, sel);
         hipLaunchKernelGGL((k_rk_sort<false>), dim3(kRkSlices), dim3(kRkSortThreads), 0, stream, ws, sel,
                            static_cast<uint32_t>(K), d, key0, key1);
         return hipGetLastError();
@@ -1012,7 +1158,7 @@ hipError_t launch_randk_select(int64_t d, int64_t K, uint64_t seed, uint32_t* se
     hipLaunchKernelGGL((k_rk_collect<false, false>), dim3(gx), dim3(kBlock), 0, stream, d, key0, key1, ws,
                        static_cast<uint32_t>(K));
     hipLaunchKernelGGL(k_rk_threshold<false>, dim3(1), dim3(kRkSortThreads), 0, stream, ws,
-                       static_cast<uint32_t>(K));
+                       static_cast<uint32_t>(K), d, key0, key1, sel);
     // ordered compaction over contiguous chunks (a multiple of 1024 coordinates)
     const int64_t per_block = 1024;
     int64_t chunk = (d + kRkMaxBlocks - 1) / kRkMaxBlocks;

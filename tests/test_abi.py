@@ -351,14 +351,14 @@ def test_grid_cap_accepts_the_range_and_restores():
         uq.uq_set_grid_cap(3)
 
 
-@pytest.mark.parametrize("mode", [-1, 3, 100])
+@pytest.mark.parametrize("mode", [-1, 5, 100])
 def test_randk_mode_rejects(mode):
     assert L.uq_set_randk_mode(mode) == uq.UQ_EINVAL
     assert b"GlobalRandK mode" in L.uq_last_error()
 
 
 def test_randk_mode_accepts_and_restores():
-    for mode in (0, 2, 1):
+    for mode in (0, 2, 3, 4, 1):
         assert L.uq_set_randk_mode(mode) == uq.UQ_OK
 
 

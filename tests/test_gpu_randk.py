@@ -33,11 +33,15 @@ def gpu_select(d, K, seed):
     # both sides of the largest K that one block sorts
     (100_000, 16_384, 11), (100_000, 16_385, 12),
 ])
-@pytest.mark.parametrize("mode", [1, 0, 2], ids=["bracket", "histograms", "bracket-missed"])
+@pytest.mark.parametrize("mode", [1, 0, 2, 3, 4], ids=["bracket", "histograms", "bracket-missed",
+                                                     "histograms-refined", "bracket-missed-refined"])
 def test_selection_matches_oracle(d, K, seed, mode):
     """Each way of finding the subset (for K <= 16384: the bracket of the K-th
     key, the histogram passes, and the bracket made to miss so that the
-    selection block's exact fallback runs) against the oracle."""
+    selection block's exact fallback runs; and both of the last two with no
+    boundary candidates kept, so that the exact refinement by the K-th key's
+    whole 32-bit high word runs, as it does when more candidates arrive than
+    the lists keep) against the oracle."""
     uq.uq_set_randk_mode(mode)
     try:
         got = gpu_select(d, K, seed)
@@ -147,14 +151,14 @@ def _random_selections(n=18, seed=3344):
         d = int(rng.choice([int(rng.integers(1, 2000)), int(rng.integers(2000, 200_000)),
                             int(rng.integers(200_000, 1_500_000))]))
         K = int(rng.choice([1, int(rng.integers(1, d + 1)), min(d, int(rng.integers(1, 20_000)))]))
-        out.append((d, K, int(rng.integers(0, 2 ** 64, dtype=np.uint64)), i % 3))
+        out.append((d, K, int(rng.integers(0, 2 ** 64, dtype=np.uint64)), i % 5))
     return out
 
 
 @pytest.mark.parametrize("d,K,seed,mode", _random_selections())
 def test_random_selections(d, K, seed, mode):
     """Seeded random (d, K, seed) in every selection mode, against the oracle."""
-    uq.uq_set_randk_mode([1, 0, 2][mode])
+    uq.uq_set_randk_mode([1, 0, 2, 3, 4][mode])
     try:
         got = gpu_select(d, K, seed)
     finally:
