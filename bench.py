@@ -164,10 +164,16 @@ def measured_traffic(kernel: str, workload: str):
 
 
 def stream_probe(workload: str, reps: int) -> None:
-    """Achievable bandwidth of the hot path's two access patterns with no work,
-    on the workload's gradient buffer: the norm pass (read M*d floats) and the
-    quantiser (read M*d floats, write M*d bytes).  Kernels from libuq_probe.so,
-    timed back to back between events."""
+    """Achievable bandwidth of the hot path's access patterns with no work, on
+    the workload's gradients (kernels of libuq_probe.so, timed back to back
+    between events, mean of three rounds):
+      read            every element of the [M, ldg] buffer, grid-stride;
+      read4_write1    4 bytes read and 1 written per element (the quantiser);
+      rows_read       the first d floats of each of the M rows, by blocks of
+                      one chunk of one row (the norm pass's bytes);
+      accumulate      4 + 1 + 4 bytes read and 4 written per coordinate of one
+                      row (the fused quantise-and-sum of a streamed worker);
+      copy            one row copied (4 bytes read, 4 written)."""
     import ctypes
 
     import torch
@@ -175,35 +181,45 @@ def stream_probe(workload: str, reps: int) -> None:
     import synth
 
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2109_12497_amd", "libuq_probe.so"))
-    P, i64 = ctypes.c_void_p, ctypes.c_int64
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.uqp_read.argtypes = [P, i64, P, P]
     lib.uqp_read_write8.argtypes = [P, i64, P, P]
     lib.uqp_read_out_floats.argtypes = [i64]
     lib.uqp_read_out_floats.restype = i64
+    lib.uqp_rows_read.argtypes = [P, i64, i32, i64, P, P]
+    lib.uqp_rows_out_floats.argtypes = [i64, i32]
+    lib.uqp_rows_out_floats.restype = i64
+    lib.uqp_accumulate.argtypes = [P, P, P, i64, P]
+    lib.uqp_copy.argtypes = [P, P, i64, P]
     g, cfg = synth.make_gradients(workload, device="cuda")
+    M, d = cfg["M"], cfg["d"]
     n = g.numel() // 512 * 512
+    dn = d // 512 * 512
     codes = torch.empty(n, dtype=torch.uint8, device="cuda")
     out = torch.empty(int(lib.uqp_read_out_floats(n)), dtype=torch.float32, device="cuda")
+    rows_out = torch.empty(int(lib.uqp_rows_out_floats(dn, M)), dtype=torch.float32, device="cuda")
+    idx = torch.ones(dn, dtype=torch.uint8, device="cuda")
+    acc = torch.zeros(dn, dtype=torch.int32, device="cuda")
+    dst = torch.empty(dn, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
     h = stream.cuda_stream
 
     def timed(fn):
-        for _ in range(max(20, reps // 4)):
+        for _ in range(3):
             assert fn() == 0
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(reps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps * 1e-3
+        return stage_ms_per_call(torch, stream, fn, max(5, reps // 4)) * 1e-3
 
     t_r = timed(lambda: lib.uqp_read(g.data_ptr(), n, out.data_ptr(), h))
     t_rw = timed(lambda: lib.uqp_read_write8(g.data_ptr(), n, codes.data_ptr(), h))
-    print(json.dumps({"stream_probe": workload, "elements": n,
-                      "read_GBps": round(4 * n / t_r / 1e9, 1), "read_us": round(t_r * 1e6, 2),
-                      "read4_write1_GBps": round(5 * n / t_rw / 1e9, 1), "read4_write1_us": round(t_rw * 1e6, 2)}))
+    t_rows = timed(lambda: lib.uqp_rows_read(g.data_ptr(), dn, M, g.stride(0), rows_out.data_ptr(), h))
+    t_acc = timed(lambda: lib.uqp_accumulate(g.data_ptr(), idx.data_ptr(), acc.data_ptr(), dn, h))
+    t_copy = timed(lambda: lib.uqp_copy(g.data_ptr(), dst.data_ptr(), dn, h))
+    res = {"stream_probe": workload, "elements": n, "d": dn, "M": M}
+    for name, nbytes, t in (("read", 4 * n, t_r), ("read4_write1", 5 * n, t_rw), ("rows_read", 4 * M * dn, t_rows),
+                            ("accumulate", 13 * dn, t_acc), ("copy", 8 * dn, t_copy)):
+        res[f"{name}_us"] = round(t * 1e6, 2)
+        res[f"{name}_GBps"] = round(nbytes / t / 1e9, 1)
+    print(json.dumps(res))
 
 
 def copy_probe(nbytes: int) -> None:

@@ -312,6 +312,43 @@ def test_index_at_scale_boundaries(M):
     assert len(set(ref["idx"][100:col:7].tolist())) >= 3
 
 
+@pytest.mark.parametrize("M", [2, 8, 16])
+def test_many_maxima_in_a_thresholds_key_bucket(M):
+    """With several scales and 2 to 16 rows the index pass compares 16-bit
+    keys of the row maxima with the thresholds' keys and re-reads the rows of
+    a coordinate whose key ties one: thousands of coordinates placed within
+    2^-9 (relative) of the scales' limits (at most 150 per row near W/16, so
+    that a one-hot row still sets W), plus tiny denormal maxima, so that much
+    of the index comes from that exact path; all against the oracle."""
+    scales = synth.scales_for(8, 4)
+    Wv = np.float32(0.9)
+    d = 40_000 + 13
+    rng = np.random.default_rng(M)
+    host = np.zeros((M, synth.round_up(d, 64)), dtype=np.float32)
+    host[1:, 1:d] = (rng.standard_normal((M - 1, d - 1)) * 1e-7).astype(np.float32)
+    cols = rng.permutation(np.arange(1, d))
+    counts = {1: 150 * (M - 1), 2: 6000, 3: 12000}
+    at = 0
+    for k in range(1, len(scales)):
+        inv = np.float32(np.float64(np.float32(scales[k])) / np.float64(Wv))
+        T = _largest_passing(inv, np.float32(scales[0]))
+        c = cols[at:at + counts[k]]
+        at += counts[k]
+        vals = (T * (1.0 + rng.uniform(-2.0 ** -9, 2.0 ** -9, size=c.size))).astype(np.float32)
+        rows = 1 + np.arange(c.size) % (M - 1)  # spread evenly over the rows after the first
+        host[rows, c] = vals * rng.choice(np.array([1, -1], dtype=np.float32), size=c.size)
+    tiny = cols[at:at + 5000]
+    host[1 + np.arange(tiny.size) % (M - 1), tiny] = (rng.integers(1, 1 << 14, size=tiny.size) *
+                                                      (2.0 ** -149)).astype(np.float32)
+    host[0, :] = 0.0
+    host[0, 0] = Wv  # a one-hot row: its norm is W
+    assert np.sqrt((host.astype(np.float64) ** 2).sum(axis=1)).max() == np.float64(Wv)
+    res, _, _ = gpu_step(host, d, scales, seed=9)
+    assert res["W"] == Wv
+    ref = assert_matches_oracle(res, host, d, scales, seed=9)
+    assert len(set(ref["idx"].tolist())) == len(scales)
+
+
 @pytest.mark.parametrize("bad", [np.inf, -np.inf, np.nan])
 def test_non_finite_inputs_take_zero_path(bad):
     d, M = 999, 2

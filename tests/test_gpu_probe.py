@@ -23,6 +23,11 @@ def probe_lib():
     lib.uqp_read_write8.argtypes = [P, i64, P, P]
     lib.uqp_read_out_floats.argtypes = [i64]
     lib.uqp_read_out_floats.restype = i64
+    lib.uqp_rows_read.argtypes = [P, i64, ctypes.c_int32, i64, P, P]
+    lib.uqp_rows_out_floats.argtypes = [i64, ctypes.c_int32]
+    lib.uqp_rows_out_floats.restype = i64
+    lib.uqp_accumulate.argtypes = [P, P, P, i64, P]
+    lib.uqp_copy.argtypes = [P, P, i64, P]
     return lib
 
 
@@ -40,3 +45,29 @@ def test_probe_kernels(n):
     assert np.array_equal(codes.cpu().numpy(), top)
     # the read kernel's per-thread sums add up to the sum of all elements
     assert abs(float(out.double().sum()) - float(g.double().sum())) <= 1e-3 * max(1.0, float(g.abs().sum()))
+
+
+@pytest.mark.parametrize("d,M", [(512, 1), (512 * 300, 3), (65536 * 2 + 1024, 4)])
+def test_row_accumulate_and_copy_probes(d, M):
+    lib = probe_lib()
+    s = torch.cuda.current_stream().cuda_stream
+    ldg = d + 64
+    g = torch.randn((M, ldg), device="cuda") * 100
+    out = torch.zeros(int(lib.uqp_rows_out_floats(d, M)), device="cuda")
+    assert lib.uqp_rows_read(g.data_ptr(), d, M, ldg, out.data_ptr(), s) == 0
+    idx = torch.randint(0, 256, (d,), dtype=torch.uint8, device="cuda")
+    acc = torch.randint(-1000, 1000, (d,), dtype=torch.int32, device="cuda")
+    before = acc.clone()
+    assert lib.uqp_accumulate(g.data_ptr(), idx.data_ptr(), acc.data_ptr(), d, s) == 0
+    dst = torch.zeros(d, device="cuda")
+    assert lib.uqp_copy(g.data_ptr(), dst.data_ptr(), d, s) == 0
+    torch.cuda.synchronize()
+    rows = g[:, :d].double().sum(dim=1)
+    got = out.double().reshape(M, -1).sum(dim=1)
+    assert torch.allclose(got, rows, rtol=1e-4, atol=1e-2 * d ** 0.5)
+    want = before + idx.to(torch.int32) + g[0, :d].to(torch.int32)  # truncation toward zero, as the probe
+    assert torch.equal(acc, want)
+    assert torch.equal(dst, g[0, :d])
+    # out-of-range arguments are refused before any launch
+    assert lib.uqp_rows_read(g.data_ptr(), d, M, d - 4, out.data_ptr(), s) == -1
+    assert lib.uqp_accumulate(g.data_ptr(), idx.data_ptr(), acc.data_ptr(), d + 1, s) == -1
