@@ -425,10 +425,25 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
 // before W is formed.  The per-coordinate rule compares thresholds instead of
 // forming products: a -> RN32(a * inv_k) is non-decreasing for inv_k > 0, so
 // RN32(a * inv_k) <= s_0 holds exactly for a <= T_k, the largest binary32
-// that passes; each block finds T_k once (a few ulp steps from s_0 / inv_k),
-// and a coordinate costs K compares.
+// that passes; each block finds T_k once (a few ulp steps from s_0 / inv_k).
+// The count #{k : a <= T_k} then needs no loop over k when no binade holds
+// two thresholds (scales at least about twice apart, as 16^k): every T_k in a
+// higher binade than a's counts, none in a lower one, so a table over the 256
+// values of the exponent field gives the count above a's binade and the one
+// threshold inside it, and a coordinate costs one lookup and one compare.
+// Otherwise the block counts with K compares per coordinate.
 constexpr int kIndexQuads = 8;
 constexpr int64_t kIndexTile = kIndexQuads * kBlock;
+static_assert(kBlock == 256, "the exponent table has one entry per thread");
+
+// Index of a >= 0 from the block's exponent table: entry e holds the one
+// threshold whose exponent field is e (or -1, which nothing passes) and the
+// index that a coordinate of binade e gets when it does not pass it.
+__device__ __forceinline__ uint32_t index_from_table(const uint2* tab, float a)
+{
+    const uint2 t = tab[__builtin_amdgcn_ubfe(__builtin_bit_cast(uint32_t, a), 23, 8)];
+    return t.y + (a <= __builtin_bit_cast(float, t.x) ? 1u : 0u);
+}
 
 // Largest binary32 a >= 0 with RN32(a * inv) <= s0, for 0 < inv; 0 when inv
 // is infinite (then no positive a passes).
@@ -465,6 +480,7 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
                                                       ScaleSet S, uint8_t* __restrict__ idx)
 {
     __shared__ float thr_s[kMaxScales];
+    __shared__ uint2 tab_s[256];
     const int64_t nquad = d >> 2;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kIndexTile;
     const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kIndexTile;
@@ -495,6 +511,37 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
     if (threadIdx.x < K)
         thr_s[threadIdx.x] = zero ? 0.0f : index_threshold(div_rn32(S.s[threadIdx.x], W), s0);
     __syncthreads();
+    // thread e forms the table's entry e: the thresholds in higher binades
+    // (all of them pass), the one in binade e; on the zero path, and for the
+    // non-finite binade, every coordinate gets K - 1
+    int crowded = 0;
+    {
+        const uint32_t e = threadIdx.x;
+        int32_t above = 0, inside = 0;
+        float tin = -1.0f;
+        for (int k = 0; k < K; ++k) {
+            const float t = thr_s[k];
+            const uint32_t be = __builtin_bit_cast(uint32_t, t) >> 23;
+            above += be > e ? 1 : 0;
+            if (be == e) {
+                ++inside;
+                tin = t;
+            }
+        }
+        uint2 ent;
+        if (zero || e == 255) {
+            ent.x = __builtin_bit_cast(uint32_t, -1.0f);
+            ent.y = static_cast<uint32_t>(K - 1);
+        } else {
+            // #{k : a <= T_k} - 1 = above - 1 + [a <= tin]; with nothing
+            // above, index 0 either way
+            crowded = inside > 1 ? 1 : 0;
+            ent.x = __builtin_bit_cast(uint32_t, above > 0 ? tin : -1.0f);
+            ent.y = static_cast<uint32_t>(above > 0 ? above - 1 : 0);
+        }
+        tab_s[e] = ent;
+    }
+    const bool by_table = __syncthreads_or(crowded) == 0;
 
     for (int64_t t0 = tile0; t0 < nquad; t0 += stride) {
         if (t0 != tile0) {
@@ -503,6 +550,20 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
                 const int64_t q = t0 + threadIdx.x + kBlock * j;
                 a[j] = q < nquad ? load_nt(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
             }
+        }
+        if (by_table) {
+#pragma unroll
+            for (int j = 0; j < kIndexQuads; ++j) {
+                const int64_t q = t0 + threadIdx.x + kBlock * j;
+                if (q < nquad) {
+                    const uint32_t packed = index_from_table(tab_s, a[j].x) |
+                                            (index_from_table(tab_s, a[j].y) << 8) |
+                                            (index_from_table(tab_s, a[j].z) << 16) |
+                                            (index_from_table(tab_s, a[j].w) << 24);
+                    *reinterpret_cast<uint32_t*>(idx + (q << 2)) = packed;
+                }
+            }
+            continue;
         }
         int32_t cnt[kIndexQuads][4];
 #pragma unroll
@@ -533,10 +594,14 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
     const int64_t t = (nquad << 2) + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     if (blockIdx.x == 0 && t < d) {
         const float x = amax[t];
-        int32_t count = 0;
-        for (int k = 0; k < K; ++k)
-            count += x <= thr_s[k] ? 1 : 0;
-        idx[t] = static_cast<uint8_t>(index_from_count(x, count, K, zero));
+        if (by_table) {
+            idx[t] = static_cast<uint8_t>(index_from_table(tab_s, x));
+        } else {
+            int32_t count = 0;
+            for (int k = 0; k < K; ++k)
+                count += x <= thr_s[k] ? 1 : 0;
+            idx[t] = static_cast<uint8_t>(index_from_count(x, count, K, zero));
+        }
     }
 }
 

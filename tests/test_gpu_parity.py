@@ -314,12 +314,12 @@ def test_index_at_scale_boundaries(M):
 
 @pytest.mark.parametrize("M", [2, 8, 16])
 def test_many_maxima_in_a_thresholds_key_bucket(M):
-    """With several scales and 2 to 16 rows the index pass compares 16-bit
-    keys of the row maxima with the thresholds' keys and re-reads the rows of
-    a coordinate whose key ties one: thousands of coordinates placed within
-    2^-9 (relative) of the scales' limits (at most 150 per row near W/16, so
-    that a one-hot row still sets W), plus tiny denormal maxima, so that much
-    of the index comes from that exact path; all against the oracle."""
+    """With several scales and 2 to 16 rows the index pass reads the row
+    maxima and compares each with the scales' limits: thousands of
+    coordinates placed within 2^-9 (relative) of the limits (at most 150 per
+    row near W/16, so that a one-hot row still sets W), in the binades where
+    the pass's exponent table holds them, plus tiny denormal maxima (the
+    table's lowest binade); all against the oracle."""
     scales = synth.scales_for(8, 4)
     Wv = np.float32(0.9)
     d = 40_000 + 13
@@ -603,6 +603,47 @@ def test_streamed_rows_longer_than_2_pow_31():
     assert int(step.sum[:d].abs().max()) <= M * scales[0]
     del g, step
     torch.cuda.empty_cache()
+
+
+# (scales, whether two limits share a binade when W = 0.9)
+CLOSE_SCALES = [([3.0, 100.0, 110.0, 120.0], True), ([7.0, 112.0, 120.0, 1792.0], True),
+                ([3.0, 20.0, 50.0, 120.0, 300.0], False), ([1.0, 3.0, 7.0, 15.0, 31.0, 63.0, 127.0], False)]
+
+
+@pytest.mark.parametrize("scales,crowded", CLOSE_SCALES, ids=["crowded3", "crowded2", "adjacent4", "adjacent6"])
+@pytest.mark.parametrize("M", [3, 16])
+def test_index_with_close_scales(scales, crowded, M):
+    """Scale sets whose limits share a binade (the index pass then counts
+    with K compares per coordinate) or sit one per binade in neighbouring
+    binades (its exponent table): coordinates at, and one ulp either side of,
+    every limit, and magnitudes spread over many binades, against the oracle
+    (Eq. (11) and the min over workers)."""
+    Wv = np.float32(0.9)
+    limits = []
+    for k in range(1, len(scales)):
+        inv = np.float32(np.float64(np.float32(scales[k])) / np.float64(Wv))
+        limits.append(_largest_passing(inv, np.float32(scales[0])))
+    binades = [int(np.float32(t).view(np.uint32)) >> 23 for t in limits]
+    assert (len(set(binades)) < len(binades)) == crowded
+    d = 8192 + 37
+    rng = np.random.default_rng(M + len(scales))
+    host = np.zeros((M, synth.round_up(d, 64)), dtype=np.float32)
+    host[0, 0] = Wv  # a one-hot row: its norm is W
+    for m in range(1, M):
+        cols = rng.choice(np.arange(1, d), size=100, replace=False)
+        host[m, cols] = (10.0 ** rng.uniform(-6.0, np.log10(0.05), size=100) *
+                         rng.choice([-1.0, 1.0], size=100)).astype(np.float32)
+    col = 9
+    for T in limits:
+        for v in (T, np.nextafter(T, np.float32(0)), np.nextafter(T, np.float32(np.inf))):
+            for sign in (1, -1):
+                host[1 + (col % (M - 1)), col] = sign * v
+                col += 11
+    assert np.sqrt((host.astype(np.float64) ** 2).sum(axis=1)).max() == np.float64(Wv)
+    res, _, _ = gpu_step(host, d, scales, seed=23)
+    assert res["W"] == Wv
+    ref = assert_matches_oracle(res, host, d, scales, seed=23)
+    assert len(set(ref["idx"][9:col:11].tolist())) >= 3
 
 
 def _random_configs(n=24, seed=2109):
