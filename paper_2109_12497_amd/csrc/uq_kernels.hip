@@ -7,14 +7,16 @@
 //                over rows, sqrt -> W
 //   k_index      shared scale index from the largest |g| over    (Eq. (11) +
 //                the workers at each coordinate                    sharing)
-//   k_norm_max   several scales, 2..16 rows: the norm's chunk    (norm + the
+//   k_norm_max   several scales, 2..16 rows: the norm's tile     (norm + the
 //                sums and the largest |g| over the rows in one     index's input)
 //                read of the gradients
-//   k_rowsum     the rows' sums from those chunk sums
+//   k_rowsum     the rows' sums from those tile sums
 //   k_index_max  W, then the shared index from the stored maxima
 //   k_quantise   Philox draws + stochastic rounding + int8 pack  (Eq. (8)/(12))
 //   k_sum        int8 (or 4-/2-bit) code rows -> int32           (all-reduce)
 //                sums, optionally with the reconstruction applied  (+ Eq. (9)/(13))
+//   k_quant_sum  the quantiser's codes added straight into the   (Eq. (8)/(12) +
+//                int32 sums, never stored (+ the reconstruction)   all-reduce)
 //   k_dequant    int32 (+ index) -> fp32                          (Eq. (9)/(13))
 //
 // Every per-coordinate result is a pure function of its inputs and the
@@ -226,8 +228,10 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 // over the gradients forms the rows' chunk sums of squares and the largest
 // usable |g| over the rows at every coordinate (amax, fp32 [d] in the
 // workspace); the index pass then reads amax instead of the M rows.
-//   k_norm_max   block c: chunk c of every row (below)
-//   k_rowsum     block m: S_m = fixed-order sum of row m's chunk partials
+//   k_norm_max   block t: tile t of every row (below)
+//   k_rowsum     twice: block (b, m) sums partials [b s, (b + 1) s) of row
+//                m in a fixed order (s = kRowsumSpan), then block (0, m)
+//                sums those into S_m
 //   k_index_max  W from the S_m (the rule of k_finish; block 0 stores it),
 //                then the index of every coordinate from amax
 // ---------------------------------------------------------------------------
