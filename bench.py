@@ -72,14 +72,14 @@ def scale_kernels(M: int, K: int) -> list:
 
 def shared_scale_bytes(d: int, M: int, K: int) -> int:
     """The gradients read once for the norm; with several scales and 2 to 16
-    workers that pass also writes the largest |g| over the workers (4 bytes
-    per coordinate), which the index pass reads instead of the gradients;
-    with more workers (or one) the index pass reads every gradient again.
-    The index is written once."""
+    workers that pass also writes a 16-bit key of the largest |g| over the
+    workers (2 bytes per coordinate), which the index pass reads instead of
+    the gradients; with more workers (or one) the index pass reads every
+    gradient again.  The index is written once."""
     if K == 1:
         return 4 * M * d
     if 2 <= M <= FUSED_MAX_ROWS:
-        return 4 * M * d + 4 * d + 4 * d + d
+        return 4 * M * d + 2 * d + 2 * d + d
     return 4 * M * d + 4 * M * d + d
 
 

@@ -106,11 +106,11 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg,
  *   Limit: the scratch the kernels need must fit the buffer.  With one
  *   scale, or more than 16 rows, or one row, that is 8 * M * ceil(d / c)
  *   bytes with c >= 8192 chunks of at most 1024 per row: any d for
- *   M <= 8192.  With several scales and 2 to 16 rows the pass keeps the
- *   row maxima (4 * d bytes) and one fp64 partial per row and 1024
- *   coordinates (8 * M * d / 1024 bytes): d up to about 16.7 million with
- *   2 rows, 16.5 million with 8 and 16.2 million with 16.  A call beyond the
- *   limit returns UQ_EWORKSPACE and launches nothing.
+ *   M <= 8192.  With several scales and 2 to 16 rows the pass keeps a
+ *   16-bit key of the row maximum (2 * d bytes) and one fp64 partial per
+ *   row and 1024 coordinates (8 * M * d / 1024 bytes): d up to about 33.3
+ *   million with 2 rows, 32.5 million with 8 and 31.6 million with 16.  A
+ *   call beyond the limit returns UQ_EWORKSPACE and launches nothing.
  *   Every call on one device shares that device's buffer (nothing in it
  *   needs to start at zero): calls that overlap on one device, on different
  *   streams or threads, race and give undefined results.
@@ -122,9 +122,10 @@ int uq_shared_scale_noalloc(const float* g, int64_t d, int32_t M, int64_t ldg,
                             void* stream);
 
 /* Workspace bytes uq_shared_scale needs for (d, M) and any K; 0 never
- * returned.  With 2 <= M <= 16 this includes 4 * d bytes: with several scales the
- * norm pass also keeps the largest |g| over the rows at every coordinate, so
- * that the index pass need not read the gradients again. */
+ * returned.  With 2 <= M <= 16 this includes 2 * d bytes: with several scales
+ * the norm pass also keeps the top 16 bits of the largest |g| over the rows
+ * at every coordinate, so that the index pass need not read the gradients
+ * again (except at the rare coordinates whose key equals a scale limit's). */
 size_t uq_workspace_bytes(int64_t d, int32_t M);
 
 /*

@@ -21,6 +21,8 @@ constexpr float kFloatMax = 3.40282346638528859812e+38f;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Single-use streams: loads and stores marked nontemporal so they do not
 // displace reused lines from the caches.
@@ -31,6 +33,10 @@ __device__ __forceinline__ f32x4 load_nt(const float* p)
 __device__ __forceinline__ i32x4 load_nt(const int32_t* p)
 {
     return __builtin_nontemporal_load(reinterpret_cast<const i32x4*>(p));
+}
+__device__ __forceinline__ u32x4 load_nt(const uint32_t* p)
+{
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 __device__ __forceinline__ uint32_t load_nt_u32(const void* p)
 {

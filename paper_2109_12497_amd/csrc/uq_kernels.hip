@@ -11,7 +11,7 @@
 //                sums and the largest |g| over the rows in one     index's input)
 //                read of the gradients
 //   k_rowsum     the rows' sums from those tile sums
-//   k_index_max  W, then the shared index from the stored maxima
+//   k_index_max  W, then the shared index from the maxima's keys
 //   k_quantise   Philox draws + stochastic rounding + int8 pack  (Eq. (8)/(12))
 //   k_sum        int8 (or 4-/2-bit) code rows -> int32           (all-reduce)
 //                sums, optionally with the reconstruction applied  (+ Eq. (9)/(13))
@@ -225,15 +225,17 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 
 // ---------------------------------------------------------------------------
 // Fused shared scale for several scales and at most kFuseRows rows: one pass
-// over the gradients forms the rows' chunk sums of squares and the largest
-// usable |g| over the rows at every coordinate (amax, fp32 [d] in the
-// workspace); the index pass then reads amax instead of the M rows.
+// over the gradients forms the rows' tile sums of squares and, at every
+// coordinate, the top 16 bits of the largest usable |g| over the rows (a
+// key, uint16 [d] in the workspace); the index pass then reads the keys
+// instead of the M rows, and the rows of the rare coordinates whose key
+// equals a threshold's.
 //   k_norm_max   block t: tile t of every row (below)
 //   k_rowsum     twice: block (b, m) sums partials [b s, (b + 1) s) of row
 //                m in a fixed order (s = kRowsumSpan), then block (0, m)
 //                sums those into S_m
 //   k_index_max  W from the S_m (the rule of k_finish; block 0 stores it),
-//                then the index of every coordinate from amax
+//                then the index of every coordinate from its key
 // ---------------------------------------------------------------------------
 // Barrier for LDS traffic only: the block's LDS writes are complete and
 // visible, while its global loads and stores stay in flight (__syncthreads
@@ -265,7 +267,7 @@ __device__ __forceinline__ void sync_lds()
 // wave adds its own rows' squares; wave 0 forms the maximum over all rows.
 template <int ROWS>
 __device__ __forceinline__ void norm_max_tail(const float* __restrict__ g, int64_t d, int32_t M, int64_t ldg,
-                                              int64_t ntiles, double* __restrict__ part, float* __restrict__ amax)
+                                              int64_t ntiles, double* __restrict__ part, uint16_t* __restrict__ keys)
 {
     constexpr int RPW = ROWS / 4;
     const int lane = threadIdx.x & 63;
@@ -284,15 +286,15 @@ __device__ __forceinline__ void norm_max_tail(const float* __restrict__ g, int64
         float mt = 0.0f;
         for (int32_t m = 0; m < M; ++m)
             mt = fmaxf(mt, usable_or_zero(g[static_cast<int64_t>(m) * ldg + tail]));
-        amax[tail] = mt;
+        keys[tail] = static_cast<uint16_t>(__builtin_bit_cast(uint32_t, mt) >> 16);
     }
 }
 
-// Tile t < ntiles: its maxima and the rows' partials t.
+// Tile t < ntiles: its maxima's keys and the rows' partials t.
 template <int ROWS, bool NT>
 __device__ __forceinline__ void norm_max_tile(const float* __restrict__ g, int64_t d, int32_t M, int64_t ldg,
                                               int64_t ntiles, int64_t t, double* __restrict__ part,
-                                              float* __restrict__ amax, f32x4 (*wave_max)[kBlock])
+                                              uint16_t* __restrict__ keys, f32x4 (*wave_max)[kBlock])
 {
     constexpr int RPW = ROWS / 4;  // rows per wave
     const int lane = threadIdx.x & 63;
@@ -354,11 +356,18 @@ __device__ __forceinline__ void norm_max_tile(const float* __restrict__ g, int64
         o.y = fmaxf(fmaxf(m0.y, m1.y), fmaxf(m2.y, m3.y));
         o.z = fmaxf(fmaxf(m0.z, m1.z), fmaxf(m2.z, m3.z));
         o.w = fmaxf(fmaxf(m0.w, m1.w), fmaxf(m2.w, m3.w));
-        f32x4* dst = reinterpret_cast<f32x4*>(amax + (q << 2));
+        // the keys: the top halves of the four maxima (permute selector:
+        // bytes 2-3 of the second operand, then bytes 2-3 of the first).
+        // __float_as_uint takes the component's value; __builtin_bit_cast of
+        // a vector component compiled to a read of component x here.
+        u32x2 k;
+        k.x = __builtin_amdgcn_perm(__float_as_uint(o.y), __float_as_uint(o.x), 0x07060302u);
+        k.y = __builtin_amdgcn_perm(__float_as_uint(o.w), __float_as_uint(o.z), 0x07060302u);
+        u32x2* dst = reinterpret_cast<u32x2*>(keys + (q << 2));
         if (NT)
-            __builtin_nontemporal_store(o, dst);
+            __builtin_nontemporal_store(k, dst);
         else
-            *dst = o;
+            *dst = k;
     }
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
@@ -374,21 +383,21 @@ __device__ __forceinline__ void norm_max_tile(const float* __restrict__ g, int64
 template <int ROWS, bool NT, bool ONE>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void k_norm_max(const float* __restrict__ g, int64_t d, int32_t M,
                                                      int64_t ldg, int64_t ntiles, double* __restrict__ part,
-                                                     float* __restrict__ amax)
+                                                     uint16_t* __restrict__ keys)
 {
     __shared__ f32x4 wave_max[4][kBlock];
     if (ONE) {
         const int64_t t = blockIdx.x;
         if (t < ntiles)
-            norm_max_tile<ROWS, NT>(g, d, M, ldg, ntiles, t, part, amax, wave_max);
+            norm_max_tile<ROWS, NT>(g, d, M, ldg, ntiles, t, part, keys, wave_max);
         else if (t == ntiles)
-            norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, amax);
+            norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, keys);
         return;
     }
     for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x)
-        norm_max_tile<ROWS, NT>(g, d, M, ldg, ntiles, t, part, amax, wave_max);
+        norm_max_tile<ROWS, NT>(g, d, M, ldg, ntiles, t, part, keys, wave_max);
     if (blockIdx.x == gridDim.x - 1)
-        norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, amax);
+        norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, keys);
 }
 
 // Block (b, m) sums part[m][b * span .. min(n, (b + 1) * span)) in a fixed
@@ -424,30 +433,27 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
             (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
 }
 
-// k_index_max: a block covers kIndexTile quads (8 per thread: quads t,
-// t + 256, ..., so each load and store of a wave is contiguous), all loaded
-// before W is formed.  The per-coordinate rule compares thresholds instead of
-// forming products: a -> RN32(a * inv_k) is non-decreasing for inv_k > 0, so
-// RN32(a * inv_k) <= s_0 holds exactly for a <= T_k, the largest binary32
-// that passes; each block finds T_k once (a few ulp steps from s_0 / inv_k).
-// The count #{k : a <= T_k} then needs no loop over k when no binade holds
-// two thresholds (scales at least about twice apart, as 16^k): every T_k in a
-// higher binade than a's counts, none in a lower one, so a table over the 256
-// values of the exponent field gives the count above a's binade and the one
-// threshold inside it, and a coordinate costs one lookup and one compare.
-// Otherwise the block counts with K compares per coordinate.
-constexpr int kIndexQuads = 8;
-constexpr int64_t kIndexTile = kIndexQuads * kBlock;
+// k_index_max: a block covers kIndexTile octets of coordinates (4 per
+// thread: octets t, t + 256, ..., so each load and store of a wave is
+// contiguous), all loaded before W is formed.  The norm pass keeps, for each
+// coordinate, the top 16 bits of its largest usable |g| over the rows (a
+// key: the exponent field and 7 mantissa bits).  The per-coordinate rule
+// compares thresholds instead of forming products: a -> RN32(a * inv_k) is
+// non-decreasing for inv_k > 0, so RN32(a * inv_k) <= s_0 holds exactly for
+// a <= T_k, the largest binary32 that passes; each block finds T_k once (a
+// few ulp steps from s_0 / inv_k).  A key below T_k's key means a < T_k, a
+// key above it a > T_k; only a key equal to T_k's leaves the comparison open,
+// and then the coordinate's rows are read again for its exact maximum (at
+// the scales used here, one coordinate in several thousand).  The count
+// #{k : a <= T_k} needs no loop over k when no binade holds two thresholds
+// (scales at least about twice apart, as 16^k): every T_k in a higher binade
+// than a's counts, none in a lower one, so a table over the 256 values of the
+// exponent field gives the count above a's binade and the key of the one
+// threshold inside it, and a coordinate costs one lookup and two compares.
+// Otherwise the block compares each key with the K thresholds' keys.
+constexpr int kIndexOcts = 4;
+constexpr int64_t kIndexTile = kIndexOcts * kBlock;
 static_assert(kBlock == 256, "the exponent table has one entry per thread");
-
-// Index of a >= 0 from the block's exponent table: entry e holds the one
-// threshold whose exponent field is e (or -1, which nothing passes) and the
-// index that a coordinate of binade e gets when it does not pass it.
-__device__ __forceinline__ uint32_t index_from_table(const uint2* tab, float a)
-{
-    const uint2 t = tab[__builtin_amdgcn_ubfe(__builtin_bit_cast(uint32_t, a), 23, 8)];
-    return t.y + (a <= __builtin_bit_cast(float, t.x) ? 1u : 0u);
-}
 
 // Largest binary32 a >= 0 with RN32(a * inv) <= s0, for 0 < inv; 0 when inv
 // is infinite (then no positive a passes).
@@ -479,20 +485,74 @@ __device__ __forceinline__ uint32_t index_from_count(float amax, int32_t count, 
     return static_cast<uint32_t>(count > 0 ? count - 1 : 0);
 }
 
-__global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ amax, int64_t d, int32_t M,
-                                                      const double* __restrict__ rows, float* __restrict__ wptr,
-                                                      ScaleSet S, uint8_t* __restrict__ idx)
+// The index of coordinate i from its exact maximum over the rows (the value
+// whose key the norm pass kept); M <= kFuseRows.  Rows past M re-read row
+// M - 1 (no change to the maximum), so that the loads carry no branch and
+// all are in flight at once.
+__device__ __forceinline__ uint32_t index_exact(const float* __restrict__ g, int64_t ldg, int32_t M, int64_t i,
+                                             const float* thr, int32_t K)
+{
+    float v[kFuseRows];
+#pragma unroll
+    for (int m = 0; m < kFuseRows; ++m)
+        v[m] = g[static_cast<int64_t>(m < M ? m : M - 1) * ldg + i];
+    float a = 0.0f;
+#pragma unroll
+    for (int m = 0; m < kFuseRows; ++m)
+        a = fmaxf(a, usable_or_zero(v[m]));
+    int32_t count = 0;
+    for (int k = 0; k < K; ++k)
+        count += a <= thr[k] ? 1 : 0;
+    return index_from_count(a, count, K, false);
+}
+
+// Index of the coordinate with key `key` from the exponent table (entry e:
+// the index when the key is not below the limit key of binade e, and that
+// key; binades without a threshold hold 0x10000, which every key is below,
+// with their index lowered by one); `tie` collects a key equal to the limit's.
+__device__ __forceinline__ uint32_t index_from_key(const uint2* tab, uint32_t key, bool& tie)
+{
+    const uint2 t = tab[key >> 7];
+    tie |= key == t.y;
+    return t.x + (key < t.y ? 1u : 0u);
+}
+
+// The same from the K thresholds' keys (binades that hold two thresholds).
+__device__ __forceinline__ uint32_t index_from_keys(const uint32_t* hk, int32_t K, uint32_t key, bool& tie)
+{
+    int32_t count = 0;
+    for (int k = 0; k < K; ++k) {
+        count += key < hk[k] ? 1 : 0;
+        tie |= key == hk[k];
+    }
+    return static_cast<uint32_t>(count > 0 ? count - 1 : 0);
+}
+
+// Key c of an octet's eight (two per 32-bit word, the lower coordinate in
+// the low half).
+__device__ __forceinline__ uint32_t octet_key(const u32x4& kv, int c)
+{
+    const uint32_t w = c < 2 ? kv.x : c < 4 ? kv.y : c < 6 ? kv.z : kv.w;
+    return (c & 1) ? w >> 16 : w & 0xFFFFu;
+}
+
+__global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict__ keys,
+                                                      const float* __restrict__ g, int64_t ldg, int64_t d,
+                                                      int32_t M, const double* __restrict__ rows,
+                                                      float* __restrict__ wptr, ScaleSet S,
+                                                      uint8_t* __restrict__ idx)
 {
     __shared__ float thr_s[kMaxScales];
+    __shared__ uint32_t hk_s[kMaxScales];
     __shared__ uint2 tab_s[256];
-    const int64_t nquad = d >> 2;
+    const int64_t noct = d >> 3;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kIndexTile;
     const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kIndexTile;
-    f32x4 a[kIndexQuads];
+    u32x4 kv[kIndexOcts];
 #pragma unroll
-    for (int j = 0; j < kIndexQuads; ++j) {
-        const int64_t q = tile0 + threadIdx.x + kBlock * j;
-        a[j] = q < nquad ? load_nt(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int j = 0; j < kIndexOcts; ++j) {
+        const int64_t o = tile0 + threadIdx.x + kBlock * j;
+        kv[j] = o < noct ? load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3))) : u32x4{0u, 0u, 0u, 0u};
     }
 
     // W = RN32(sqrt(max_m S_m)), NaN if any S_m is NaN (as k_finish): lane m
@@ -512,103 +572,127 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const float* __restrict__ 
     const float s0 = S.s[0];
     const int32_t K = S.K;
     const bool zero = zero_path(W, div_rn32(s0, W));
-    if (threadIdx.x < K)
-        thr_s[threadIdx.x] = zero ? 0.0f : index_threshold(div_rn32(S.s[threadIdx.x], W), s0);
+    if (threadIdx.x < K) {
+        const float t = zero ? 0.0f : index_threshold(div_rn32(S.s[threadIdx.x], W), s0);
+        thr_s[threadIdx.x] = t;
+        hk_s[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 16;
+    }
     __syncthreads();
     // thread e forms the table's entry e: the thresholds in higher binades
-    // (all of them pass), the one in binade e; on the zero path, and for the
-    // non-finite binade, every coordinate gets K - 1
+    // (every key of binade e is below theirs), the one in binade e; on the
+    // zero path every coordinate gets K - 1
     int crowded = 0;
     {
         const uint32_t e = threadIdx.x;
         int32_t above = 0, inside = 0;
-        float tin = -1.0f;
+        uint32_t kin = 0u;
         for (int k = 0; k < K; ++k) {
-            const float t = thr_s[k];
-            const uint32_t be = __builtin_bit_cast(uint32_t, t) >> 23;
+            const uint32_t be = __builtin_bit_cast(uint32_t, thr_s[k]) >> 23;
             above += be > e ? 1 : 0;
             if (be == e) {
                 ++inside;
-                tin = t;
+                kin = hk_s[k];
             }
         }
         uint2 ent;
-        if (zero || e == 255) {
-            ent.x = __builtin_bit_cast(uint32_t, -1.0f);
-            ent.y = static_cast<uint32_t>(K - 1);
+        if (zero) {
+            ent.x = static_cast<uint32_t>(K - 2);
+            ent.y = 0x10000u;
         } else {
-            // #{k : a <= T_k} - 1 = above - 1 + [a <= tin]; with nothing
-            // above, index 0 either way
+            // #{k : a <= T_k} - 1 = above - 1 + [key below kin]; with nothing
+            // above, index 0 either way (nor does a tie matter then)
             crowded = inside > 1 ? 1 : 0;
-            ent.x = __builtin_bit_cast(uint32_t, above > 0 ? tin : -1.0f);
-            ent.y = static_cast<uint32_t>(above > 0 ? above - 1 : 0);
+            const bool limit = inside > 0 && above > 0;
+            ent.x = static_cast<uint32_t>(above > 0 ? above - 1 : 0) - (limit ? 0u : 1u);
+            ent.y = limit ? kin : 0x10000u;
         }
         tab_s[e] = ent;
     }
     const bool by_table = __syncthreads_or(crowded) == 0;
 
-    for (int64_t t0 = tile0; t0 < nquad; t0 += stride) {
+    for (int64_t t0 = tile0; t0 < noct; t0 += stride) {
         if (t0 != tile0) {
 #pragma unroll
-            for (int j = 0; j < kIndexQuads; ++j) {
-                const int64_t q = t0 + threadIdx.x + kBlock * j;
-                a[j] = q < nquad ? load_nt(amax + (q << 2)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int j = 0; j < kIndexOcts; ++j) {
+                const int64_t o = t0 + threadIdx.x + kBlock * j;
+                kv[j] = o < noct ? load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3)))
+                                 : u32x4{0u, 0u, 0u, 0u};
             }
         }
+        uint32_t ties = 0u;  // octets j holding a key equal to a threshold's
         if (by_table) {
 #pragma unroll
-            for (int j = 0; j < kIndexQuads; ++j) {
-                const int64_t q = t0 + threadIdx.x + kBlock * j;
-                if (q < nquad) {
-                    const uint32_t packed = index_from_table(tab_s, a[j].x) |
-                                            (index_from_table(tab_s, a[j].y) << 8) |
-                                            (index_from_table(tab_s, a[j].z) << 16) |
-                                            (index_from_table(tab_s, a[j].w) << 24);
-                    *reinterpret_cast<uint32_t*>(idx + (q << 2)) = packed;
+            for (int j = 0; j < kIndexOcts; ++j) {
+                const int64_t o = t0 + threadIdx.x + kBlock * j;
+                if (o >= noct)
+                    continue;
+                const uint32_t k8[8] = {kv[j].x & 0xFFFFu, kv[j].x >> 16, kv[j].y & 0xFFFFu, kv[j].y >> 16,
+                                        kv[j].z & 0xFFFFu, kv[j].z >> 16, kv[j].w & 0xFFFFu, kv[j].w >> 16};
+                uint32_t ix[8];
+                bool tie = false;
+#pragma unroll
+                for (int c = 0; c < 8; ++c)
+                    ix[c] = index_from_key(tab_s, k8[c], tie);
+                u32x2 packed;
+                packed.x = ix[0] | (ix[1] << 8) | (ix[2] << 16) | (ix[3] << 24);
+                packed.y = ix[4] | (ix[5] << 8) | (ix[6] << 16) | (ix[7] << 24);
+                *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
+                ties |= tie ? 1u << j : 0u;
+            }
+        } else {
+            // binades holding two thresholds (unusual scale sets): the keys
+            // again from memory, one octet at a time
+#pragma unroll 1
+            for (int j = 0; j < kIndexOcts; ++j) {
+                const int64_t o = t0 + threadIdx.x + kBlock * j;
+                if (o >= noct)
+                    continue;
+                const u32x4 kj = load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3)));
+                u32x2 packed = {0u, 0u};
+                bool tie = false;
+#pragma unroll 1
+                for (int c = 0; c < 8; ++c) {
+                    const uint32_t v = index_from_keys(hk_s, K, octet_key(kj, c), tie);
+                    if (c < 4)
+                        packed.x |= v << (8 * c);
+                    else
+                        packed.y |= v << (8 * (c - 4));
                 }
-            }
-            continue;
-        }
-        int32_t cnt[kIndexQuads][4];
-#pragma unroll
-        for (int j = 0; j < kIndexQuads; ++j)
-            cnt[j][0] = cnt[j][1] = cnt[j][2] = cnt[j][3] = 0;
-        for (int k = 0; k < K; ++k) {
-            const float t = thr_s[k];
-#pragma unroll
-            for (int j = 0; j < kIndexQuads; ++j) {
-                cnt[j][0] += a[j].x <= t ? 1 : 0;
-                cnt[j][1] += a[j].y <= t ? 1 : 0;
-                cnt[j][2] += a[j].z <= t ? 1 : 0;
-                cnt[j][3] += a[j].w <= t ? 1 : 0;
+                *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
+                ties |= tie ? 1u << j : 0u;
             }
         }
-#pragma unroll
-        for (int j = 0; j < kIndexQuads; ++j) {
-            const int64_t q = t0 + threadIdx.x + kBlock * j;
-            if (q < nquad) {
-                const uint32_t packed = index_from_count(a[j].x, cnt[j][0], K, zero) |
-                                        (index_from_count(a[j].y, cnt[j][1], K, zero) << 8) |
-                                        (index_from_count(a[j].z, cnt[j][2], K, zero) << 16) |
-                                        (index_from_count(a[j].w, cnt[j][3], K, zero) << 24);
-                *reinterpret_cast<uint32_t*>(idx + (q << 2)) = packed;
+        // keys equal to a threshold's (rare): those coordinates' indices again
+        // from their exact maxima, over the index bytes just stored
+        while (ties != 0u) {
+            const int j = __builtin_ctz(ties);
+            ties &= ties - 1u;
+            const int64_t o = t0 + threadIdx.x + kBlock * j;
+            const u32x4 kj = load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3)));
+#pragma unroll 1
+            for (int c = 0; c < 8; ++c) {
+                bool tc = false;
+                const uint32_t key = octet_key(kj, c);
+                if (by_table)
+                    index_from_key(tab_s, key, tc);
+                else
+                    index_from_keys(hk_s, K, key, tc);
+                if (tc)
+                    idx[(o << 3) + c] = static_cast<uint8_t>(index_exact(g, ldg, M, (o << 3) + c, thr_s, K));
             }
         }
     }
-    const int64_t t = (nquad << 2) + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    // the d % 8 trailing coordinates: threads of block 0
+    const int64_t t = (noct << 3) + threadIdx.x;
     if (blockIdx.x == 0 && t < d) {
-        const float x = amax[t];
-        if (by_table) {
-            idx[t] = static_cast<uint8_t>(index_from_table(tab_s, x));
-        } else {
-            int32_t count = 0;
-            for (int k = 0; k < K; ++k)
-                count += x <= thr_s[k] ? 1 : 0;
-            idx[t] = static_cast<uint8_t>(index_from_count(x, count, K, zero));
-        }
+        bool tie = false;
+        const uint32_t key = keys[t];
+        uint32_t v = by_table ? index_from_key(tab_s, key, tie) : index_from_keys(hk_s, K, key, tie);
+        if (tie)
+            v = index_exact(g, ldg, M, t, thr_s, K);
+        idx[t] = static_cast<uint8_t>(v);
     }
 }
-
 // ---------------------------------------------------------------------------
 // Quantisation.  One thread handles a group of 8 consecutive coordinates,
 // which is exactly one Philox block: its eight 16-bit halves are the high
@@ -1041,8 +1125,6 @@ struct DeqArgs {
 // 0.55 GB of sums), 1.7% slower at ResNet-18 size (45 MB).
 constexpr int64_t kSumNontemporalBytes = int64_t(64) << 20;
 
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // The 16 BITS-bit fields starting at p (16-byte aligned for BITS = 8, 8-byte
 // for 4, 4-byte for 2).
@@ -1564,20 +1646,20 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         double* part = static_cast<double*>(ws);
         double* sub = reinterpret_cast<double*>(static_cast<char*>(ws) + L.sub_off);
         double* rows = reinterpret_cast<double*>(static_cast<char*>(ws) + L.rows_off);
-        float* amax = reinterpret_cast<float*>(static_cast<char*>(ws) + L.amax_off);
+        uint16_t* keys = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + L.keys_off);
         const dim3 grid(one_shot(plan.ntiles + 1, 1));
         // maxima beyond twice the 256 MB Infinity Cache are stored
         // nontemporally (the index pass cannot find them there anyway)
-        const bool nt = 4 * d > kMaximaNontemporalBytes;
+        const bool nt = 2 * d > kMaximaNontemporalBytes;
         const bool one = static_cast<int64_t>(grid.x) >= plan.ntiles + 1;
 #define UQ_LAUNCH_NORM_MAX_(R, NT)                                                                                \
     do {                                                                                                          \
         if (one)                                                                                                  \
             hipLaunchKernelGGL((k_norm_max<R, NT, true>), grid, dim3(kBlock), 0, stream, g, d, M, ldg,            \
-                               plan.ntiles, part, amax);                                                          \
+                               plan.ntiles, part, keys);                                                          \
         else                                                                                                      \
             hipLaunchKernelGGL((k_norm_max<R, NT, false>), grid, dim3(kBlock), 0, stream, g, d, M, ldg,           \
-                               plan.ntiles, part, amax);                                                          \
+                               plan.ntiles, part, keys);                                                          \
     } while (0)
 #define UQ_LAUNCH_NORM_MAX(R)              \
     do {                                   \
@@ -1599,8 +1681,8 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
                            0, stream, part, plan.ntiles + 1, kRowsumSpan, sub);
         hipLaunchKernelGGL(k_rowsum, dim3(1, static_cast<unsigned>(M)), dim3(kBlock), 0, stream, sub, plan.nsub,
                            plan.nsub, rows);
-        const unsigned gx = one_shot((d + 3) / 4, kIndexTile);
-        hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, amax, d, M, rows, w, S, idx);
+        const unsigned gx = one_shot((d + 7) / 8, kIndexTile);
+        hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, rows, w, S, idx);
         return hipGetLastError();
     }
     double* part = static_cast<double*>(ws);

@@ -55,12 +55,12 @@ inline FusedPlan fused_plan(int64_t d)
 
 // Workspace of the fused path, in bytes from the start of the workspace:
 // tile partials [M][ntiles + 1] fp64, their sums [M][nsub] fp64, row sums
-// [M] fp64, row maxima [d] fp32 followed by one spare quad (padding; nothing
-// is stored there).
+// [M] fp64, the row maxima's 16-bit keys [d] followed by one spare quad
+// (padding; nothing is stored there).
 struct FusedLayout {
     size_t sub_off;
     size_t rows_off;
-    size_t amax_off;
+    size_t keys_off;
     size_t bytes;
 };
 
@@ -75,8 +75,8 @@ inline FusedLayout fused_layout(int64_t d, int32_t M)
     FusedLayout L;
     L.sub_off = align256(static_cast<size_t>(M) * static_cast<size_t>(p.ntiles + 1) * sizeof(double));
     L.rows_off = L.sub_off + align256(static_cast<size_t>(M) * static_cast<size_t>(p.nsub) * sizeof(double));
-    L.amax_off = L.rows_off + align256(static_cast<size_t>(M) * sizeof(double));
-    L.bytes = L.amax_off + align256(static_cast<size_t>((d + 3) / 4 * 4 + 4) * sizeof(float));
+    L.keys_off = L.rows_off + align256(static_cast<size_t>(M) * sizeof(double));
+    L.bytes = L.keys_off + align256(static_cast<size_t>((d + 3) / 4 * 4 + 4) * sizeof(uint16_t));
     return L;
 }
 

@@ -66,11 +66,11 @@ def test_strerror_and_workspace():
         b = uq.uq_workspace_bytes(d, M)
         assert b % 256 == 0 and b >= 8 * M
         if 2 <= M <= 16:
-            # several scales with 2 to 16 rows: d fp32 row maxima, one fp64
-            # partial per row and 1024 coordinates, their sums per 16384
-            # partials, and M row sums
+            # several scales with 2 to 16 rows: d 16-bit keys of the row
+            # maxima, one fp64 partial per row and 1024 coordinates, their
+            # sums per 16384 partials, and M row sums
             tiles = -(-d // 1024)
-            assert 4 * d <= b <= 4 * d + 8 * M * (tiles + -(-tiles // 16384) + 1) + 5 * 256
+            assert 2 * d <= b <= 2 * d + 8 * M * (tiles + -(-tiles // 16384) + 1) + 5 * 256
         else:
             assert b <= 8 * M * 1024 + 256
     assert uq.uq_workspace_bytes(2 ** 30, 17) <= 17 * 1024 * 8 + 256
@@ -133,9 +133,10 @@ def status_noalloc(g=A, d=100, M=2, ldg=128, scales=S127, K=1, w=A, idx=A):
     (dict(w=A + 2), "align"), (dict(K=0), "range"), (dict(K=2, scales=[3.0, 3.0]), "range"),
     (dict(K=2, scales=S4[:2], idx=None), "inval"), (dict(K=2, scales=S4[:2], idx=A + 1), "align"),
     (dict(K=2, scales=None), "inval"),
-    # beyond the static scratch: the row maxima of 20 million coordinates
-    # (several scales, 8 rows), or 8 KiB of norm partials for each of 9000 rows
-    (dict(d=20_000_000, ldg=20_000_000, M=8, K=4, scales=S4), "ws"),
+    # beyond the static scratch: the row maxima's keys of 40 million
+    # coordinates (several scales, 8 rows), or 8 KiB of norm partials for each
+    # of 9000 rows
+    (dict(d=40_000_000, ldg=40_000_000, M=8, K=4, scales=S4), "ws"),
     (dict(d=1 << 30, ldg=1 << 30, M=9000), "ws"),
 ])
 def test_shared_scale_noalloc_rejects(kw, want):
@@ -149,7 +150,7 @@ def test_shared_scale_noalloc_limit_is_the_header_s():
     m = re.search(r"#define UQ_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
     assert m and int(m.group(1)) << int(m.group(2)) == uq.UQ_NOALLOC_SCRATCH_BYTES == 64 << 20
     # the same sizes with a workspace argument are accepted by the checks
-    need = uq.uq_workspace_bytes(20_000_000, 8)
+    need = uq.uq_workspace_bytes(40_000_000, 8)
     assert need > uq.UQ_NOALLOC_SCRATCH_BYTES
 
 
@@ -157,10 +158,10 @@ def test_shared_scale_noalloc_limit_is_the_header_s():
 def test_shared_scale_needs_the_full_workspace(M):
     """The workspace of uq_workspace_bytes(d, M) covers any K; one 256-byte
     line less is refused before anything is launched (with 2 to 16 rows the
-    size includes the 4 d bytes of row maxima of the fused pass)."""
+    size includes the 2 d bytes of the row maxima's keys of the fused pass)."""
     d = 100_003
     need = uq.uq_workspace_bytes(d, M)
-    assert (need >= 4 * d) == (2 <= M <= 16)
+    assert (need >= 2 * d) == (2 <= M <= 16)
     for K, scales, idx in ((1, S127, A), (4, S4, A)):
         assert status_shared(d=d, M=M, ldg=100_032, scales=scales, K=K, idx=idx, ws_bytes=need - 256) == E["ws"]
 

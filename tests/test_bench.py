@@ -26,13 +26,13 @@ def test_step_bytes_per_coordinate(M):
     assert per_coord(M, 1) == 10 * M + 8
     # several scales: the index read once by the quantiser and once by the
     # sum's reconstruction; with 2 to 16 workers the norm pass also writes the
-    # row maxima the index pass reads
-    want = 10 * M + 19 if 2 <= M <= bench.FUSED_MAX_ROWS else 14 * M + 11
+    # row maxima's 16-bit keys, which the index pass reads
+    want = 10 * M + 15 if 2 <= M <= bench.FUSED_MAX_ROWS else 14 * M + 11
     assert per_coord(M, 4) == want
     # all rows quantised and summed in one fused call: the gradients and the
     # index in, the sums and the output out
     assert per_coord(M, 1, quant_sum=True) - 4 * M == 4 * M + 8
-    assert per_coord(M, 4, quant_sum=True) == want - (10 * M + 19 - (8 * M + 18) if 2 <= M <= 16 else
+    assert per_coord(M, 4, quant_sum=True) == want - (10 * M + 15 - (8 * M + 14) if 2 <= M <= 16 else
                                                       14 * M + 11 - (12 * M + 10))
 
 
@@ -48,8 +48,8 @@ def test_streamed_bytes():
     # sums; the last also writes the output
     f = bench.algorithmic_bytes(d, M, K, True, quant_sum=True)
     assert f["quant_sum_first"] == 9 * d and f["quant_sum"] == (M - 2) * 13 * d and f["quant_sum_last"] == 17 * d
-    # the whole step: norm + maxima 4M + 4, index 4 + 1, then 9 + 13 (M - 2) + 17
-    assert per_coord(M, K, True, quant_sum=True) == 17 * M + 9
+    # the whole step: norm + maxima keys 4M + 2, index 2 + 1, then 9 + 13 (M - 2) + 17
+    assert per_coord(M, K, True, quant_sum=True) == 17 * M + 5
     assert per_coord(1, K, True, quant_sum=True) == per_coord(1, K, False, quant_sum=True)
 
 

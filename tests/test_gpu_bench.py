@@ -75,7 +75,7 @@ def test_default_bench_line():
     assert (cfg["workload"], cfg["d"], cfg["M"], len(cfg["scales"]), cfg["streamed"]) == \
         ("student-t", 1 << 30, 16, 8, True)
     assert cfg["path"] == "quantise-and-sum fused"
-    assert j["step_bytes"] == (17 * 16 + 9) * (1 << 30)
+    assert j["step_bytes"] == (17 * 16 + 5) * (1 << 30)
     check_roofline(j, 0.85, 1.15)
     assert j["roofline"]["stage"] == "quant_sum" and j["roofline"]["launches_per_step"] == 14
     assert j["cpu_baseline"]["one_core"]["value"] > 0

@@ -2,8 +2,8 @@
 cannot allocate device memory, through the C ABI: the same W (bit for bit)
 and the same shared scale index as uq_shared_scale with a workspace, on two
 calls in a row (the second with a smaller input, on the same static scratch)
-for one scale, for several scales with 2 to 16 rows (the row maxima in the
-scratch), with more than 16 rows and with one row; W within one binary32 ulp
+for one scale, for several scales with 2 to 16 rows (the row maxima's keys
+in the scratch), with more than 16 rows and with one row; W within one binary32 ulp
 of the oracle's and the index equal to the oracle's given that W.
 """
 import numpy as np
@@ -50,11 +50,11 @@ def check_oracle(host, d, scales, W, idx):
 
 
 # (rows, first d, second d, scales): one scale; several scales with 2 to 16
-# rows (the fused pass, whose row maxima fill most of the scratch at the
-# first size); more than 16 rows; one row
+# rows (the fused pass, whose row maxima's keys fill most of the scratch at
+# the first size); more than 16 rows; one row
 CASES = [
     (8, 3_000_017, 1_000_003, [127.0]),
-    (8, 16_000_000, 2_500_001, synth.scales_for(8, 4)),
+    (8, 32_000_000, 2_500_001, synth.scales_for(8, 4)),
     (16, 4_000_037, 65_539, synth.scales_for(4, 4)),
     (17, 1_000_003, 10_007, synth.scales_for(8, 4)),
     (1, 777_777, 4_097, synth.scales_for(8, 8)),
@@ -85,7 +85,7 @@ def test_noalloc_small_and_empty_inputs():
 
 
 def test_noalloc_beyond_the_limit_is_refused_and_launches_nothing():
-    d, M = 17_000_000, 8
+    d, M = 34_000_000, 8
     # whole buffers, although the call is refused before any launch
     g = torch.zeros((M, d), device=DEV)
     w = torch.full((4,), 9.0, device=DEV)
