@@ -253,9 +253,10 @@ __device__ __forceinline__ void sync_lds()
 // w, w + 4, ... (ROWS / 4 of them; rows past M re-read row M - 1 and are not
 // accumulated): lane l loads quads l, l + 64, l + 128, l + 192 of the tile from
 // each of its rows (4 KiB per row per wave), all loads issued at once.  The
-// waves' maxima meet in LDS and leave as one coalesced store; each row's
-// squares leave as one fp64 partial per tile.  Measured at 2^30 coordinates
-// and 16 rows (MI355X): 12.3 ms (0.74 of 8 TB/s) in a probe of this form,
+// waves' maxima meet in LDS and leave as one coalesced store of their 16-bit
+// keys; each row's squares leave as one fp64 partial per tile.  Measured at
+// 2^30 coordinates and 16 rows (MI355X), with fp32 maxima then: 12.3 ms
+// (0.74 of 8 TB/s) in a probe of this form,
 // against 13.8 ms for blocks that loop over 16 tiles with the next tile's
 // loads issued before the current tile's store, and 12.8-13.8 ms for every
 // looping form tried (double-buffered, no prefetch, 8 waves of 2 rows,
@@ -1631,11 +1632,11 @@ static unsigned one_shot(int64_t units, int64_t per_block)
     return static_cast<unsigned>(blocks);
 }
 
-// The fused pass stores the row maxima nontemporally when they exceed this
-// many bytes: measured 2.4% faster at VGG-16 size (553 MB) and 3.2% at
-// 2^30 coordinates, 6% slower at ResNet-50 size (102 MB), where the index
-// pass reads them back from the 256 MB Infinity Cache.
-constexpr int64_t kMaximaNontemporalBytes = int64_t(512) << 20;
+// The fused pass stores the row maxima's keys nontemporally when they exceed
+// this many bytes: measured 5% faster (the shared scale) at VGG-16 size
+// (277 MB of keys), 3% slower at ResNet-50 size (51 MB), where the index pass
+// reads them back from the 256 MB Infinity Cache.
+constexpr int64_t kMaximaNontemporalBytes = int64_t(128) << 20;
 
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
                                float* w, uint8_t* idx, void* ws, hipStream_t stream)
@@ -1648,8 +1649,8 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         double* rows = reinterpret_cast<double*>(static_cast<char*>(ws) + L.rows_off);
         uint16_t* keys = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + L.keys_off);
         const dim3 grid(one_shot(plan.ntiles + 1, 1));
-        // maxima beyond twice the 256 MB Infinity Cache are stored
-        // nontemporally (the index pass cannot find them there anyway)
+        // keys beyond half the 256 MB Infinity Cache are stored
+        // nontemporally (the index pass would not find them there)
         const bool nt = 2 * d > kMaximaNontemporalBytes;
         const bool one = static_cast<int64_t>(grid.x) >= plan.ntiles + 1;
 #define UQ_LAUNCH_NORM_MAX_(R, NT)                                                                                \
