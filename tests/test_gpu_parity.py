@@ -312,14 +312,16 @@ def test_index_at_scale_boundaries(M):
     assert len(set(ref["idx"][100:col:7].tolist())) >= 3
 
 
+@pytest.mark.parametrize("cap", [0, 8], ids=["one-shot", "capped"])
 @pytest.mark.parametrize("M", [2, 8, 16])
-def test_many_maxima_in_a_thresholds_key_bucket(M):
+def test_many_maxima_in_a_thresholds_key_bucket(M, cap):
     """With several scales and 2 to 16 rows the index pass reads the row
     maxima and compares each with the scales' limits: thousands of
     coordinates placed within 2^-9 (relative) of the limits (at most 150 per
     row near W/16, so that a one-hot row still sets W), in the binades where
     the pass's exponent table holds them, plus tiny denormal maxima (the
-    table's lowest binade); all against the oracle."""
+    table's lowest binade); on one-shot grids and on grids of 8 blocks; all
+    against the oracle."""
     scales = synth.scales_for(8, 4)
     Wv = np.float32(0.9)
     d = 40_000 + 13
@@ -343,7 +345,11 @@ def test_many_maxima_in_a_thresholds_key_bucket(M):
     host[0, :] = 0.0
     host[0, 0] = Wv  # a one-hot row: its norm is W
     assert np.sqrt((host.astype(np.float64) ** 2).sum(axis=1)).max() == np.float64(Wv)
-    res, _, _ = gpu_step(host, d, scales, seed=9)
+    uq.uq_set_grid_cap(cap)  # 8 blocks: the passes' grid-stride loops
+    try:
+        res, _, _ = gpu_step(host, d, scales, seed=9)
+    finally:
+        uq.uq_set_grid_cap(0)
     assert res["W"] == Wv
     ref = assert_matches_oracle(res, host, d, scales, seed=9)
     assert len(set(ref["idx"].tolist())) == len(scales)
