@@ -11,15 +11,15 @@ the 8 TB/s HBM peak the step's algorithmic bytes reach.
 The default workload is the largest that fits one GPU: d = 2^30 heavy-tailed
 (Student-t) coordinates, 16 workers streamed one at a time through a resident
 int32 sum, eight scales (Algorithm 2), each worker quantised and added into
-the sum in one fused call.
+the sum in one fused call (with resident workers, one call quantises and sums
+all rows; workloads with packed codes store them, then sum them).
 
 Prints one JSON line: the step's rate, its stages' times and shares, the
 roofline of the stage with the largest share, the oracle's rate on one core
 and on all cores over a bounded sample, and the device's results on that
 sample checked against the oracle's.  Extra modes:
   --workload NAME       another workload of synth.WORKLOADS
-  --composed            streamed workers: codes stored, then summed (two calls)
-  --quant-sum           resident workers: one fused quantise-and-sum call
+  --composed            codes stored, then summed (separate calls)
   --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
@@ -459,10 +459,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="student-t")
     ap.add_argument("--composed", action="store_true",
-                    help="streamed workers: quantise and sum in separate calls (codes through HBM) instead of "
-                         "the fused quantise-and-sum")
-    ap.add_argument("--quant-sum", action="store_true",
-                    help="resident workers: quantise and sum all rows in one fused call (no codes stored)")
+                    help="quantise and sum in separate calls (the codes through HBM) instead of the fused "
+                         "quantise-and-sum (packed-code workloads always store their codes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work to aim for, for each of the two CPU figures")
@@ -503,7 +501,9 @@ def main() -> int:
     if cfg.get("randk"):
         return bench_randk(args, g, cfg)
     bits = int(cfg.get("bits", 8))
-    quant_sum = (streamed and not args.composed) or (not streamed and args.quant_sum)
+    # int8 codes: quantised and summed in one fused call unless asked for;
+    # packed codes are stored (their packing is what those workloads show)
+    quant_sum = bits == 8 and not args.composed
     step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits, quant_sum=quant_sum)
     torch.cuda.synchronize()
 
