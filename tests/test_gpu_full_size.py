@@ -1,9 +1,10 @@
 """GPU parity at full size, every coordinate, against the oracle.
 
 The VGG-16-shaped workload (d = 138,357,544, 16 workers; one scale s = 7, and
-four scales 7 * 16^k) and the 2^30-coordinate workload (16 workers streamed
-through the fused quantise-and-sum, eight scales) in the launch configuration
-the benchmark times.  Each is compared with the oracle (Eq. (7)-(13),
+four scales 7 * 16^k, with the codes stored and, for four scales, with all
+rows through the fused quantise-and-sum the benchmark times) and the
+2^30-coordinate workload (16 workers streamed through the fused
+quantise-and-sum, eight scales).  Each is compared with the oracle (Eq. (7)-(13),
 Algorithms 1-2) over all of d, in coordinate chunks of 2^24 (every worker's
 chunk copied to the host, the oracle on the host's threads, given the
 device's W): the scale index, every worker's codes where the step keeps them,
@@ -70,15 +71,18 @@ def compare_in_chunks(step, g, d, scales, seed, with_codes):
         assert bad.size == 0, f"outputs differ at {(c0 + bad[:5]).tolist()}"
 
 
-@pytest.mark.parametrize("name", ["vgg16-single", "vgg16-multi"])
-def test_vgg16_every_coordinate(name):
+@pytest.mark.parametrize("name,quant_sum", [("vgg16-single", False), ("vgg16-multi", False), ("vgg16-multi", True)],
+                         ids=["vgg16-single", "vgg16-multi", "vgg16-multi-fused"])
+def test_vgg16_every_coordinate(name, quant_sum):
+    """The codes stored and summed, or (fused) all 16 rows quantised and
+    summed in one call with no codes stored."""
     g, cfg = synth.make_gradients(name, device=DEV)
     d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
-    step = Step(d, M, scales, device=DEV)
+    step = Step(d, M, scales, device=DEV, quant_sum=quant_sum)
     step.run(g, seed)
     torch.cuda.synchronize()
     check_norm(g, d, np.float32(step.w[0].item()))
-    compare_in_chunks(step, g, d, scales, seed, with_codes=True)
+    compare_in_chunks(step, g, d, scales, seed, with_codes=not quant_sum)
 
 
 def unpack_rows(packed, d, bits):
