@@ -12,7 +12,9 @@ The default workload is the largest that fits one GPU: d = 2^30 heavy-tailed
 (Student-t) coordinates, 16 workers streamed one at a time through a resident
 int32 sum, eight scales (Algorithm 2), each worker quantised and added into
 the sum in one fused call (with resident workers, one call quantises and sums
-all rows; workloads with packed codes store them, then sum them).
+all rows, and with several scales and at most 16 workers it also forms the
+shared scale index from the rows it holds, so the shared-scale call forms W
+only; workloads with packed codes store them, then sum them).
 
 Prints one JSON line: the step's rate, its stages' times and shares, the
 roofline of the stage with the largest share, the oracle's rate on one core
@@ -20,6 +22,9 @@ and on all cores over a bounded sample, and the device's results on that
 sample checked against the oracle's.  Extra modes:
   --workload NAME       another workload of synth.WORKLOADS
   --composed            codes stored, then summed (separate calls)
+  --index-pass          resident workers, several scales: the shared index
+                        from the shared-scale call's own pass, not formed
+                        inside the quantise-and-sum
   --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
@@ -83,7 +88,8 @@ def shared_scale_bytes(d: int, M: int, K: int) -> int:
     return 4 * M * d + 4 * M * d + d
 
 
-def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, quant_sum: bool = False) -> list:
+def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, quant_sum: bool = False,
+                index_in_pass: bool = False) -> list:
     """The library calls of one step as stages: name, the kernel it launches
     (several for the shared scale, the longest first), calls per step and the
     algorithmic bytes per call."""
@@ -91,6 +97,12 @@ def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, q
     ib = d if multi else 0
     cb = code_bytes(d, bits)
     qk = ("k_quantise_multi" if multi else "k_quantise_single") + ("" if bits == 8 else f"_{bits}bit")
+    if index_in_pass:
+        # W alone (the one-scale norm pass), then one call that reads every
+        # row, writes the index it forms, the sums and the output
+        return [dict(name="shared_scale", kernels=scale_kernels(M, 1), calls=1, bytes=shared_scale_bytes(d, M, 1)),
+                dict(name="index_quant_sum", kernels=["k_index_quant_sum"], calls=1,
+                     bytes=4 * M * d + d + 4 * d + 4 * d)]
     st = [dict(name="shared_scale", kernels=scale_kernels(M, K), calls=1, bytes=shared_scale_bytes(d, M, K))]
     if quant_sum and streamed:
         # one worker per call into the running sum; the last call reconstructs
@@ -123,11 +135,12 @@ def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, q
     return st
 
 
-def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8, quant_sum: bool = False) -> dict:
+def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8, quant_sum: bool = False,
+                      index_in_pass: bool = False) -> dict:
     """Bytes each stage must move at minimum (reads + writes) per step, and
     their total."""
     b = {}
-    for s in plan_stages(d, M, K, bits, streamed, quant_sum):
+    for s in plan_stages(d, M, K, bits, streamed, quant_sum, index_in_pass):
         b[s["name"]] = b.get(s["name"], 0) + s["calls"] * s["bytes"]
     b["total"] = sum(b.values())
     return b
@@ -434,7 +447,8 @@ def stage_fns(step, g, seed: int, M: int) -> dict:
     buffers (its inputs are the previous stage's outputs, already in place)."""
     last = M - 1
     return {
-        "shared_scale": lambda: step.shared_scale(g),
+        "shared_scale": lambda: step.shared_scale(g, w_only=step.index_in_pass),
+        "index_quant_sum": lambda: step.index_quantize_sum(g, seed),
         "quant_sum_first": lambda: step.quantize_sum(g[0:1], seed, rows=1, worker0=0, accumulate=0,
                                                      reconstruct=False),
         "quant_sum": ((lambda: step.quantize_sum(g[1:2], seed, rows=1, worker0=1, accumulate=1, reconstruct=False))
@@ -461,6 +475,9 @@ def main() -> int:
     ap.add_argument("--composed", action="store_true",
                     help="quantise and sum in separate calls (the codes through HBM) instead of the fused "
                          "quantise-and-sum (packed-code workloads always store their codes)")
+    ap.add_argument("--index-pass", action="store_true",
+                    help="resident workers with several scales: the shared index from the shared-scale call's own "
+                         "pass instead of formed inside the quantise-and-sum")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work to aim for, for each of the two CPU figures")
@@ -504,7 +521,8 @@ def main() -> int:
     # int8 codes: quantised and summed in one fused call unless asked for;
     # packed codes are stored (their packing is what those workloads show)
     quant_sum = bits == 8 and not args.composed
-    step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits, quant_sum=quant_sum)
+    step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits, quant_sum=quant_sum,
+                index_in_pass=False if args.index_pass else None)
     torch.cuda.synchronize()
 
     # -- timed region: K whole steps (host launches, or with --graph replays
@@ -525,7 +543,7 @@ def main() -> int:
     # -- per-stage times: each stage's call repeated back to back between two
     # events on the stream (mean over rounds), so host launch overhead does
     # not enter them; a stage's share of the step is calls x time per call
-    stages = plan_stages(d, M, K, bits, streamed, quant_sum)
+    stages = plan_stages(d, M, K, bits, streamed, quant_sum, step.index_in_pass)
     fns = stage_fns(step, g, seed, M)
     reps = stage_reps(args.steps, elapsed / args.steps)
     for st in stages:
@@ -559,7 +577,8 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed,
                    "quantizer": "multi" if K > 1 else "single", "streamed": streamed, "code_bits": bits,
-                   "path": "quantise-and-sum fused" if quant_sum else "codes stored, then summed",
+                   "path": ("quantise-and-sum fused, index formed in it" if step.index_in_pass
+                            else "quantise-and-sum fused" if quant_sum else "codes stored, then summed"),
                    "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
         "pct_hbm_peak": round(100 * step_bytes / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),

@@ -221,6 +221,30 @@ int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_
                     uint64_t seed, int32_t accumulate, int32_t* sum, int32_t M, float* out,
                     void* stream);
 
+/*
+ * The shared scale index of Sec. 3.2 (the rule of Eq. (11) with scale
+ * sharing) formed inside the quantise-and-sum over all M workers: Eq. (12),
+ * the all-reduce of Algorithm 2 and the reconstruction of Eq. (13) with the
+ * 1/M of the averaging step, in one pass over the gradients.  Bit for bit the
+ * idx of uq_shared_scale followed by uq_quantize_sum over all M rows
+ * (worker0 = 0, accumulate = 0, out set), given the same W.  Every row of a
+ * tile is held in registers, so each coordinate's index comes from its exact
+ * largest usable |g| over the rows; uq_shared_scale then only has to form W,
+ * which does not depend on the scales (call it with K = 1 and idx = NULL).
+ *   g        [M][ldg] fp32, 1 <= M <= 16; row m is worker m
+ *   w        device pointer to W (one fp32, read)
+ *   scales   host array of K floats, 1 <= K <= UQ_MAX_SCALES, as for
+ *            uq_quantize_multi
+ *   idx      [d] uint8 (written): k*_i in 0..K-1
+ *   sum      [d] int32 (written): the sum over the M workers' codes
+ *   out      [d] fp32 (written): the reconstruction, the rule of uq_dequantize
+ * The checks of uq_quantize_multi and uq_dequantize apply; M > 16 returns
+ * UQ_ERANGE (use uq_shared_scale and uq_quantize_sum there).
+ */
+int uq_index_quantize_sum(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
+                          const float* scales, int32_t K, uint64_t seed, uint8_t* idx,
+                          int32_t* sum, float* out, void* stream);
+
 /* ------------------------------------------------------------------------
  * Sub-byte codes.  The paper stores every code in 8 bits because its
  * framework had no narrower type, and found bit-packing too slow (Sec. 5,

@@ -62,6 +62,7 @@ def _load() -> ctypes.CDLL:
     L.uq_sum_dequantize.argtypes = [P, i64, i32, i64, i32, i32, P, i32, P, P, i32, P, P, P]
     L.uq_quantize_packed.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i64, P]
     L.uq_quantize_sum.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i32, P, P]
+    L.uq_index_quantize_sum.argtypes = [P, i64, i32, i64, P, P, i32, u64, P, P, P, P]
     L.uq_sum_packed.argtypes = [P, i64, i32, i64, i32, i32, P, P]
     L.uq_randk_workspace_bytes.argtypes = [i64, i64]
     L.uq_randk_workspace_bytes.restype = sz
@@ -76,6 +77,7 @@ def _load() -> ctypes.CDLL:
     L.uq_last_error.restype = ctypes.c_char_p
     for name in ("uq_shared_scale", "uq_shared_scale_noalloc", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
                  "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_quantize_sum",
+                 "uq_index_quantize_sum",
                  "uq_randk_select", "uq_gather",
                  "uq_scatter", "uq_set_grid_cap", "uq_set_randk_mode"):
         getattr(L, name).restype = ctypes.c_int
@@ -200,6 +202,12 @@ def uq_quantize_sum(g, d, rows, ldg, worker0, w, scales, K, idx, seed, accumulat
     hs = _host_scales(scales)
     _check(lib.uq_quantize_sum(_ptr(g), d, rows, ldg, worker0, _ptr(w), hs.ptr, K, _ptr(idx), seed, accumulate,
                                _ptr(sum), M, _ptr(out), _stream(stream)))
+
+
+def uq_index_quantize_sum(g, d, M, ldg, w, scales, K, seed, idx, sum, out, stream=None) -> None:
+    hs = _host_scales(scales)
+    _check(lib.uq_index_quantize_sum(_ptr(g), d, M, ldg, _ptr(w), hs.ptr, K, seed, _ptr(idx), _ptr(sum), _ptr(out),
+                                     _stream(stream)))
 
 
 def uq_sum_packed(packed, d, rows, ldp, bits, accumulate, sum, stream=None) -> None:

@@ -450,6 +450,26 @@ int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_
                                          static_cast<hipStream_t>(stream)));
 }
 
+int uq_index_quantize_sum(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w, const float* scales,
+                          int32_t K, uint64_t seed, uint8_t* idx, int32_t* sum, float* out, void* stream)
+{
+    uq::ScaleSet S;
+    UQ_TRY(check_scales(scales, K, &S));
+    UQ_TRY(check_dims(d, M, "M"));
+    if (M > uq::kFuseRows)
+        return fail(UQ_ERANGE, "M = %d exceeds the %d rows held in registers", M, uq::kFuseRows);
+    UQ_TRY(check_rows(g, d, M, ldg, 4, "g"));
+    UQ_TRY(check_w(w));
+    if (idx == nullptr && d > 0)
+        return fail(UQ_EINVAL, "idx is NULL");
+    UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    UQ_TRY(check_vec(sum, d, "sum"));
+    uq::ScaleSet S2;
+    UQ_TRY(check_reconstruction(d, M, w, scales, K, K > 1 ? idx : nullptr, out, &S2));
+    return launched(uq::launch_index_quant_sum(g, d, M, ldg, w, S, seed, idx, sum, out,
+                                               static_cast<hipStream_t>(stream)));
+}
+
 size_t uq_randk_workspace_bytes(int64_t d, int64_t K)
 {
     (void)d;

@@ -17,6 +17,9 @@
 //                sums, optionally with the reconstruction applied  (+ Eq. (9)/(13))
 //   k_quant_sum  the quantiser's codes added straight into the   (Eq. (8)/(12) +
 //                int32 sums, never stored (+ the reconstruction)   all-reduce)
+//   k_index_quant_sum  all of up to 16 rows held at once: the     (Eq. (11) +
+//                shared index from their exact maxima, then        sharing, (12),
+//                k_quant_sum's codes, sums and reconstruction      sum, (13))
 //   k_dequant    int32 (+ index) -> fp32                          (Eq. (9)/(13))
 //
 // Every per-coordinate result is a pure function of its inputs and the
@@ -1584,6 +1587,291 @@ __global__ __launch_bounds__(kBlock) void k_quant_sum(const float* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// The shared scale index formed inside the quantise-and-sum over all M <=
+// kFuseRows rows (Sec. 3.2: Eq. (11) with scale sharing, then Eq. (12), the
+// sum and Eq. (13)).  One wave per 512-coordinate tile, as k_quant_sum, but
+// every row of the tile is loaded at once and held in registers: a
+// coordinate's index comes from its exact largest usable |g| over the rows,
+// and the rows are then quantised from registers, so neither the rows'
+// maxima nor an index pass over them is needed.  The index uses the
+// thresholds T_k of k_index_max (#{k : a <= T_k} - 1): when no binade holds
+// two thresholds, a table over the exponent field gives, for binade e, the
+// count above it and the bits of the one threshold inside it, and since the
+// bits of non-negative binary32 values order like the values, a coordinate
+// costs one lookup and one integer compare, exact with no ties to resolve.
+// ROWS is M rounded up to a power of two; rows past M re-read row M - 1
+// (no change to the maximum, no branch on the loads) and are not quantised.
+// ---------------------------------------------------------------------------
+// max(m, |x|, |y|) in one instruction (v_maximum3_f32, the absolute values
+// by source modifiers).  This maximum propagates NaN: the result is NaN if
+// any operand is, else infinite if any operand is, else the largest finite
+// value, so a running maximum that stays finite saw finite values only.
+__device__ __forceinline__ float max3_abs(float m, float x, float y)
+{
+    return __builtin_elementwise_maximum(m, __builtin_elementwise_maximum(fabsf(x), fabsf(y)));
+}
+
+template <int ROWS, bool PRE, bool NT>
+__device__ __forceinline__ void index_quant_sum_tile(const f32x4 (&A)[ROWS], const f32x4 (&B)[ROWS], int32_t M,
+                                                     int64_t T, const uint2* tab, bool by_table, const float* thr,
+                                                     int32_t K, bool zero, const float* inv_t, float s0x,
+                                                     const float* deq_t, uint32_t key0, uint32_t key1, uint32_t one2,
+                                                     uint8_t* __restrict__ idx, int32_t* __restrict__ sum,
+                                                     float* __restrict__ out)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t a_off = (T << 9) + 4 * lane;
+    // the largest |g| over the rows, two rows per instruction; a result that
+    // is not finite means some value was not usable (infinite or NaN), and
+    // then the lane forms the largest usable |g| value by value
+    float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    static_assert(ROWS % 2 == 0, "rows are taken in pairs");
+#pragma unroll
+    for (int r = 0; r < ROWS; r += 2) {
+        a[0] = max3_abs(a[0], A[r].x, A[r + 1].x);
+        a[1] = max3_abs(a[1], A[r].y, A[r + 1].y);
+        a[2] = max3_abs(a[2], A[r].z, A[r + 1].z);
+        a[3] = max3_abs(a[3], A[r].w, A[r + 1].w);
+        a[4] = max3_abs(a[4], B[r].x, B[r + 1].x);
+        a[5] = max3_abs(a[5], B[r].y, B[r + 1].y);
+        a[6] = max3_abs(a[6], B[r].z, B[r + 1].z);
+        a[7] = max3_abs(a[7], B[r].w, B[r + 1].w);
+    }
+    uint32_t worst = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        worst = max(worst, __float_as_uint(a[j]));
+    if (__builtin_expect(worst >= 0x7F800000u, 0)) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            a[j] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            a[0] = fmaxf(a[0], usable_or_zero(A[r].x));
+            a[1] = fmaxf(a[1], usable_or_zero(A[r].y));
+            a[2] = fmaxf(a[2], usable_or_zero(A[r].z));
+            a[3] = fmaxf(a[3], usable_or_zero(A[r].w));
+            a[4] = fmaxf(a[4], usable_or_zero(B[r].x));
+            a[5] = fmaxf(a[5], usable_or_zero(B[r].y));
+            a[6] = fmaxf(a[6], usable_or_zero(B[r].z));
+            a[7] = fmaxf(a[7], usable_or_zero(B[r].w));
+        }
+    }
+    uint32_t k[8];
+    if (by_table) {
+        const uint32_t kzero = static_cast<uint32_t>(K - 1);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t b = __float_as_uint(a[j]);
+            const uint2 t = tab[b >> 23];
+            k[j] = b != 0u ? t.x + (b <= t.y ? 1u : 0u) : kzero;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            int32_t count = 0;
+            for (int q = 0; q < K; ++q)
+                count += a[j] <= thr[q] ? 1 : 0;
+            k[j] = index_from_count(a[j], count, K, zero);
+        }
+    }
+    const uint32_t ka = k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24);
+    const uint32_t kb = k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24);
+    uint32_t* ip = reinterpret_cast<uint32_t*>(idx + a_off);
+    if (NT) {
+        __builtin_nontemporal_store(ka, ip);
+        __builtin_nontemporal_store(kb, ip + 64);
+    } else {
+        ip[0] = ka;
+        ip[64] = kb;
+    }
+    float inv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        inv[j] = inv_t[k[j]];
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        if (r < M) {
+            const float v[8] = {A[r].x, A[r].y, A[r].z, A[r].w, B[r].x, B[r].y, B[r].z, B[r].w};
+            uint32_t p[4];
+            tile_codes<PRE>(v, inv, s0x, T, static_cast<uint32_t>(r), key0, key1, one2, p);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                h[j] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, h[j]) + __builtin_bit_cast(u16x2, p[j]));
+        }
+    }
+    int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    widen_pairs(h, acc);
+    const i32x4 sa = {acc[0], acc[1], acc[2], acc[3]};
+    const i32x4 sb = {acc[4], acc[5], acc[6], acc[7]};
+    store_sum4<NT>(sum + a_off, sa);
+    store_sum4<NT>(sum + a_off + 256, sb);
+    f32x4 oa, ob;
+    oa.x = static_cast<float>(sa.x) * deq_t[k[0]];
+    oa.y = static_cast<float>(sa.y) * deq_t[k[1]];
+    oa.z = static_cast<float>(sa.z) * deq_t[k[2]];
+    oa.w = static_cast<float>(sa.w) * deq_t[k[3]];
+    ob.x = static_cast<float>(sb.x) * deq_t[k[4]];
+    ob.y = static_cast<float>(sb.y) * deq_t[k[5]];
+    ob.z = static_cast<float>(sb.z) * deq_t[k[6]];
+    ob.w = static_cast<float>(sb.w) * deq_t[k[7]];
+    store_nt(out + a_off, oa);
+    store_nt(out + a_off + 256, ob);
+}
+
+// The coordinates past the last whole tile (fewer than 512): lane t of one
+// wave takes the 8 contiguous coordinates of group ntiles * 64 + t, forms
+// their indices from the rows' maxima (threshold counts), then quantises and
+// sums every row.  inv_s holds s_k / W (not scaled).
+__device__ __forceinline__ void index_quant_sum_tail(const float* __restrict__ g, int64_t d, int64_t ldg, int32_t M,
+                                                     int64_t ntiles, const float* thr, int32_t K, bool zero,
+                                                     const float* inv_s, float s0, uint32_t key0, uint32_t key1,
+                                                     uint8_t* __restrict__ idx, int32_t* __restrict__ sum,
+                                                     const float* deq_t, float* __restrict__ out)
+{
+    const int64_t q = (ntiles << 6) + (threadIdx.x & 63);
+    const int64_t base = q << 3;
+    if (base >= d)
+        return;
+    float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    for (int32_t r = 0; r < M; ++r) {
+        const float* row = g + static_cast<int64_t>(r) * ldg;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            a[j] = fmaxf(a[j], usable_or_zero(base + j < d ? row[base + j] : 0.0f));
+    }
+    uint32_t kk[8];
+    float inv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        int32_t count = 0;
+        for (int k = 0; k < K; ++k)
+            count += a[j] <= thr[k] ? 1 : 0;
+        kk[j] = index_from_count(a[j], count, K, zero);
+        inv[j] = inv_s[kk[j]];
+    }
+    int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int32_t r = 0; r < M; ++r) {
+        const float* row = g + static_cast<int64_t>(r) * ldg;
+        float v[8];
+        int32_t code[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            v[j] = base + j < d ? row[base + j] : 0.0f;
+        quantise_group(v, inv, s0, static_cast<uint64_t>(q), static_cast<uint32_t>(r), key0, key1, code);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc[j] += code[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (base + j < d) {
+            idx[base + j] = static_cast<uint8_t>(kk[j]);
+            sum[base + j] = acc[j];
+            out[base + j] = static_cast<float>(acc[j]) * deq_t[kk[j]];
+        }
+    }
+}
+
+template <int ROWS, bool NT>
+__global__ __launch_bounds__(kBlock) void k_index_quant_sum(const float* __restrict__ g, int64_t d, int32_t M,
+                                                            int64_t ldg, const float* __restrict__ wptr, ScaleSet S,
+                                                            uint32_t key0, uint32_t key1, uint8_t* __restrict__ idx,
+                                                            int32_t* __restrict__ sum, float* __restrict__ out)
+{
+    __shared__ float inv_s[kMaxScales];  // s_k / W
+    __shared__ float inv_p[kMaxScales];  // s_k / W * 2^16 when pre
+    __shared__ float deq_s[kMaxScales];  // RN32(W / (M s_k))
+    __shared__ float thr_s[kMaxScales];  // T_k
+    __shared__ uint2 tab_s[256];
+    const int lane = threadIdx.x & 63;
+    const int64_t ntiles = d >> 9;
+    const int32_t wave_in_block = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave_in_block;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
+
+    // every row of the first tile goes out before W is read and the tables
+    // are formed
+    f32x4 A[ROWS], B[ROWS];
+    const auto load_rows = [&](int64_t T) {
+        const int64_t a_off = (T << 9) + 4 * lane;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            const float* row = g + static_cast<int64_t>(r < M ? r : M - 1) * ldg;
+            A[r] = load_nt(row + a_off);
+            B[r] = load_nt(row + a_off + 256);
+        }
+    };
+    if (first < ntiles)
+        load_rows(first);
+
+    const float W = *wptr;
+    const float s0 = S.s[0];
+    const int32_t K = S.K;
+    const float q0 = div_rn32(s0, W);
+    const bool zero = zero_path(W, q0);
+    const bool pre = zero || div_rn32(S.s_last, W) <= 0x1p100f;
+    if (threadIdx.x < K) {
+        const float inv = zero ? 0.0f : div_rn32(S.s[threadIdx.x], W);
+        inv_s[threadIdx.x] = inv;
+        inv_p[threadIdx.x] = pre ? inv * 65536.0f : inv;
+        const float denom = static_cast<float>(static_cast<double>(M) * static_cast<double>(S.s[threadIdx.x]));
+        deq_s[threadIdx.x] = zero ? 0.0f : div_rn32(W, denom);
+        thr_s[threadIdx.x] = zero ? 0.0f : index_threshold(inv, s0);
+    }
+    __syncthreads();
+    // thread e forms the table's entry e (the rule of k_index_max with the
+    // thresholds' full bits): x + [bits(a) <= y] is the index of a value a > 0
+    // of binade e; a binade without a threshold inside holds y = 0xFFFFFFFF
+    // with x lowered by one; on the zero path every value gets K - 1
+    int crowded = 0;
+    {
+        const uint32_t e = threadIdx.x;
+        int32_t above = 0, inside = 0;
+        uint32_t tin = 0u;
+        for (int k = 0; k < K; ++k) {
+            const uint32_t tb = __float_as_uint(thr_s[k]);
+            above += (tb >> 23) > e ? 1 : 0;
+            if ((tb >> 23) == e) {
+                ++inside;
+                tin = tb;
+            }
+        }
+        uint2 ent;
+        if (zero) {
+            ent.x = static_cast<uint32_t>(K - 2);
+            ent.y = 0xFFFFFFFFu;
+        } else {
+            crowded = inside > 1 ? 1 : 0;
+            const bool limit = inside > 0 && above > 0;
+            ent.x = static_cast<uint32_t>(above > 0 ? above - 1 : 0) - (limit ? 0u : 1u);
+            ent.y = limit ? tin : 0xFFFFFFFFu;
+        }
+        tab_s[e] = ent;
+    }
+    const bool by_table = __syncthreads_or(crowded) == 0;
+    uint32_t one2 = 0x00010001u;
+    asm("" : "+s"(one2));
+    const float s0x = pre ? s0 * 65536.0f : s0;
+
+    // the preloaded tile, then (on a grid capped below one tile per wave)
+    // every stride-th tile after it
+    for (int64_t T = first; T < ntiles; T += stride) {
+        if (T != first)
+            load_rows(T);
+        if (pre)
+            index_quant_sum_tile<ROWS, true, NT>(A, B, M, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x, deq_s, key0,
+                                                 key1, one2, idx, sum, out);
+        else
+            index_quant_sum_tile<ROWS, false, NT>(A, B, M, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x, deq_s, key0,
+                                                  key1, one2, idx, sum, out);
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 64)
+        index_quant_sum_tail(g, d, ldg, M, ntiles, thr_s, K, zero, inv_s, s0, key0, key1, idx, sum, deq_s, out);
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers (called by the ABI layer after validation).
 // ---------------------------------------------------------------------------
 // Tiles per wave for the quantiser.  Launch-shape sweeps on MI355X with cold
@@ -1789,6 +2077,37 @@ hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg
 #undef UQ_LAUNCH_QSUM_DEQ
 #undef UQ_LAUNCH_QSUM_NT
 #undef UQ_LAUNCH_QSUM
+    return hipGetLastError();
+}
+
+hipError_t launch_index_quant_sum(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
+                                  const ScaleSet& S, uint64_t seed, uint8_t* idx, int32_t* sum, float* out,
+                                  hipStream_t stream)
+{
+    if (d == 0)
+        return hipSuccess;
+    const uint32_t key0 = static_cast<uint32_t>(seed);
+    const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
+    const dim3 grid(one_shot(d >> 9, kBlock / 64));
+    const bool nt = 4 * d > kSumNontemporalBytes;
+#define UQ_LAUNCH_IQS(ROWS)                                                                                        \
+    do {                                                                                                           \
+        if (nt)                                                                                                    \
+            hipLaunchKernelGGL((k_index_quant_sum<ROWS, true>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, w, S, \
+                               key0, key1, idx, sum, out);                                                         \
+        else                                                                                                       \
+            hipLaunchKernelGGL((k_index_quant_sum<ROWS, false>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, w,   \
+                               S, key0, key1, idx, sum, out);                                                      \
+    } while (0)
+    if (M <= 2)
+        UQ_LAUNCH_IQS(2);
+    else if (M <= 4)
+        UQ_LAUNCH_IQS(4);
+    else if (M <= 8)
+        UQ_LAUNCH_IQS(8);
+    else
+        UQ_LAUNCH_IQS(16);
+#undef UQ_LAUNCH_IQS
     return hipGetLastError();
 }
 

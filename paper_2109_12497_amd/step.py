@@ -10,8 +10,8 @@ from __future__ import annotations
 
 import torch
 
-from . import (_stream, uq_dequantize, uq_gather, uq_quantize_multi, uq_quantize_packed, uq_quantize_single,
-               uq_quantize_sum, uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale,
+from . import (_stream, uq_dequantize, uq_gather, uq_index_quantize_sum, uq_quantize_multi, uq_quantize_packed,
+               uq_quantize_single, uq_quantize_sum, uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale,
                uq_sum_codes, uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
 
 
@@ -32,16 +32,24 @@ class Step:
     (uq_quantize_sum) and never stored: one call per worker when streamed
     (the last one also reconstructs), one call for all workers otherwise.
     The default is True for a streamed step with fused=True, else False.
+    index_in_pass=True (all rows in one call, several scales, M <= 16): the
+    shared index is formed inside that call from the rows it holds
+    (uq_index_quantize_sum), so the shared-scale call forms W only.  The
+    default is True exactly when those conditions hold.
     """
 
     def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None,
-                 bits: int = 8, fused: bool = True, quant_sum: bool | None = None):
+                 bits: int = 8, fused: bool = True, quant_sum: bool | None = None,
+                 index_in_pass: bool | None = None):
         self.d, self.M = d, M
         self.fused = fused
         self.quant_sum = (streamed and fused) if quant_sum is None else quant_sum
         assert not (self.quant_sum and not fused), "quant_sum reconstructs in the same pass (fused)"
         self.scales = [float(s) for s in scales]
         self.K = len(self.scales)
+        can = self.quant_sum and not streamed and self.K > 1 and 1 <= M <= 16
+        self.index_in_pass = can if index_in_pass is None else index_in_pass
+        assert not (self.index_in_pass and not can), "index_in_pass needs all rows in one quant_sum call, K > 1, M <= 16"
         self.streamed = streamed
         self.bits = bits
         row_bytes = (max(d, 1) * bits + 7) // 8
@@ -60,9 +68,14 @@ class Step:
         self.out = torch.zeros(round_up(max(d, 1), 64), dtype=torch.float32, device=device)
 
     # -- the four stages -------------------------------------------------------
-    def shared_scale(self, g, stream=None):
-        uq_shared_scale(g, self.d, self.M, g.stride(0), self.scales, self.K, self.w, self.idx, self.ws,
-                        self.ws_bytes, stream)
+    def shared_scale(self, g, stream=None, w_only: bool = False):
+        if w_only:
+            # W does not depend on the scales: the one-scale call forms it alone
+            uq_shared_scale(g, self.d, self.M, g.stride(0), self.scales[:1], 1, self.w, None, self.ws,
+                            self.ws_bytes, stream)
+        else:
+            uq_shared_scale(g, self.d, self.M, g.stride(0), self.scales, self.K, self.w, self.idx, self.ws,
+                            self.ws_bytes, stream)
 
     def quantize(self, g, seed: int, rows: int | None = None, worker0: int = 0, codes=None, stream=None):
         rows = self.M if rows is None else rows
@@ -91,6 +104,10 @@ class Step:
         uq_quantize_sum(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed,
                         accumulate, self.sum, self.M, self.out if reconstruct else None, stream)
 
+    def index_quantize_sum(self, g, seed: int, stream=None):
+        uq_index_quantize_sum(g, self.d, self.M, g.stride(0), self.w, self.scales, self.K, seed, self.idx, self.sum,
+                              self.out, stream)
+
     def dequantize(self, stream=None):
         uq_dequantize(self.sum, self.d, self.M, self.w, self.scales, self.K, self.idx, self.out, stream)
 
@@ -106,8 +123,10 @@ class Step:
         assert g.dtype == torch.float32 and g.device == self.device and g.shape[0] == self.M
         assert g.stride(1) == 1 and g.shape[1] >= self.d
         stream = _stream(stream)  # resolved once for the step's calls
-        self.shared_scale(g, stream)
-        if self.quant_sum and self.streamed:
+        self.shared_scale(g, stream, w_only=self.index_in_pass)
+        if self.index_in_pass:
+            self.index_quantize_sum(g, seed, stream=stream)
+        elif self.quant_sum and self.streamed:
             for m in range(self.M):
                 self.quantize_sum(g[m:m + 1], seed, rows=1, worker0=m, accumulate=1 if m > 0 else 0,
                                   reconstruct=m == self.M - 1, stream=stream)

@@ -262,6 +262,33 @@ def test_quantize_sum_reconstruction_checks_only_with_out():
     assert status_qsum(d=0, M=0) == uq.UQ_EINVAL
 
 
+def status_iqs(g=A, d=100, M=2, ldg=128, w=A, scales=S4, K=4, seed=1, idx=A, sum_=A, out=A):
+    hs = uq._HostScales(scales)
+    return L.uq_index_quantize_sum(g, d, M, ldg, w, hs.ptr, K, seed, idx, sum_, out, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(g=None), "inval"), (dict(w=None), "inval"), (dict(w=A + 2), "align"), (dict(d=-1), "inval"),
+    (dict(M=0), "inval"), (dict(M=17), "range"), (dict(ldg=96), "inval"), (dict(ldg=102), "align"),
+    (dict(g=A + 8), "align"), (dict(idx=None), "inval"), (dict(idx=A + 4), "align"), (dict(K=0), "range"),
+    (dict(scales=None), "inval"), (dict(scales=[127.0, 100.0, 200.0, 300.0]), "range"),
+    (dict(sum_=None), "inval"), (dict(sum_=A + 4), "align"), (dict(out=None), "inval"),
+    (dict(out=A + 4), "align"), (dict(M=3, K=2, scales=[7.0, 11184811.0]), "range"),
+    (dict(K=1, scales=[128.0]), "range"),
+])
+def test_index_quantize_sum_rejects(kw, want):
+    assert status_iqs(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
+def test_index_quantize_sum_accepts_valid_no_ops():
+    """d = 0 passes every check and launches nothing; one scale is valid (the
+    index is then 0 everywhere)."""
+    assert status_iqs(d=0) == uq.UQ_OK
+    assert status_iqs(d=0, K=1, scales=[127.0]) == uq.UQ_OK
+    assert status_iqs(d=0, M=16) == uq.UQ_OK
+
+
 def test_binding_raises_with_detail():
     with pytest.raises(uq.UQError) as e:
         uq.uq_quantize_single(A, 100, 2, 128, 0, A, 200, 1, A, 128, stream=0)

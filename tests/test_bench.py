@@ -36,6 +36,19 @@ def test_step_bytes_per_coordinate(M):
                                                       14 * M + 11 - (12 * M + 10))
 
 
+@pytest.mark.parametrize("M", [1, 2, 8, 16])
+def test_index_in_pass_bytes(M):
+    """Several scales, all rows in one call that also forms the index: the
+    one-scale norm pass (4M), then the rows in (4M), the index, the sums and
+    the output out (1 + 4 + 4); no row maxima and no index pass."""
+    d = 1 << 20
+    b = bench.algorithmic_bytes(d, M, 4, False, 8, True, True)
+    assert b["shared_scale"] == 4 * M * d and b["index_quant_sum"] == (4 * M + 9) * d
+    assert b["total"] == (8 * M + 9) * d
+    st = bench.plan_stages(d, M, 4, 8, False, True, True)
+    assert [s["kernels"] for s in st] == [["k_sumsq", "k_finish"], ["k_index_quant_sum"]]
+
+
 def test_streamed_bytes():
     d, M, K = 1 << 20, 16, 8
     # codes stored, then summed: the quantiser row by row (the index read by

@@ -54,12 +54,19 @@ def check_oracle(st, host, d, scales, seed):
 
 @pytest.mark.parametrize("d", [1, 5, 8, 9, 511, 512, 513, 1000, 4097, 10_007, 65_539, 200_003])
 @pytest.mark.parametrize("name", list(SCALE_SETS))
-@pytest.mark.parametrize("streamed", [True, False], ids=["per-worker", "all-rows"])
-def test_quant_sum_matches_oracle(d, name, streamed):
+@pytest.mark.parametrize("form", ["per-worker", "all-rows", "all-rows-index-in-pass"])
+def test_quant_sum_matches_oracle(d, name, form):
+    """Per-worker calls, and all rows in one call with the shared index from
+    uq_shared_scale or (several scales) formed inside the call."""
     scales = SCALE_SETS[name]
+    if form == "all-rows-index-in-pass" and len(scales) == 1:
+        pytest.skip("one scale has no index to form")
     M = 5
     host = synth.mixed_rows(M, d, seed=d + 3, ldg=synth.round_up(d, 64))
-    st, _ = run_step(host, d, scales, seed=900 + d, streamed=streamed, quant_sum=True)
+    kw = dict(streamed=form == "per-worker", quant_sum=True)
+    if form != "per-worker":
+        kw["index_in_pass"] = form == "all-rows-index-in-pass"
+    st, _ = run_step(host, d, scales, seed=900 + d, **kw)
     assert st.codes is None  # no code row is kept
     check_oracle(st, host, d, scales, seed=900 + d)
 
@@ -73,7 +80,7 @@ def test_quant_sum_equals_composed_calls(M, name):
     d = 123_457
     host = synth.mixed_rows(M, d, seed=M, ldg=synth.round_up(d, 64))
     a, _ = run_step(host, d, scales, seed=11, streamed=True, quant_sum=True)
-    b, _ = run_step(host, d, scales, seed=11, streamed=False, quant_sum=True)
+    b, _ = run_step(host, d, scales, seed=11, streamed=False, quant_sum=True, index_in_pass=False)
     c, _ = run_step(host, d, scales, seed=11, streamed=True, quant_sum=False)
     e, _ = run_step(host, d, scales, seed=11, streamed=False, fused=False)
     for st in (b, c, e):
@@ -117,8 +124,9 @@ def test_quant_sum_capped_grids(cap, streamed):
     uq.uq_set_grid_cap(cap)
     try:
         for scales in (SCALE_SETS["s127"], SCALE_SETS["K4"]):
-            st, _ = run_step(host, d, scales, seed=cap, streamed=streamed, quant_sum=True)
-            check_oracle(st, host, d, scales, seed=cap)
+            for iip in ((None,) if streamed or len(scales) == 1 else (False, True)):
+                st, _ = run_step(host, d, scales, seed=cap, streamed=streamed, quant_sum=True, index_in_pass=iip)
+                check_oracle(st, host, d, scales, seed=cap)
     finally:
         uq.uq_set_grid_cap(0)
 
