@@ -1611,79 +1611,84 @@ __device__ __forceinline__ float max3_abs(float m, float x, float y)
     return __builtin_elementwise_maximum(m, __builtin_elementwise_maximum(fabsf(x), fabsf(y)));
 }
 
-template <int ROWS, bool PRE, bool NT>
-__device__ __forceinline__ void index_quant_sum_tile(const f32x4 (&A)[ROWS], const f32x4 (&B)[ROWS], int32_t M,
-                                                     int64_t T, const uint2* tab, bool by_table, const float* thr,
-                                                     int32_t K, bool zero, const float* inv_t, float s0x,
-                                                     const float* deq_t, uint32_t key0, uint32_t key1, uint32_t one2,
-                                                     uint8_t* __restrict__ idx, int32_t* __restrict__ sum,
-                                                     float* __restrict__ out)
+// INDEX: form the tile's shared index (several scales) and store it; else
+// one scale, every index 0.  The first `rows` rows are quantised, row r as
+// worker worker0 + r.
+template <int ROWS, bool PRE, bool NT, bool INDEX>
+__device__ __forceinline__ void index_quant_sum_tile(const f32x4 (&A)[ROWS], const f32x4 (&B)[ROWS], int32_t rows,
+                                                     uint32_t worker0, int64_t T, const uint2* tab, bool by_table,
+                                                     const float* thr, int32_t K, bool zero, const float* inv_t,
+                                                     float s0x, const float* deq_t, uint32_t key0, uint32_t key1,
+                                                     uint32_t one2, uint8_t* __restrict__ idx,
+                                                     int32_t* __restrict__ sum, float* __restrict__ out)
 {
     const int lane = threadIdx.x & 63;
     const int64_t a_off = (T << 9) + 4 * lane;
-    // the largest |g| over the rows, two rows per instruction; a result that
-    // is not finite means some value was not usable (infinite or NaN), and
-    // then the lane forms the largest usable |g| value by value
-    float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-    static_assert(ROWS % 2 == 0, "rows are taken in pairs");
+    uint32_t k[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (INDEX) {
+        // the largest |g| over the rows, two rows per instruction; a result that
+        // is not finite means some value was not usable (infinite or NaN), and
+        // then the lane forms the largest usable |g| value by value
+        float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        static_assert(ROWS % 2 == 0, "rows are taken in pairs");
 #pragma unroll
-    for (int r = 0; r < ROWS; r += 2) {
-        a[0] = max3_abs(a[0], A[r].x, A[r + 1].x);
-        a[1] = max3_abs(a[1], A[r].y, A[r + 1].y);
-        a[2] = max3_abs(a[2], A[r].z, A[r + 1].z);
-        a[3] = max3_abs(a[3], A[r].w, A[r + 1].w);
-        a[4] = max3_abs(a[4], B[r].x, B[r + 1].x);
-        a[5] = max3_abs(a[5], B[r].y, B[r + 1].y);
-        a[6] = max3_abs(a[6], B[r].z, B[r + 1].z);
-        a[7] = max3_abs(a[7], B[r].w, B[r + 1].w);
-    }
-    uint32_t worst = 0u;
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-        worst = max(worst, __float_as_uint(a[j]));
-    if (__builtin_expect(worst >= 0x7F800000u, 0)) {
+        for (int r = 0; r < ROWS; r += 2) {
+            a[0] = max3_abs(a[0], A[r].x, A[r + 1].x);
+            a[1] = max3_abs(a[1], A[r].y, A[r + 1].y);
+            a[2] = max3_abs(a[2], A[r].z, A[r + 1].z);
+            a[3] = max3_abs(a[3], A[r].w, A[r + 1].w);
+            a[4] = max3_abs(a[4], B[r].x, B[r + 1].x);
+            a[5] = max3_abs(a[5], B[r].y, B[r + 1].y);
+            a[6] = max3_abs(a[6], B[r].z, B[r + 1].z);
+            a[7] = max3_abs(a[7], B[r].w, B[r + 1].w);
+        }
+        uint32_t worst = 0u;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            a[j] = 0.0f;
+            worst = max(worst, __float_as_uint(a[j]));
+        if (__builtin_expect(worst >= 0x7F800000u, 0)) {
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-            a[0] = fmaxf(a[0], usable_or_zero(A[r].x));
-            a[1] = fmaxf(a[1], usable_or_zero(A[r].y));
-            a[2] = fmaxf(a[2], usable_or_zero(A[r].z));
-            a[3] = fmaxf(a[3], usable_or_zero(A[r].w));
-            a[4] = fmaxf(a[4], usable_or_zero(B[r].x));
-            a[5] = fmaxf(a[5], usable_or_zero(B[r].y));
-            a[6] = fmaxf(a[6], usable_or_zero(B[r].z));
-            a[7] = fmaxf(a[7], usable_or_zero(B[r].w));
-        }
-    }
-    uint32_t k[8];
-    if (by_table) {
-        const uint32_t kzero = static_cast<uint32_t>(K - 1);
+            for (int j = 0; j < 8; ++j)
+                a[j] = 0.0f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint32_t b = __float_as_uint(a[j]);
-            const uint2 t = tab[b >> 23];
-            k[j] = b != 0u ? t.x + (b <= t.y ? 1u : 0u) : kzero;
+            for (int r = 0; r < ROWS; ++r) {
+                a[0] = fmaxf(a[0], usable_or_zero(A[r].x));
+                a[1] = fmaxf(a[1], usable_or_zero(A[r].y));
+                a[2] = fmaxf(a[2], usable_or_zero(A[r].z));
+                a[3] = fmaxf(a[3], usable_or_zero(A[r].w));
+                a[4] = fmaxf(a[4], usable_or_zero(B[r].x));
+                a[5] = fmaxf(a[5], usable_or_zero(B[r].y));
+                a[6] = fmaxf(a[6], usable_or_zero(B[r].z));
+                a[7] = fmaxf(a[7], usable_or_zero(B[r].w));
+            }
         }
-    } else {
+        if (by_table) {
+            const uint32_t kzero = static_cast<uint32_t>(K - 1);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            int32_t count = 0;
-            for (int q = 0; q < K; ++q)
-                count += a[j] <= thr[q] ? 1 : 0;
-            k[j] = index_from_count(a[j], count, K, zero);
+            for (int j = 0; j < 8; ++j) {
+                const uint32_t b = __float_as_uint(a[j]);
+                const uint2 t = tab[b >> 23];
+                k[j] = b != 0u ? t.x + (b <= t.y ? 1u : 0u) : kzero;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                int32_t count = 0;
+                for (int q = 0; q < K; ++q)
+                    count += a[j] <= thr[q] ? 1 : 0;
+                k[j] = index_from_count(a[j], count, K, zero);
+            }
         }
-    }
-    const uint32_t ka = k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24);
-    const uint32_t kb = k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24);
-    uint32_t* ip = reinterpret_cast<uint32_t*>(idx + a_off);
-    if (NT) {
-        __builtin_nontemporal_store(ka, ip);
-        __builtin_nontemporal_store(kb, ip + 64);
-    } else {
-        ip[0] = ka;
-        ip[64] = kb;
+        const uint32_t ka = k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24);
+        const uint32_t kb = k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24);
+        uint32_t* ip = reinterpret_cast<uint32_t*>(idx + a_off);
+        if (NT) {
+            __builtin_nontemporal_store(ka, ip);
+            __builtin_nontemporal_store(kb, ip + 64);
+        } else {
+            ip[0] = ka;
+            ip[64] = kb;
+        }
     }
     float inv[8];
 #pragma unroll
@@ -1692,10 +1697,10 @@ __device__ __forceinline__ void index_quant_sum_tile(const f32x4 (&A)[ROWS], con
     uint32_t h[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
-        if (r < M) {
+        if (r < rows) {
             const float v[8] = {A[r].x, A[r].y, A[r].z, A[r].w, B[r].x, B[r].y, B[r].z, B[r].w};
             uint32_t p[4];
-            tile_codes<PRE>(v, inv, s0x, T, static_cast<uint32_t>(r), key0, key1, one2, p);
+            tile_codes<PRE>(v, inv, s0x, T, worker0 + static_cast<uint32_t>(r), key0, key1, one2, p);
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 h[j] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, h[j]) + __builtin_bit_cast(u16x2, p[j]));
@@ -1861,14 +1866,79 @@ __global__ __launch_bounds__(kBlock) void k_index_quant_sum(const float* __restr
         if (T != first)
             load_rows(T);
         if (pre)
-            index_quant_sum_tile<ROWS, true, NT>(A, B, M, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x, deq_s, key0,
-                                                 key1, one2, idx, sum, out);
+            index_quant_sum_tile<ROWS, true, NT, true>(A, B, M, 0u, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x,
+                                                       deq_s, key0, key1, one2, idx, sum, out);
         else
-            index_quant_sum_tile<ROWS, false, NT>(A, B, M, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x, deq_s, key0,
-                                                  key1, one2, idx, sum, out);
+            index_quant_sum_tile<ROWS, false, NT, true>(A, B, M, 0u, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x,
+                                                        deq_s, key0, key1, one2, idx, sum, out);
     }
     if (blockIdx.x == 0 && threadIdx.x < 64)
         index_quant_sum_tail(g, d, ldg, M, ntiles, thr_s, K, zero, inv_s, s0, key0, key1, idx, sum, deq_s, out);
+}
+
+// One scale, 9 to ROWS rows set and reconstructed in one call: the tiles of
+// k_index_quant_sum without the index (every row of a tile loaded at once,
+// which keeps more loads in flight than k_quant_sum's one row ahead).
+template <int ROWS, bool NT>
+__global__ __launch_bounds__(kBlock) void k_quant_sum_rows(const float* __restrict__ g, int64_t d, int32_t rows,
+                                                           int64_t ldg, int32_t worker0, const float* __restrict__ wptr,
+                                                           ScaleSet S, uint32_t key0, uint32_t key1,
+                                                           int32_t* __restrict__ sum, int32_t M,
+                                                           float* __restrict__ out)
+{
+    __shared__ float inv_s[1];  // s_0 / W
+    __shared__ float inv_p[1];  // s_0 / W * 2^16 when pre
+    __shared__ float deq_s[1];  // RN32(W / (M s_0))
+    const int lane = threadIdx.x & 63;
+    const int64_t ntiles = d >> 9;
+    const int32_t wave_in_block = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave_in_block;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
+    const uint32_t w0 = static_cast<uint32_t>(worker0);
+
+    f32x4 A[ROWS], B[ROWS];
+    const auto load_rows = [&](int64_t T) {
+        const int64_t a_off = (T << 9) + 4 * lane;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            const float* row = g + static_cast<int64_t>(r < rows ? r : rows - 1) * ldg;
+            A[r] = load_nt(row + a_off);
+            B[r] = load_nt(row + a_off + 256);
+        }
+    };
+    if (first < ntiles)
+        load_rows(first);
+
+    const float W = *wptr;
+    const float s0 = S.s[0];
+    const float q0 = div_rn32(s0, W);
+    const bool zero = zero_path(W, q0);
+    const bool pre = zero || q0 <= 0x1p100f;
+    const float inv0 = zero ? 0.0f : q0;
+    if (threadIdx.x == 0) {
+        inv_s[0] = inv0;
+        inv_p[0] = pre ? inv0 * 65536.0f : inv0;
+        const float denom = static_cast<float>(static_cast<double>(M) * static_cast<double>(s0));
+        deq_s[0] = zero ? 0.0f : div_rn32(W, denom);
+    }
+    __syncthreads();
+    uint32_t one2 = 0x00010001u;
+    asm("" : "+s"(one2));
+    const float s0x = pre ? s0 * 65536.0f : s0;
+
+    for (int64_t T = first; T < ntiles; T += stride) {
+        if (T != first)
+            load_rows(T);
+        if (pre)
+            index_quant_sum_tile<ROWS, true, NT, false>(A, B, rows, w0, T, nullptr, true, nullptr, 1, zero, inv_p,
+                                                        s0x, deq_s, key0, key1, one2, nullptr, sum, out);
+        else
+            index_quant_sum_tile<ROWS, false, NT, false>(A, B, rows, w0, T, nullptr, true, nullptr, 1, zero, inv_p,
+                                                         s0x, deq_s, key0, key1, one2, nullptr, sum, out);
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 64)
+        quant_sum_tail<false, false, true>(g, d, ldg, rows, w0, nullptr, ntiles, inv_s, inv0, s0, 0u, key0, key1, sum,
+                                           deq_s, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -2046,6 +2116,15 @@ hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg
     const bool multi = S.K > 1;
     const bool acc = accumulate != 0;
     const bool deq = out != nullptr;
+    if (!multi && !acc && deq && rows > 8 && rows <= kFuseRows) {
+        if (nt)
+            hipLaunchKernelGGL((k_quant_sum_rows<kFuseRows, true>), grid, dim3(kBlock), 0, stream, g, d, rows, ldg,
+                               worker0, w, S, key0, key1, sum, M, out);
+        else
+            hipLaunchKernelGGL((k_quant_sum_rows<kFuseRows, false>), grid, dim3(kBlock), 0, stream, g, d, rows, ldg,
+                               worker0, w, S, key0, key1, sum, M, out);
+        return hipGetLastError();
+    }
 #define UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, NT)                                                                        \
     do {                                                                                                           \
         if (rows == 1)                                                                                             \

@@ -1,9 +1,9 @@
 """GPU parity at full size, every coordinate, against the oracle.
 
 The VGG-16-shaped workload (d = 138,357,544, 16 workers; one scale s = 7, and
-four scales 7 * 16^k, with the codes stored and, for four scales, with all
-rows through the fused quantise-and-sum the benchmark times, which also forms
-the shared index), the ResNet-50-shaped one (d = 25,557,032, 8 workers, four
+four scales 7 * 16^k, with the codes stored, and with all rows through the
+fused quantise-and-sum the benchmark times, which with four scales also
+forms the shared index), the ResNet-50-shaped one (d = 25,557,032, 8 workers, four
 scales 127 * 16^k, through that same call) and the
 2^30-coordinate workload (16 workers streamed through the fused
 quantise-and-sum, eight scales).  Each is compared with the oracle (Eq. (7)-(13),
@@ -73,9 +73,10 @@ def compare_in_chunks(step, g, d, scales, seed, with_codes):
         assert bad.size == 0, f"outputs differ at {(c0 + bad[:5]).tolist()}"
 
 
-@pytest.mark.parametrize("name,quant_sum", [("vgg16-single", False), ("vgg16-multi", False), ("vgg16-multi", True),
-                                            ("resnet50", True)],
-                         ids=["vgg16-single", "vgg16-multi", "vgg16-multi-fused", "resnet50-fused"])
+@pytest.mark.parametrize("name,quant_sum", [("vgg16-single", False), ("vgg16-single", True), ("vgg16-multi", False),
+                                            ("vgg16-multi", True), ("resnet50", True)],
+                         ids=["vgg16-single", "vgg16-single-fused", "vgg16-multi", "vgg16-multi-fused",
+                              "resnet50-fused"])
 def test_every_coordinate(name, quant_sum):
     """The codes stored and summed, or (fused) all rows quantised and summed
     in one call with no codes stored, which with several scales also forms

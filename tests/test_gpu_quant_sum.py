@@ -166,3 +166,59 @@ def test_forced_scale_values(W):
     torch.cuda.synchronize()
     assert int(st.sum[:d].abs().max()) == 0
     assert int(st.out[:d].view(torch.int32).abs().max()) == 0
+
+
+@pytest.mark.parametrize("M", [9, 12, 16])
+@pytest.mark.parametrize("d", [1, 511, 513, 4097, 100_003])
+@pytest.mark.parametrize("name", ["s127", "s7"])
+def test_one_scale_rows_held_at_once(M, d, name):
+    """One scale with 9 to 16 rows set and reconstructed in one call runs the
+    form that holds every row of a tile at once; against the oracle."""
+    scales = SCALE_SETS[name]
+    host = synth.mixed_rows(M, d, seed=M * 7 + d, ldg=synth.round_up(d, 64))
+    st, _ = run_step(host, d, scales, seed=d + M, streamed=False, quant_sum=True)
+    check_oracle(st, host, d, scales, seed=d + M)
+
+
+def test_rows_held_at_once_from_a_worker_offset():
+    """Rows 3..13 of 14 workers (11 rows, worker ids 3..13) in one call: the
+    sums of those workers' codes and their reconstruction with M = 14."""
+    d, M, seed = 50_001, 14, 21
+    scales = [127.0]
+    host = synth.mixed_rows(M, d, seed=4, ldg=synth.round_up(d, 64))
+    st, g = run_step(host, d, scales, seed=seed, streamed=False, fused=False)
+    W = np.float32(st.w[0].item())
+    ref = O.pipeline(host, scales, seed, d=d, W=W)
+    uq.uq_quantize_sum(g[3:], d, 11, g.stride(0), 3, st.w, scales, 1, None, seed, 0, st.sum, M, st.out)
+    torch.cuda.synchronize()
+    want = O.sum_codes(ref["codes"][3:14])
+    assert np.array_equal(st.sum[:d].cpu().numpy(), want)
+    out = O.dequantize(want, M, W, scales)
+    assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), out.view(np.int32))
+
+
+@pytest.mark.parametrize("cap", [8, 24])
+def test_rows_held_at_once_capped_grids(cap):
+    d, M = 100_003, 16
+    host = synth.mixed_rows(M, d, seed=cap + 1, ldg=synth.round_up(d, 64))
+    uq.uq_set_grid_cap(cap)
+    try:
+        st, _ = run_step(host, d, SCALE_SETS["s7"], seed=cap, streamed=False, quant_sum=True)
+        check_oracle(st, host, d, SCALE_SETS["s7"], seed=cap)
+    finally:
+        uq.uq_set_grid_cap(0)
+
+
+@pytest.mark.parametrize("W", [0.0, float("inf"), float("nan"), 1e-45])
+def test_rows_held_at_once_forced_scale_values(W):
+    d, M = 5_003, 12
+    host = synth.gaussian_rows(M, d, seed=2, ldg=synth.round_up(d, 64))
+    g = torch.from_numpy(host).to(DEV)
+    st = Step(d, M, [127.0], device=DEV, streamed=False, quant_sum=True)
+    st.shared_scale(g)
+    st.w.fill_(W)
+    st.sum.fill_(5)
+    st.quantize_sum(g, 1)
+    torch.cuda.synchronize()
+    assert int(st.sum[:d].abs().max()) == 0
+    assert int(st.out[:d].view(torch.int32).abs().max()) == 0
