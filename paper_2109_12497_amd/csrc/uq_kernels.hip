@@ -10,8 +10,10 @@
 //   k_norm_max   several scales, 2..16 rows: the norm's tile     (norm + the
 //                sums and the largest |g| over the rows in one     index's input)
 //                read of the gradients
-//   k_rowsum     the rows' sums from those tile sums
-//   k_index_max  W, then the shared index from the maxima's keys
+//   k_rowsum     sums of those tile sums
+//   k_index_prep the rows' sums, W and the index pass's thresholds
+//                and exponent table, once per call
+//   k_index_max  the shared index from the maxima's keys
 //   k_quantise   Philox draws + stochastic rounding + int8 pack  (Eq. (8)/(12))
 //   k_sum        int8 (or 4-/2-bit) code rows -> int32           (all-reduce)
 //                sums, optionally with the reconstruction applied  (+ Eq. (9)/(13))
@@ -234,11 +236,12 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 // instead of the M rows, and the rows of the rare coordinates whose key
 // equals a threshold's.
 //   k_norm_max   block t: tile t of every row (below)
-//   k_rowsum     twice: block (b, m) sums partials [b s, (b + 1) s) of row
-//                m in a fixed order (s = kRowsumSpan), then block (0, m)
-//                sums those into S_m
-//   k_index_max  W from the S_m (the rule of k_finish; block 0 stores it),
-//                then the index of every coordinate from its key
+//   k_rowsum     block (b, m) sums partials [b s, (b + 1) s) of row m in a
+//                fixed order (s = kRowsumSpan)
+//   k_index_prep one block: those sums into S_m (the same order), W (the
+//                rule of k_finish), the thresholds, their keys and the
+//                exponent table, into the workspace
+//   k_index_max  the index of every coordinate from its key and that table
 // ---------------------------------------------------------------------------
 // Barrier for LDS traffic only: the block's LDS writes are complete and
 // visible, while its global loads and stores stay in flight (__syncthreads
@@ -404,18 +407,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         norm_max_tail<ROWS>(g, d, M, ldg, ntiles, part, keys);
 }
 
-// Block (b, m) sums part[m][b * span .. min(n, (b + 1) * span)) in a fixed
-// order (lane-strided sequential sums, 16 loads in flight per thread, then a
-// fixed butterfly and the four waves in order) into out[m * gridDim.x + b].
-__global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ part, int64_t n, int64_t span,
-                                                   double* __restrict__ out)
+// The block's fixed-order sum of p[b0, b1): lane-strided sequential sums
+// (16 loads in flight per thread), a fixed butterfly, then the four waves in
+// order.  The total is valid in thread 0; wave_part must not be reused before
+// the block's next barrier.
+__device__ __forceinline__ double rowsum_span(const double* __restrict__ p, int64_t b0, int64_t b1,
+                                              double* wave_part)
 {
-    __shared__ double wave_part[kBlock / 64];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * span;
-    const int64_t b1 = b0 + span < n ? b0 + span : n;
-    const double* p = part + static_cast<int64_t>(blockIdx.y) * n;
     double s = 0.0;
     for (int64_t j0 = b0; j0 < b1; j0 += 16 * kBlock) {
         double x[16];
@@ -432,20 +432,32 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
     if (lane == 0)
         wave_part[wave] = s;
     __syncthreads();
+    return (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
+}
+
+// Block (b, m) sums part[m][b * span .. min(n, (b + 1) * span)) in the fixed
+// order of rowsum_span into out[m * gridDim.x + b].
+__global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ part, int64_t n, int64_t span,
+                                                   double* __restrict__ out)
+{
+    __shared__ double wave_part[kBlock / 64];
+    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * span;
+    const int64_t b1 = b0 + span < n ? b0 + span : n;
+    const double s = rowsum_span(part + static_cast<int64_t>(blockIdx.y) * n, b0, b1, wave_part);
     if (threadIdx.x == 0)
-        out[static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x] =
-            (wave_part[0] + wave_part[1]) + (wave_part[2] + wave_part[3]);
+        out[static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x] = s;
 }
 
 // k_index_max: a block covers kIndexTile octets of coordinates (4 per
 // thread: octets t, t + 256, ..., so each load and store of a wave is
-// contiguous), all loaded before W is formed.  The norm pass keeps, for each
+// contiguous), all loaded before the call's constants are read.  The norm
+// pass keeps, for each
 // coordinate, the top 16 bits of its largest usable |g| over the rows (a
 // key: the exponent field and 7 mantissa bits).  The per-coordinate rule
 // compares thresholds instead of forming products: a -> RN32(a * inv_k) is
 // non-decreasing for inv_k > 0, so RN32(a * inv_k) <= s_0 holds exactly for
-// a <= T_k, the largest binary32 that passes; each block finds T_k once (a
-// few ulp steps from s_0 / inv_k).  A key below T_k's key means a < T_k, a
+// a <= T_k, the largest binary32 that passes; k_index_prep finds T_k once
+// per call (a few ulp steps from s_0 / inv_k).  A key below T_k's key means a < T_k, a
 // key above it a > T_k; only a key equal to T_k's leaves the comparison open,
 // and then the coordinate's rows are read again for its exact maximum (at
 // the scales used here, one coordinate in several thousand).  The count
@@ -454,7 +466,10 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
 // than a's counts, none in a lower one, so a table over the 256 values of the
 // exponent field gives the count above a's binade and the key of the one
 // threshold inside it, and a coordinate costs one lookup and two compares.
-// Otherwise the block compares each key with the K thresholds' keys.
+// Otherwise the block compares each key with the K thresholds' keys.  The
+// thresholds, their keys and the table are formed once per call
+// (k_index_prep) rather than in each of the pass's blocks: at 2^30
+// coordinates that prologue was most of the pass's VALU work.
 constexpr int kIndexOcts = 4;
 constexpr int64_t kIndexTile = kIndexOcts * kBlock;
 static_assert(kBlock == 256, "the exponent table has one entry per thread");
@@ -540,39 +555,72 @@ __device__ __forceinline__ uint32_t octet_key(const u32x4& kv, int c)
     return (c & 1) ? w >> 16 : w & 0xFFFFu;
 }
 
-__global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict__ keys,
-                                                      const float* __restrict__ g, int64_t ldg, int64_t d,
-                                                      int32_t M, const double* __restrict__ rows,
-                                                      float* __restrict__ wptr, ScaleSet S,
-                                                      uint8_t* __restrict__ idx)
+// One block: the rows' sums S_m from their kRowsumSpan-partial sums (the
+// order of k_rowsum), W = RN32(sqrt(max_m S_m)) (NaN if any S_m is NaN, as
+// k_finish), stored to *wptr, then the index pass's constants for the call:
+// thresholds T_k, their keys and the exponent table (thread e forms entry e:
+// the thresholds in higher binades, every key of binade e being below
+// theirs, and the one inside binade e).  On the zero path every coordinate
+// gets K - 1.
+__global__ __launch_bounds__(kBlock) void k_index_prep(const double* __restrict__ sub, int64_t nsub, int32_t M,
+                                                       double* __restrict__ rows, float* __restrict__ wptr,
+                                                       ScaleSet S, IndexTables* __restrict__ T)
 {
+    __shared__ double wave_part[kBlock / 64];
+    __shared__ double row_part[kFuseRows][kBlock / 64];
+    __shared__ double row_s[kFuseRows];
     __shared__ float thr_s[kMaxScales];
     __shared__ uint32_t hk_s[kMaxScales];
-    __shared__ uint2 tab_s[256];
-    const int64_t noct = d >> 3;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kIndexTile;
-    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kIndexTile;
-    u32x4 kv[kIndexOcts];
+    __shared__ float w_s;
+    if (nsub <= kBlock) {
+        // at most one partial per thread and row (every d below 2^32): all
+        // rows' loads at once, then for each row the arithmetic of
+        // rowsum_span (its sequential sum is the one value plus zeros,
+        // exactly that value; then the butterfly and the four waves in order)
+        const int lane = threadIdx.x & 63;
+        const int wave = threadIdx.x >> 6;
+        double x[kFuseRows];
 #pragma unroll
-    for (int j = 0; j < kIndexOcts; ++j) {
-        const int64_t o = tile0 + threadIdx.x + kBlock * j;
-        kv[j] = o < noct ? load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3))) : u32x4{0u, 0u, 0u, 0u};
-    }
-
-    // W = RN32(sqrt(max_m S_m)), NaN if any S_m is NaN (as k_finish): lane m
-    // of every wave loads S_m (M <= 64), then a butterfly maximum
-    const int lane = threadIdx.x & 63;
-    double r = lane < M ? rows[lane] : 0.0;
-    const bool any_nan = __ballot(r != r) != 0;
-    r = r != r ? 0.0 : r;
+        for (int m = 0; m < kFuseRows; ++m)
+            x[m] = 0.0 + (m < M && threadIdx.x < nsub ? sub[static_cast<int64_t>(m) * nsub + threadIdx.x] : 0.0);
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const double o = __shfl_xor(r, off, 64);
-        r = o > r ? o : r;
+        for (int m = 0; m < kFuseRows; ++m) {
+            const double s = wave_sum(x[m]);
+            if (lane == 0)
+                row_part[m][wave] = s;
+        }
+        __syncthreads();
+        if (threadIdx.x < M) {
+            const double* w4 = row_part[threadIdx.x];
+            const double r = (w4[0] + w4[1]) + (w4[2] + w4[3]);
+            rows[threadIdx.x] = r;
+            row_s[threadIdx.x] = r;
+        }
+    } else {
+        for (int32_t m = 0; m < M; ++m) {
+            const double r = rowsum_span(sub + static_cast<int64_t>(m) * nsub, 0, nsub, wave_part);
+            if (threadIdx.x == 0) {
+                rows[m] = r;
+                row_s[m] = r;
+            }
+            __syncthreads();  // wave_part is written again by the next row
+        }
     }
-    const float W = any_nan ? __builtin_nanf("") : static_cast<float>(sqrt(r));
-    if (blockIdx.x == 0 && threadIdx.x == 0)
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double best = 0.0;
+        bool any_nan = false;
+        for (int32_t m = 0; m < M; ++m) {
+            const double r = row_s[m];
+            any_nan = any_nan || (r != r);
+            best = r > best ? r : best;
+        }
+        const float W = any_nan ? __builtin_nanf("") : static_cast<float>(sqrt(best));
         *wptr = W;
+        w_s = W;
+    }
+    __syncthreads();
+    const float W = w_s;
     const float s0 = S.s[0];
     const int32_t K = S.K;
     const bool zero = zero_path(W, div_rn32(s0, W));
@@ -580,11 +628,10 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict
         const float t = zero ? 0.0f : index_threshold(div_rn32(S.s[threadIdx.x], W), s0);
         thr_s[threadIdx.x] = t;
         hk_s[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 16;
+        T->thr[threadIdx.x] = t;
+        T->hk[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 16;
     }
     __syncthreads();
-    // thread e forms the table's entry e: the thresholds in higher binades
-    // (every key of binade e is below theirs), the one in binade e; on the
-    // zero path every coordinate gets K - 1
     int crowded = 0;
     {
         const uint32_t e = threadIdx.x;
@@ -610,9 +657,38 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict
             ent.x = static_cast<uint32_t>(above > 0 ? above - 1 : 0) - (limit ? 0u : 1u);
             ent.y = limit ? kin : 0x10000u;
         }
-        tab_s[e] = ent;
+        T->tab[e] = ent;
     }
     const bool by_table = __syncthreads_or(crowded) == 0;
+    if (threadIdx.x == 0)
+        T->by_table = by_table ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict__ keys,
+                                                      const float* __restrict__ g, int64_t ldg, int64_t d,
+                                                      int32_t M, const IndexTables* __restrict__ T, int32_t K,
+                                                      uint8_t* __restrict__ idx)
+{
+    __shared__ float thr_s[kMaxScales];
+    __shared__ uint32_t hk_s[kMaxScales];
+    __shared__ uint2 tab_s[256];
+    const int64_t noct = d >> 3;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kIndexTile;
+    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kIndexTile;
+    u32x4 kv[kIndexOcts];
+#pragma unroll
+    for (int j = 0; j < kIndexOcts; ++j) {
+        const int64_t o = tile0 + threadIdx.x + kBlock * j;
+        kv[j] = o < noct ? load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3))) : u32x4{0u, 0u, 0u, 0u};
+    }
+    // the call's constants (k_index_prep), through LDS
+    tab_s[threadIdx.x] = T->tab[threadIdx.x];
+    if (threadIdx.x < K) {
+        thr_s[threadIdx.x] = T->thr[threadIdx.x];
+        hk_s[threadIdx.x] = T->hk[threadIdx.x];
+    }
+    const bool by_table = T->by_table != 0;
+    __syncthreads();
 
     for (int64_t t0 = tile0; t0 < noct; t0 += stride) {
         if (t0 != tile0) {
@@ -2005,7 +2081,8 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         double* part = static_cast<double*>(ws);
         double* sub = reinterpret_cast<double*>(static_cast<char*>(ws) + L.sub_off);
         double* rows = reinterpret_cast<double*>(static_cast<char*>(ws) + L.rows_off);
-        uint16_t* keys = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + L.keys_off);
+        IndexTables* tabs = reinterpret_cast<IndexTables*>(static_cast<char*>(ws) + L.tab_off);
+        uint16_t* keys = fused_keys(ws, L);
         const dim3 grid(one_shot(plan.ntiles + 1, 1));
         // keys beyond half the 256 MB Infinity Cache are stored
         // nontemporally (the index pass would not find them there)
@@ -2038,10 +2115,10 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         // the rows' sums: kRowsumSpan tile partials at a time, then those sums
         hipLaunchKernelGGL(k_rowsum, dim3(static_cast<unsigned>(plan.nsub), static_cast<unsigned>(M)), dim3(kBlock),
                            0, stream, part, plan.ntiles + 1, kRowsumSpan, sub);
-        hipLaunchKernelGGL(k_rowsum, dim3(1, static_cast<unsigned>(M)), dim3(kBlock), 0, stream, sub, plan.nsub,
-                           plan.nsub, rows);
+        // then S_m, W and the index pass's constants in one block
+        hipLaunchKernelGGL(k_index_prep, dim3(1), dim3(kBlock), 0, stream, sub, plan.nsub, M, rows, w, S, tabs);
         const unsigned gx = one_shot((d + 7) / 8, kIndexTile);
-        hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, rows, w, S, idx);
+        hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K, idx);
         return hipGetLastError();
     }
     double* part = static_cast<double*>(ws);

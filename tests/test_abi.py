@@ -68,9 +68,13 @@ def test_strerror_and_workspace():
         if 2 <= M <= 16:
             # several scales with 2 to 16 rows: d 16-bit keys of the row
             # maxima, one fp64 partial per row and 1024 coordinates, their
-            # sums per 16384 partials, and M row sums
+            # sums per 16384 partials, M row sums, and the index pass's
+            # constants (a 256-entry table of 8 bytes, two words per scale
+            # for at most 16 scales, one flag), and up to 4 KiB to align the
+            # keys
             tiles = -(-d // 1024)
-            assert 2 * d <= b <= 2 * d + 8 * M * (tiles + -(-tiles // 16384) + 1) + 5 * 256
+            consts = 256 * 8 + 2 * 4 * 16 + 4
+            assert 2 * d <= b <= 2 * d + 8 * M * (tiles + -(-tiles // 16384) + 1) + consts + 4096 + 6 * 256
         else:
             assert b <= 8 * M * 1024 + 256
     assert uq.uq_workspace_bytes(2 ** 30, 17) <= 17 * 1024 * 8 + 256

@@ -558,6 +558,34 @@ def test_rows_longer_than_2_pow_31():
     torch.cuda.empty_cache()
 
 
+def test_shared_scale_rows_longer_than_2_pow_32():
+    """d = 2^32 + 2^22 + 333 coordinates, two rows, four scales: the norm
+    pass's partial sums then take more than 256 second-level sums per row,
+    the one size range where the index pass's set-up sums each row in the
+    fixed order of the first level instead of one partial per thread.  W
+    against a float64 norm; the shared index against the oracle on windows
+    around 2^32 and at the ragged end."""
+    d, M = (1 << 32) + (1 << 22) + 333, 2
+    scales = S_MULTI4
+    g = _long_rows(d, M, seed=32)
+    g[0, (1 << 32) + 77] = 0.5  # a large coordinate past 2^32 sets the index there
+    w = torch.zeros(4, dtype=torch.float32, device=DEV)
+    idx = torch.zeros(synth.round_up(d, 256), dtype=torch.uint8, device=DEV)
+    wsb = uq.uq_workspace_bytes(d, M)
+    ws = torch.zeros(wsb // 8 + 1, dtype=torch.float64, device=DEV)
+    uq.uq_shared_scale(g, d, M, g.stride(0), scales, len(scales), w, idx, ws, wsb)
+    torch.cuda.synchronize()
+    W = np.float32(w[0].item())
+    device_norm_check(g, d, W)
+    n = 1 << 14
+    for i0 in (0, (1 << 32) - n // 2, (1 << 32) + 1, d - n):
+        host = g[:, i0:i0 + n].cpu().numpy()
+        ref = O.scale_index_shared(host, W, scales)
+        assert np.array_equal(idx[i0:i0 + n].cpu().numpy(), ref), f"idx window {i0}"
+    del g, idx, ws
+    torch.cuda.empty_cache()
+
+
 def _long_rows(d, M, seed):
     ldg = synth.round_up(d, 64)
     gen = torch.Generator(device=DEV)
