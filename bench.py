@@ -46,7 +46,10 @@ METRIC = "G gradient elements/s quantize+sum+dequantize; % of HBM peak GB/s"
 HBM_PEAK_GBS = 8000.0
 # workers up to which the shared scale takes the fused norm + row-maximum pass
 FUSED_MAX_ROWS = 16
-KERNEL_SOURCES = ["paper_2109_12497_amd/csrc/uq_kernels.hip", "paper_2109_12497_amd/csrc/uq_device.hpp"]
+# the sources whose code the counter summaries are tied to (kernels, device
+# helpers, launch planning and workspace layout)
+KERNEL_SOURCES = ["paper_2109_12497_amd/csrc/uq_kernels.hip", "paper_2109_12497_amd/csrc/uq_device.hpp",
+                  "paper_2109_12497_amd/csrc/uq_launch.hpp", "paper_2109_12497_amd/csrc/uq_randk.hip"]
 
 
 def code_bytes(d: int, bits: int) -> int:
@@ -71,7 +74,7 @@ def scale_kernels(M: int, K: int) -> list:
     if K == 1:
         return ["k_sumsq", "k_finish"]
     if 2 <= M <= FUSED_MAX_ROWS:
-        return ["k_norm_max", "k_rowsum", "k_index_max"]
+        return ["k_norm_max", "k_rowsum", "k_index_prep", "k_index_max"]
     return ["k_sumsq", "k_finish", "k_index"]
 
 
@@ -118,7 +121,9 @@ def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, q
             st.append(dict(name="quant_sum_last", kernels=["k_quant_sum_acc_deq"], calls=1,
                            bytes=quant_sum_bytes_per_call(d, 1, K, True, True)))
     elif quant_sum:
-        st.append(dict(name="quant_sum", kernels=["k_quant_sum_set_deq"], calls=1,
+        # one scale and 5 to 16 rows: a tile's rows split over a block's waves
+        kern = "k_quant_sum_split" if K == 1 and 4 < M <= FUSED_MAX_ROWS else "k_quant_sum_set_deq"
+        st.append(dict(name="quant_sum", kernels=[kern], calls=1,
                        bytes=quant_sum_bytes_per_call(d, M, K, False, True)))
     elif streamed:
         # the codes of one worker per call, then summed into the running sum

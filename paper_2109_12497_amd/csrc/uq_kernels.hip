@@ -22,6 +22,9 @@
 //   k_index_quant_sum  all of up to 16 rows held at once: the     (Eq. (11) +
 //                shared index from their exact maxima, then        sharing, (12),
 //                k_quant_sum's codes, sums and reconstruction      sum, (13))
+//   k_quant_sum_split  one scale, 5 to 16 rows: a tile's rows     (Eq. (8),
+//                split over a block's waves, their sums meeting    sum, (9))
+//                in LDS
 //   k_dequant    int32 (+ index) -> fp32                          (Eq. (9)/(13))
 //
 // Every per-coordinate result is a pure function of its inputs and the
@@ -1952,32 +1955,92 @@ __global__ __launch_bounds__(kBlock) void k_index_quant_sum(const float* __restr
         index_quant_sum_tail(g, d, ldg, M, ntiles, thr_s, K, zero, inv_s, s0, key0, key1, idx, sum, deq_s, out);
 }
 
-// One scale, 9 to ROWS rows set and reconstructed in one call: the tiles of
-// k_index_quant_sum without the index (every row of a tile loaded at once,
-// which keeps more loads in flight than k_quant_sum's one row ahead).
-template <int ROWS, bool NT>
-__global__ __launch_bounds__(kBlock) void k_quant_sum_rows(const float* __restrict__ g, int64_t d, int32_t rows,
-                                                           int64_t ldg, int32_t worker0, const float* __restrict__ wptr,
-                                                           ScaleSet S, uint32_t key0, uint32_t key1,
-                                                           int32_t* __restrict__ sum, int32_t M,
-                                                           float* __restrict__ out)
+// ---------------------------------------------------------------------------
+// One scale, 5 to 16 rows set and reconstructed in one call, the rows of a
+// tile split over the block's four waves: wave w holds rows w, w + 4, ...
+// (RPW of them) of the block's 512-coordinate tile in k_quantise's lane
+// layout, codes them (the codes and draws of k_quantise for that row and
+// tile) and sums them in the 16-bit lanes of the pair registers; the waves'
+// int32 sums meet in LDS, and waves 0 and 1 add them and store the tile's A
+// and B quads of sums and of the reconstruction.  The integer sums are exact
+// in any order.  Against one wave holding every row of a tile (the layout
+// k_index_quant_sum keeps for several scales), a wave needs about a third of
+// the registers (86 against 217 for 16 rows), so five waves share a SIMD
+// instead of two and hide each other's loads: measured on MI355X, 1.76 ->
+// 1.62 ms at VGG-16 size (16 rows) and 72.9 -> 69.6 us at ResNet-18 size
+// (8 rows, against k_quant_sum's row loop).  The same split with the shared
+// index formed in the pass (the waves' maxima meeting in LDS first) was
+// slower with several scales: each tile then waits at two barriers and each
+// block forms the thresholds and the exponent table again (ResNet-50 size,
+// 8 rows: 0.237 against 0.175 ms; VGG-16, four scales: 1.94 against 1.79 ms;
+// 0.209 and 1.82 ms with four tiles per block).
+// ---------------------------------------------------------------------------
+template <int RPW, bool PRE, bool NT>
+__device__ __forceinline__ void split_tile(const f32x4 (&A)[RPW], const f32x4 (&B)[RPW], int32_t rows,
+                                           uint32_t worker0, int64_t T, float inv0, float s0x, float deq0,
+                                           uint32_t key0, uint32_t key1, uint32_t one2, i32x4 (*ps)[128],
+                                           int32_t* __restrict__ sum, float* __restrict__ out)
 {
-    __shared__ float inv_s[1];  // s_0 / W
-    __shared__ float inv_p[1];  // s_0 / W * 2^16 when pre
-    __shared__ float deq_s[1];  // RN32(W / (M s_0))
     const int lane = threadIdx.x & 63;
-    const int64_t ntiles = d >> 9;
-    const int32_t wave_in_block = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
-    const int64_t first = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave_in_block;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
-    const uint32_t w0 = static_cast<uint32_t>(worker0);
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t a_off = (T << 9) + 4 * lane;
+    const float inv[8] = {inv0, inv0, inv0, inv0, inv0, inv0, inv0, inv0};
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+        const int32_t m = wave + 4 * r;
+        if (m < rows) {
+            const float v[8] = {A[r].x, A[r].y, A[r].z, A[r].w, B[r].x, B[r].y, B[r].z, B[r].w};
+            uint32_t p[4];
+            tile_codes<PRE>(v, inv, s0x, T, worker0 + static_cast<uint32_t>(m), key0, key1, one2, p);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                h[j] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, h[j]) + __builtin_bit_cast(u16x2, p[j]));
+        }
+    }
+    int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    widen_pairs(h, acc);
+    ps[wave][lane] = i32x4{acc[0], acc[1], acc[2], acc[3]};
+    ps[wave][64 + lane] = i32x4{acc[4], acc[5], acc[6], acc[7]};
+    __syncthreads();
+    if (wave < 2) {
+        // wave 0: the A quad of every lane, wave 1: the B quad
+        const int q = 64 * wave + lane;
+        const i32x4 s = (ps[0][q] + ps[1][q]) + (ps[2][q] + ps[3][q]);
+        const int64_t off = a_off + 256 * wave;
+        store_sum4<NT>(sum + off, s);
+        f32x4 o;
+        o.x = static_cast<float>(s.x) * deq0;
+        o.y = static_cast<float>(s.y) * deq0;
+        o.z = static_cast<float>(s.z) * deq0;
+        o.w = static_cast<float>(s.w) * deq0;
+        store_nt(out + off, o);
+    }
+}
 
-    f32x4 A[ROWS], B[ROWS];
+// One block per tile (blocks stride over the tiles on a capped grid).
+template <int RPW, bool NT>
+__global__ __launch_bounds__(kBlock) void k_quant_sum_split(const float* __restrict__ g, int64_t d, int32_t rows,
+                                                            int64_t ldg, int32_t worker0,
+                                                            const float* __restrict__ wptr, ScaleSet S, uint32_t key0,
+                                                            uint32_t key1, int32_t* __restrict__ sum, int32_t M,
+                                                            float* __restrict__ out)
+{
+    __shared__ i32x4 ps_s[2][4][128];  // by tile parity: the next tile's sums never overwrite ones being read
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t ntiles = d >> 9;
+    const uint32_t w0 = static_cast<uint32_t>(worker0);
+    const int64_t first = blockIdx.x;
+
+    // the first tile's rows go out before W is read
+    f32x4 A[RPW], B[RPW];
     const auto load_rows = [&](int64_t T) {
         const int64_t a_off = (T << 9) + 4 * lane;
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-            const float* row = g + static_cast<int64_t>(r < rows ? r : rows - 1) * ldg;
+        for (int r = 0; r < RPW; ++r) {
+            const int32_t m = wave + 4 * r;
+            const float* row = g + static_cast<int64_t>(m < rows ? m : rows - 1) * ldg;
             A[r] = load_nt(row + a_off);
             B[r] = load_nt(row + a_off + 256);
         }
@@ -1991,30 +2054,28 @@ __global__ __launch_bounds__(kBlock) void k_quant_sum_rows(const float* __restri
     const bool zero = zero_path(W, q0);
     const bool pre = zero || q0 <= 0x1p100f;
     const float inv0 = zero ? 0.0f : q0;
-    if (threadIdx.x == 0) {
-        inv_s[0] = inv0;
-        inv_p[0] = pre ? inv0 * 65536.0f : inv0;
-        const float denom = static_cast<float>(static_cast<double>(M) * static_cast<double>(s0));
-        deq_s[0] = zero ? 0.0f : div_rn32(W, denom);
-    }
-    __syncthreads();
+    const float denom = static_cast<float>(static_cast<double>(M) * static_cast<double>(s0));
+    const float deq0 = zero ? 0.0f : div_rn32(W, denom);
     uint32_t one2 = 0x00010001u;
     asm("" : "+s"(one2));
     const float s0x = pre ? s0 * 65536.0f : s0;
+    const float invx = pre ? inv0 * 65536.0f : inv0;
 
-    for (int64_t T = first; T < ntiles; T += stride) {
+    int parity = 0;
+    for (int64_t T = first; T < ntiles; T += gridDim.x) {
         if (T != first)
             load_rows(T);
         if (pre)
-            index_quant_sum_tile<ROWS, true, NT, false>(A, B, rows, w0, T, nullptr, true, nullptr, 1, zero, inv_p,
-                                                        s0x, deq_s, key0, key1, one2, nullptr, sum, out);
+            split_tile<RPW, true, NT>(A, B, rows, w0, T, invx, s0x, deq0, key0, key1, one2, ps_s[parity], sum, out);
         else
-            index_quant_sum_tile<ROWS, false, NT, false>(A, B, rows, w0, T, nullptr, true, nullptr, 1, zero, inv_p,
-                                                         s0x, deq_s, key0, key1, one2, nullptr, sum, out);
+            split_tile<RPW, false, NT>(A, B, rows, w0, T, invx, s0x, deq0, key0, key1, one2, ps_s[parity], sum, out);
+        parity ^= 1;
     }
-    if (blockIdx.x == 0 && threadIdx.x < 64)
-        quant_sum_tail<false, false, true>(g, d, ldg, rows, w0, nullptr, ntiles, inv_s, inv0, s0, 0u, key0, key1, sum,
-                                           deq_s, out);
+    if (blockIdx.x == 0 && threadIdx.x < 64) {
+        const float inv_t[1] = {inv0}, deq_t[1] = {deq0};
+        quant_sum_tail<false, false, true>(g, d, ldg, rows, w0, nullptr, ntiles, inv_t, inv0, s0, 0u, key0, key1, sum,
+                                           deq_t, out);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -2193,13 +2254,25 @@ hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg
     const bool multi = S.K > 1;
     const bool acc = accumulate != 0;
     const bool deq = out != nullptr;
-    if (!multi && !acc && deq && rows > 8 && rows <= kFuseRows) {
-        if (nt)
-            hipLaunchKernelGGL((k_quant_sum_rows<kFuseRows, true>), grid, dim3(kBlock), 0, stream, g, d, rows, ldg,
-                               worker0, w, S, key0, key1, sum, M, out);
-        else
-            hipLaunchKernelGGL((k_quant_sum_rows<kFuseRows, false>), grid, dim3(kBlock), 0, stream, g, d, rows, ldg,
-                               worker0, w, S, key0, key1, sum, M, out);
+    if (!multi && !acc && deq && rows > 4 && rows <= kFuseRows) {
+        // one scale, 5 to 16 rows set and reconstructed: the rows of a tile
+        // split over the block's waves, one block per tile
+        const dim3 sgrid(one_shot(d >> 9, 1));
+#define UQ_LAUNCH_SPLIT(RPW, NT)                                                                                  \
+    hipLaunchKernelGGL((k_quant_sum_split<RPW, NT>), sgrid, dim3(kBlock), 0, stream, g, d, rows, ldg, worker0, w,   \
+                       S, key0, key1, sum, M, out)
+        if (rows <= 8) {
+            if (nt)
+                UQ_LAUNCH_SPLIT(2, true);
+            else
+                UQ_LAUNCH_SPLIT(2, false);
+        } else {
+            if (nt)
+                UQ_LAUNCH_SPLIT(4, true);
+            else
+                UQ_LAUNCH_SPLIT(4, false);
+        }
+#undef UQ_LAUNCH_SPLIT
         return hipGetLastError();
     }
 #define UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, NT)                                                                        \

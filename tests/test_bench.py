@@ -75,11 +75,18 @@ def test_packed_bytes():
 def test_stage_plan_names_the_kernels():
     st = bench.plan_stages(1 << 20, 16, 8, 8, True, True)
     assert [s["name"] for s in st] == ["shared_scale", "quant_sum_first", "quant_sum", "quant_sum_last"]
-    assert st[0]["kernels"] == ["k_norm_max", "k_rowsum", "k_index_max"]
+    assert st[0]["kernels"] == ["k_norm_max", "k_rowsum", "k_index_prep", "k_index_max"]
     assert [s["calls"] for s in st] == [1, 1, 14, 1]
     assert bench.plan_stages(100, 8, 1)[1]["kernels"] == ["k_quantise_single"]
     assert bench.plan_stages(100, 16, 4, 4)[1]["kernels"] == ["k_quantise_multi_4bit"]
     assert bench.plan_stages(100, 17, 4)[0]["kernels"] == ["k_sumsq", "k_finish", "k_index"]
+    # all rows through one quantise-and-sum call: one scale and 5 to 16 rows
+    # split a tile's rows over a block's waves
+    assert bench.plan_stages(100, 16, 1, 8, False, True)[1]["kernels"] == ["k_quant_sum_split"]
+    assert bench.plan_stages(100, 5, 1, 8, False, True)[1]["kernels"] == ["k_quant_sum_split"]
+    assert bench.plan_stages(100, 4, 1, 8, False, True)[1]["kernels"] == ["k_quant_sum_set_deq"]
+    assert bench.plan_stages(100, 16, 4, 8, False, True)[1]["kernels"] == ["k_quant_sum_set_deq"]
+    assert bench.plan_stages(100, 16, 4, 8, False, True, True)[1]["kernels"] == ["k_index_quant_sum"]
     for M in (1, 2, 3):
         st = bench.plan_stages(100, M, 2, 8, True, True)
         assert sum(s["calls"] for s in st[1:]) == M

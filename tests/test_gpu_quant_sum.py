@@ -52,15 +52,17 @@ def check_oracle(st, host, d, scales, seed):
     assert np.array_equal(st.out[:d].cpu().numpy().view(np.int32), ref["out"].view(np.int32)), "outputs differ"
 
 
+# forming the shared index inside the call needs several scales
+FORMS = [(form, name) for form in ("per-worker", "all-rows", "all-rows-index-in-pass") for name in SCALE_SETS
+         if form != "all-rows-index-in-pass" or len(SCALE_SETS[name]) > 1]
+
+
 @pytest.mark.parametrize("d", [1, 5, 8, 9, 511, 512, 513, 1000, 4097, 10_007, 65_539, 200_003])
-@pytest.mark.parametrize("name", list(SCALE_SETS))
-@pytest.mark.parametrize("form", ["per-worker", "all-rows", "all-rows-index-in-pass"])
+@pytest.mark.parametrize("form,name", FORMS)
 def test_quant_sum_matches_oracle(d, name, form):
     """Per-worker calls, and all rows in one call with the shared index from
     uq_shared_scale or (several scales) formed inside the call."""
     scales = SCALE_SETS[name]
-    if form == "all-rows-index-in-pass" and len(scales) == 1:
-        pytest.skip("one scale has no index to form")
     M = 5
     host = synth.mixed_rows(M, d, seed=d + 3, ldg=synth.round_up(d, 64))
     kw = dict(streamed=form == "per-worker", quant_sum=True)
@@ -168,19 +170,20 @@ def test_forced_scale_values(W):
     assert int(st.out[:d].view(torch.int32).abs().max()) == 0
 
 
-@pytest.mark.parametrize("M", [9, 12, 16])
+@pytest.mark.parametrize("M", [5, 6, 8, 9, 12, 16])
 @pytest.mark.parametrize("d", [1, 511, 513, 4097, 100_003])
 @pytest.mark.parametrize("name", ["s127", "s7"])
-def test_one_scale_rows_held_at_once(M, d, name):
-    """One scale with 9 to 16 rows set and reconstructed in one call runs the
-    form that holds every row of a tile at once; against the oracle."""
+def test_one_scale_rows_split_over_waves(M, d, name):
+    """One scale with 5 to 16 rows set and reconstructed in one call runs the
+    form that splits a tile's rows over a block's waves (two rows per wave up
+    to 8 rows, four beyond); against the oracle."""
     scales = SCALE_SETS[name]
     host = synth.mixed_rows(M, d, seed=M * 7 + d, ldg=synth.round_up(d, 64))
     st, _ = run_step(host, d, scales, seed=d + M, streamed=False, quant_sum=True)
     check_oracle(st, host, d, scales, seed=d + M)
 
 
-def test_rows_held_at_once_from_a_worker_offset():
+def test_rows_split_over_waves_from_a_worker_offset():
     """Rows 3..13 of 14 workers (11 rows, worker ids 3..13) in one call: the
     sums of those workers' codes and their reconstruction with M = 14."""
     d, M, seed = 50_001, 14, 21
@@ -198,9 +201,12 @@ def test_rows_held_at_once_from_a_worker_offset():
 
 
 @pytest.mark.parametrize("cap", [8, 24])
-def test_rows_held_at_once_capped_grids(cap):
-    d, M = 100_003, 16
-    host = synth.mixed_rows(M, d, seed=cap + 1, ldg=synth.round_up(d, 64))
+@pytest.mark.parametrize("M", [7, 16])
+def test_rows_split_over_waves_capped_grids(cap, M):
+    """Blocks striding over several tiles (their LDS sums alternate between
+    two buffers by tile); the results must not depend on the grid."""
+    d = 100_003
+    host = synth.mixed_rows(M, d, seed=cap + M, ldg=synth.round_up(d, 64))
     uq.uq_set_grid_cap(cap)
     try:
         st, _ = run_step(host, d, SCALE_SETS["s7"], seed=cap, streamed=False, quant_sum=True)
@@ -210,8 +216,9 @@ def test_rows_held_at_once_capped_grids(cap):
 
 
 @pytest.mark.parametrize("W", [0.0, float("inf"), float("nan"), 1e-45])
-def test_rows_held_at_once_forced_scale_values(W):
-    d, M = 5_003, 12
+@pytest.mark.parametrize("M", [6, 12])
+def test_rows_split_over_waves_forced_scale_values(W, M):
+    d = 5_003
     host = synth.gaussian_rows(M, d, seed=2, ldg=synth.round_up(d, 64))
     g = torch.from_numpy(host).to(DEV)
     st = Step(d, M, [127.0], device=DEV, streamed=False, quant_sum=True)
