@@ -71,11 +71,11 @@ struct IndexTables {
 // maxima's 16-bit keys [d] followed by one spare quad (padding; nothing is
 // stored there).  A block of the norm pass stores the keys of 1024
 // coordinates, 2 KiB, so with the keys 4 KiB aligned each store fills
-// aligned 2 KiB.  Measured on MI355X at 2^30 coordinates and 16 rows: key
-// buffers at multiples of 1024 bytes ran the pass up to 2.5% faster than
-// at other multiples of 256 in a work-free probe of its access pattern, and
-// the library's pass took 11.2 instead of 12.5 ms with its keys moved from
-// 768 to 3072 bytes past a 4 KiB boundary.
+// aligned 2 KiB.  Measured on MI355X at 2^30 coordinates and 16 rows, in a
+// work-free probe of the pass's access pattern: key buffers at multiples of
+// 1024 bytes ran up to 2.5% faster than at other multiples of 256.  (The
+// pass's time also depends on where the gradients lie in memory: 11.2 to
+// 12.5 ms on different boxes with these keys.)
 constexpr size_t kKeysAlign = 4096;
 
 struct FusedLayout {
