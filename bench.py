@@ -52,6 +52,29 @@ KERNEL_SOURCES = ["paper_2109_12497_amd/csrc/uq_kernels.hip", "paper_2109_12497_
                   "paper_2109_12497_amd/csrc/uq_launch.hpp", "paper_2109_12497_amd/csrc/uq_randk.hip"]
 
 
+# GlobalRandK's selection is bound by Philox arithmetic, not bytes: its
+# roofline counts Philox4x32-10 blocks.  A block is at least 40 VALU
+# instructions per lane (10 rounds of two 32x32->64 multiplies and two
+# three-input XORs); the chip issues 256 CUs x 4 SIMDs x 16 lanes per cycle at
+# 2.4 GHz, so at most 983 G blocks/s even with every instruction at full rate.
+PHILOX_BLOCK_MIN_INSTRUCTIONS = 40
+VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9
+PHILOX_PEAK_GBLOCKS = VALU_LANE_OPS_PER_S / PHILOX_BLOCK_MIN_INSTRUCTIONS / 1e9
+
+
+def selection_roofline(d: int, select_ms: float) -> dict:
+    """The selection's one key pass evaluates one Philox block (the keys' high
+    words) per four coordinates; the rare keys inside the bracket cost one
+    more block each, not counted.  Rate over the whole select call."""
+    blocks = (d + 3) // 4
+    achieved = blocks / (select_ms * 1e-3) / 1e9
+    return {"bound": "alu", "kernel": "k_rk_init+k_rk_collect+k_rk_sort", "stage": "select",
+            "achieved": round(achieved, 1), "peak": round(PHILOX_PEAK_GBLOCKS, 1), "unit": "G Philox blocks/s",
+            "frac": round(achieved / PHILOX_PEAK_GBLOCKS, 4), "traffic": None,
+            "algorithmic_blocks_per_launch": blocks, "avg_launch_us": round(select_ms * 1e3, 2),
+            "launches_per_step": 1}
+
+
 def code_bytes(d: int, bits: int) -> int:
     return (d * bits + 7) // 8
 
@@ -403,7 +426,7 @@ def bench_randk(args, g, cfg) -> int:
                    "quantizer": "multi" if len(scales) > 1 else "single",
                    "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
-        "stage_ms": stage_ms, "roofline": None, "cpu_baseline": base}
+        "stage_ms": stage_ms, "roofline": selection_roofline(d, stage_ms["select"]), "cpu_baseline": base}
     if parity is not None:
         result["parity_vs_oracle"] = parity
     print(json.dumps(result))

@@ -184,3 +184,13 @@ def test_parity_on_sample_reads_every_code_width(bits, scales, streamed):
         else:
             st.codes[1, 0] ^= 1
         assert bench.parity_on_sample(st, ref, d, d, bits) == "MISMATCH"
+
+
+def test_selection_roofline():
+    """GlobalRandK's selection is priced in Philox blocks (one per four
+    coordinates) against the issue-rate bound of 40 instructions per block."""
+    assert abs(bench.PHILOX_PEAK_GBLOCKS - 983.04) < 1e-6
+    r = bench.selection_roofline(11_173_962, 0.0285)
+    assert r["bound"] == "alu" and r["algorithmic_blocks_per_launch"] == 2_793_491
+    assert abs(r["achieved"] - 2_793_491 / 28.5e-6 / 1e9) < 0.1
+    assert abs(r["frac"] - r["achieved"] / 983.04) < 1e-3 and r["traffic"] is None

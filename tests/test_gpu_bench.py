@@ -91,6 +91,11 @@ def test_randk_bench_line():
         ("resnet18-grandk", d, m, 10_000)
     assert j["value"] == pytest.approx(m * d / (j["ms_per_step"] * 1e-3) / 1e9, rel=0.02)
     assert set(j["stage_ms"]) == {"select", "gather", "aggregate", "scatter"}
+    # the selection, bound by Philox arithmetic, carries an ALU roofline
+    roof = j["roofline"]
+    assert roof["bound"] == "alu" and roof["stage"] == "select" and roof["traffic"] is None
+    assert roof["achieved"] == pytest.approx((d + 3) // 4 / (j["stage_ms"]["select"] * 1e-3) / 1e9, rel=0.01)
+    assert 0 < roof["frac"] < 1
     base = j["cpu_baseline"]
     assert base["kind"] == "oracle" and base["cores"] >= 1 and base["value"] > 0
     assert base["sample"].startswith("full workload")
