@@ -123,12 +123,19 @@ def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, q
     ib = d if multi else 0
     cb = code_bytes(d, bits)
     qk = ("k_quantise_multi" if multi else "k_quantise_single") + ("" if bits == 8 else f"_{bits}bit")
-    if index_in_pass:
+    if index_in_pass and quant_sum:
         # W alone (the one-scale norm pass), then one call that reads every
         # row, writes the index it forms, the sums and the output
         return [dict(name="shared_scale", kernels=scale_kernels(M, 1), calls=1, bytes=shared_scale_bytes(d, M, 1)),
                 dict(name="index_quant_sum", kernels=["k_index_quant_sum"], calls=1,
                      bytes=4 * M * d + d + 4 * d + 4 * d)]
+    if index_in_pass:
+        # W alone, then one call that reads every row and writes the index it
+        # forms and every row's codes, then the sum with the reconstruction
+        iq = "k_index_quantise" + ("" if bits == 8 else f"_{bits}bit")
+        return [dict(name="shared_scale", kernels=scale_kernels(M, 1), calls=1, bytes=shared_scale_bytes(d, M, 1)),
+                dict(name="index_quantize", kernels=[iq], calls=1, bytes=4 * M * d + d + M * cb),
+                dict(name="sum_dequantize", kernels=["k_sum_dequant"], calls=1, bytes=M * cb + 4 * d + 4 * d + ib)]
     st = [dict(name="shared_scale", kernels=scale_kernels(M, K), calls=1, bytes=shared_scale_bytes(d, M, K))]
     if quant_sum and streamed:
         # one worker per call into the running sum; the last call reconstructs
@@ -477,6 +484,7 @@ def stage_fns(step, g, seed: int, M: int) -> dict:
     return {
         "shared_scale": lambda: step.shared_scale(g, w_only=step.index_in_pass),
         "index_quant_sum": lambda: step.index_quantize_sum(g, seed),
+        "index_quantize": lambda: step.index_quantize(g, seed),
         "quant_sum_first": lambda: step.quantize_sum(g[0:1], seed, rows=1, worker0=0, accumulate=0,
                                                      reconstruct=False),
         "quant_sum": ((lambda: step.quantize_sum(g[1:2], seed, rows=1, worker0=1, accumulate=1, reconstruct=False))
@@ -605,8 +613,10 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "d": d, "M": M, "scales": scales, "seed": seed,
                    "quantizer": "multi" if K > 1 else "single", "streamed": streamed, "code_bits": bits,
-                   "path": ("quantise-and-sum fused, index formed in it" if step.index_in_pass
-                            else "quantise-and-sum fused" if quant_sum else "codes stored, then summed"),
+                   "path": ("quantise-and-sum fused, index formed in it" if step.index_in_pass and quant_sum
+                            else "quantise-and-sum fused" if quant_sum
+                            else "codes stored with the index formed in the quantiser, then summed"
+                            if step.index_in_pass else "codes stored, then summed"),
                    "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
         "pct_hbm_peak": round(100 * step_bytes / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),

@@ -245,6 +245,34 @@ int uq_index_quantize_sum(const float* g, int64_t d, int32_t M, int64_t ldg, con
                           const float* scales, int32_t K, uint64_t seed, uint8_t* idx,
                           int32_t* sum, float* out, void* stream);
 
+/*
+ * The shared scale index of Sec. 3.2 (the rule of Eq. (11) with scale
+ * sharing) formed inside the multi-scale quantiser over all M workers, with
+ * every worker's codes stored: Eq. (12) and the code of Sec. 3.2, as int8 or
+ * as the 4- or 2-bit fields of uq_quantize_packed.  Bit for bit the idx of
+ * uq_shared_scale followed by uq_quantize_multi (bits = 8) or
+ * uq_quantize_packed (bits = 4, 2) over all M rows with worker0 = 0, given
+ * the same W.  As in uq_index_quantize_sum, every row of a tile is held in
+ * registers, so each coordinate's index comes from its exact largest usable
+ * |g|; uq_shared_scale then only has to form W (call it with K = 1 and
+ * idx = NULL).
+ *   g        [M][ldg] fp32, 1 <= M <= 16; row m is worker m
+ *   w        device pointer to W (one fp32, read)
+ *   scales   host array of K floats, 1 <= K <= UQ_MAX_SCALES, as for
+ *            uq_quantize_multi; with bits < 8 the smallest must fit the field
+ *            (s_0 <= 7 for 4 bits, s_0 <= 1 for 2 bits)
+ *   bits     8, 4 or 2
+ *   idx      [d] uint8 (written): k*_i in 0..K-1
+ *   codes    [M][ldc] bytes (written): int8 codes, or packed fields in the
+ *            layout of uq_quantize_packed (ldc >= ceil(d * bits / 8))
+ *   ldc      code row stride in bytes, a multiple of 16
+ * The checks of uq_quantize_multi / uq_quantize_packed apply; M > 16
+ * returns UQ_ERANGE (use uq_shared_scale and the quantiser there).
+ */
+int uq_index_quantize(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
+                      const float* scales, int32_t K, uint64_t seed, int32_t bits, uint8_t* idx,
+                      void* codes, int64_t ldc, void* stream);
+
 /* ------------------------------------------------------------------------
  * Sub-byte codes.  The paper stores every code in 8 bits because its
  * framework had no narrower type, and found bit-packing too slow (Sec. 5,

@@ -63,6 +63,7 @@ def _load() -> ctypes.CDLL:
     L.uq_quantize_packed.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i64, P]
     L.uq_quantize_sum.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i32, P, P]
     L.uq_index_quantize_sum.argtypes = [P, i64, i32, i64, P, P, i32, u64, P, P, P, P]
+    L.uq_index_quantize.argtypes = [P, i64, i32, i64, P, P, i32, u64, i32, P, P, i64, P]
     L.uq_sum_packed.argtypes = [P, i64, i32, i64, i32, i32, P, P]
     L.uq_randk_workspace_bytes.argtypes = [i64, i64]
     L.uq_randk_workspace_bytes.restype = sz
@@ -77,7 +78,7 @@ def _load() -> ctypes.CDLL:
     L.uq_last_error.restype = ctypes.c_char_p
     for name in ("uq_shared_scale", "uq_shared_scale_noalloc", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
                  "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_quantize_sum",
-                 "uq_index_quantize_sum",
+                 "uq_index_quantize_sum", "uq_index_quantize",
                  "uq_randk_select", "uq_gather",
                  "uq_scatter", "uq_set_grid_cap", "uq_set_randk_mode"):
         getattr(L, name).restype = ctypes.c_int
@@ -208,6 +209,12 @@ def uq_index_quantize_sum(g, d, M, ldg, w, scales, K, seed, idx, sum, out, strea
     hs = _host_scales(scales)
     _check(lib.uq_index_quantize_sum(_ptr(g), d, M, ldg, _ptr(w), hs.ptr, K, seed, _ptr(idx), _ptr(sum), _ptr(out),
                                      _stream(stream)))
+
+
+def uq_index_quantize(g, d, M, ldg, w, scales, K, seed, bits, idx, codes, ldc, stream=None) -> None:
+    hs = _host_scales(scales)
+    _check(lib.uq_index_quantize(_ptr(g), d, M, ldg, _ptr(w), hs.ptr, K, seed, bits, _ptr(idx), _ptr(codes), ldc,
+                                 _stream(stream)))
 
 
 def uq_sum_packed(packed, d, rows, ldp, bits, accumulate, sum, stream=None) -> None:

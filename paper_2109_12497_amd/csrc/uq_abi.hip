@@ -470,6 +470,29 @@ int uq_index_quantize_sum(const float* g, int64_t d, int32_t M, int64_t ldg, con
                                                static_cast<hipStream_t>(stream)));
 }
 
+int uq_index_quantize(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w, const float* scales,
+                      int32_t K, uint64_t seed, int32_t bits, uint8_t* idx, void* codes, int64_t ldc, void* stream)
+{
+    if (bits != 8 && bits != 4 && bits != 2)
+        return fail(UQ_ERANGE, "bits = %d is not 8, 4 or 2", bits);
+    uq::ScaleSet S;
+    UQ_TRY(check_scales(scales, K, &S));
+    if (bits < 8 && S.s[0] > static_cast<float>((1 << (bits - 1)) - 1))
+        return fail(UQ_ERANGE, "smallest scale %g does not fit a %d-bit code", (double)S.s[0], bits);
+    UQ_TRY(check_dims(d, M, "M"));
+    if (M > uq::kFuseRows)
+        return fail(UQ_ERANGE, "M = %d exceeds the %d rows held in registers", M, uq::kFuseRows);
+    UQ_TRY(check_rows(g, d, M, ldg, 4, "g"));
+    const int64_t row_bytes = (d * bits + 7) / 8;
+    UQ_TRY(check_rows(codes, row_bytes, M, ldc, 16, "codes"));
+    UQ_TRY(check_w(w));
+    if (idx == nullptr && d > 0)
+        return fail(UQ_EINVAL, "idx is NULL");
+    UQ_TRY(check_vec(idx, d > 0 ? d : 1, "idx"));
+    return launched(uq::launch_index_quantise(g, d, M, ldg, w, S, seed, bits, idx, static_cast<uint8_t*>(codes), ldc,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 size_t uq_randk_workspace_bytes(int64_t d, int64_t K)
 {
     (void)d;

@@ -1693,6 +1693,85 @@ __device__ __forceinline__ float max3_abs(float m, float x, float y)
 // INDEX: form the tile's shared index (several scales) and store it; else
 // one scale, every index 0.  The first `rows` rows are quantised, row r as
 // worker worker0 + r.
+// The shared index of a lane's eight coordinates of one tile (A quad, then B
+// quad) from the largest usable |g| over the ROWS rows it holds: two rows per
+// instruction with the NaN- and infinity-propagating maximum; a result that
+// is not finite means some value was not usable (infinite or NaN), and then
+// the lane forms the largest usable |g| value by value.  Then the exponent
+// table (by_table) or K threshold compares.
+template <int ROWS>
+__device__ __forceinline__ void tile_index(const f32x4 (&A)[ROWS], const f32x4 (&B)[ROWS], const uint2* tab,
+                                           bool by_table, const float* thr, int32_t K, bool zero, uint32_t k[8])
+{
+    float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    static_assert(ROWS % 2 == 0, "rows are taken in pairs");
+#pragma unroll
+    for (int r = 0; r < ROWS; r += 2) {
+        a[0] = max3_abs(a[0], A[r].x, A[r + 1].x);
+        a[1] = max3_abs(a[1], A[r].y, A[r + 1].y);
+        a[2] = max3_abs(a[2], A[r].z, A[r + 1].z);
+        a[3] = max3_abs(a[3], A[r].w, A[r + 1].w);
+        a[4] = max3_abs(a[4], B[r].x, B[r + 1].x);
+        a[5] = max3_abs(a[5], B[r].y, B[r + 1].y);
+        a[6] = max3_abs(a[6], B[r].z, B[r + 1].z);
+        a[7] = max3_abs(a[7], B[r].w, B[r + 1].w);
+    }
+    uint32_t worst = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        worst = max(worst, __float_as_uint(a[j]));
+    if (__builtin_expect(worst >= 0x7F800000u, 0)) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            a[j] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            a[0] = fmaxf(a[0], usable_or_zero(A[r].x));
+            a[1] = fmaxf(a[1], usable_or_zero(A[r].y));
+            a[2] = fmaxf(a[2], usable_or_zero(A[r].z));
+            a[3] = fmaxf(a[3], usable_or_zero(A[r].w));
+            a[4] = fmaxf(a[4], usable_or_zero(B[r].x));
+            a[5] = fmaxf(a[5], usable_or_zero(B[r].y));
+            a[6] = fmaxf(a[6], usable_or_zero(B[r].z));
+            a[7] = fmaxf(a[7], usable_or_zero(B[r].w));
+        }
+    }
+    if (by_table) {
+        const uint32_t kzero = static_cast<uint32_t>(K - 1);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t b = __float_as_uint(a[j]);
+            const uint2 t = tab[b >> 23];
+            k[j] = b != 0u ? t.x + (b <= t.y ? 1u : 0u) : kzero;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            int32_t count = 0;
+            for (int q = 0; q < K; ++q)
+                count += a[j] <= thr[q] ? 1 : 0;
+            k[j] = index_from_count(a[j], count, K, zero);
+        }
+    }
+}
+
+// Stores a lane's eight index bytes of one tile: the A quad's at a_off, the B
+// quad's at a_off + 256.
+template <bool NT>
+__device__ __forceinline__ void store_index(uint8_t* __restrict__ idx, int64_t a_off, const uint32_t k[8])
+{
+    const uint32_t ka = k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24);
+    const uint32_t kb = k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24);
+    uint32_t* ip = reinterpret_cast<uint32_t*>(idx + a_off);
+    if (NT) {
+        __builtin_nontemporal_store(ka, ip);
+        __builtin_nontemporal_store(kb, ip + 64);
+    } else {
+        ip[0] = ka;
+        ip[64] = kb;
+    }
+}
+
 template <int ROWS, bool PRE, bool NT, bool INDEX>
 __device__ __forceinline__ void index_quant_sum_tile(const f32x4 (&A)[ROWS], const f32x4 (&B)[ROWS], int32_t rows,
                                                      uint32_t worker0, int64_t T, const uint2* tab, bool by_table,
@@ -1705,69 +1784,8 @@ __device__ __forceinline__ void index_quant_sum_tile(const f32x4 (&A)[ROWS], con
     const int64_t a_off = (T << 9) + 4 * lane;
     uint32_t k[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
     if (INDEX) {
-        // the largest |g| over the rows, two rows per instruction; a result that
-        // is not finite means some value was not usable (infinite or NaN), and
-        // then the lane forms the largest usable |g| value by value
-        float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-        static_assert(ROWS % 2 == 0, "rows are taken in pairs");
-#pragma unroll
-        for (int r = 0; r < ROWS; r += 2) {
-            a[0] = max3_abs(a[0], A[r].x, A[r + 1].x);
-            a[1] = max3_abs(a[1], A[r].y, A[r + 1].y);
-            a[2] = max3_abs(a[2], A[r].z, A[r + 1].z);
-            a[3] = max3_abs(a[3], A[r].w, A[r + 1].w);
-            a[4] = max3_abs(a[4], B[r].x, B[r + 1].x);
-            a[5] = max3_abs(a[5], B[r].y, B[r + 1].y);
-            a[6] = max3_abs(a[6], B[r].z, B[r + 1].z);
-            a[7] = max3_abs(a[7], B[r].w, B[r + 1].w);
-        }
-        uint32_t worst = 0u;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            worst = max(worst, __float_as_uint(a[j]));
-        if (__builtin_expect(worst >= 0x7F800000u, 0)) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                a[j] = 0.0f;
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-                a[0] = fmaxf(a[0], usable_or_zero(A[r].x));
-                a[1] = fmaxf(a[1], usable_or_zero(A[r].y));
-                a[2] = fmaxf(a[2], usable_or_zero(A[r].z));
-                a[3] = fmaxf(a[3], usable_or_zero(A[r].w));
-                a[4] = fmaxf(a[4], usable_or_zero(B[r].x));
-                a[5] = fmaxf(a[5], usable_or_zero(B[r].y));
-                a[6] = fmaxf(a[6], usable_or_zero(B[r].z));
-                a[7] = fmaxf(a[7], usable_or_zero(B[r].w));
-            }
-        }
-        if (by_table) {
-            const uint32_t kzero = static_cast<uint32_t>(K - 1);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t b = __float_as_uint(a[j]);
-                const uint2 t = tab[b >> 23];
-                k[j] = b != 0u ? t.x + (b <= t.y ? 1u : 0u) : kzero;
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                int32_t count = 0;
-                for (int q = 0; q < K; ++q)
-                    count += a[j] <= thr[q] ? 1 : 0;
-                k[j] = index_from_count(a[j], count, K, zero);
-            }
-        }
-        const uint32_t ka = k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24);
-        const uint32_t kb = k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24);
-        uint32_t* ip = reinterpret_cast<uint32_t*>(idx + a_off);
-        if (NT) {
-            __builtin_nontemporal_store(ka, ip);
-            __builtin_nontemporal_store(kb, ip + 64);
-        } else {
-            ip[0] = ka;
-            ip[64] = kb;
-        }
+        tile_index<ROWS>(A, B, tab, by_table, thr, K, zero, k);
+        store_index<NT>(idx, a_off, k);
     }
     float inv[8];
 #pragma unroll
@@ -1953,6 +1971,190 @@ __global__ __launch_bounds__(kBlock) void k_index_quant_sum(const float* __restr
     }
     if (blockIdx.x == 0 && threadIdx.x < 64)
         index_quant_sum_tail(g, d, ldg, M, ntiles, thr_s, K, zero, inv_s, s0, key0, key1, idx, sum, deq_s, out);
+}
+
+// ---------------------------------------------------------------------------
+// The shared index formed in the quantiser (several scales, at most 16 rows,
+// codes stored): k_index_quant_sum's tiles, every row of a tile held by one
+// wave and the index formed from their exact maxima and stored, with each
+// row's codes stored (int8, or packed 4- or 2-bit fields) instead of summed.
+// The codes and the index equal uq_shared_scale's index followed by the
+// quantiser's codes, given the same W.
+// ---------------------------------------------------------------------------
+template <int ROWS, int BITS, bool PRE, bool NT>
+__device__ __forceinline__ void index_quantise_tile(const f32x4 (&A)[ROWS], const f32x4 (&B)[ROWS], int32_t rows,
+                                                    int64_t T, const uint2* tab, bool by_table, const float* thr,
+                                                    int32_t K, bool zero, const float* inv_t, float s0x,
+                                                    uint32_t key0, uint32_t key1, uint32_t one2,
+                                                    uint8_t* __restrict__ idx, uint8_t* __restrict__ codes,
+                                                    int64_t ldc)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t a_off = (T << 9) + 4 * lane;
+    uint32_t k[8];
+    tile_index<ROWS>(A, B, tab, by_table, thr, K, zero, k);
+    store_index<NT>(idx, a_off, k);
+    float inv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        inv[j] = inv_t[k[j]];
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        if (r < rows) {
+            const float v[8] = {A[r].x, A[r].y, A[r].z, A[r].w, B[r].x, B[r].y, B[r].z, B[r].w};
+            uint32_t p[4];
+            tile_codes<PRE>(v, inv, s0x, T, static_cast<uint32_t>(r), key0, key1, one2, p);
+            uint8_t* row = codes + static_cast<int64_t>(r) * ldc;
+            store_pairs<BITS, NT>(row, a_off, p[0], p[1]);
+            store_pairs<BITS, NT>(row, a_off + 256, p[2], p[3]);
+        }
+    }
+}
+
+// The coordinates past the last whole tile (fewer than 512): lane t of one
+// wave takes the 8 contiguous coordinates of group ntiles * 64 + t, forms
+// their indices from the rows' maxima (threshold counts), then quantises and
+// stores every row's codes.  inv_s holds s_k / W (not scaled).
+template <int BITS>
+__device__ __forceinline__ void index_quantise_tail(const float* __restrict__ g, int64_t d, int64_t ldg, int32_t M,
+                                                    int64_t ntiles, const float* thr, int32_t K, bool zero,
+                                                    const float* inv_s, float s0, uint32_t key0, uint32_t key1,
+                                                    uint8_t* __restrict__ idx, uint8_t* __restrict__ codes,
+                                                    int64_t ldc)
+{
+    const int64_t q = (ntiles << 6) + (threadIdx.x & 63);
+    const int64_t base = q << 3;
+    if (base >= d)
+        return;
+    float a[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    for (int32_t r = 0; r < M; ++r) {
+        const float* row = g + static_cast<int64_t>(r) * ldg;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            a[j] = fmaxf(a[j], usable_or_zero(base + j < d ? row[base + j] : 0.0f));
+    }
+    float inv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        int32_t count = 0;
+        for (int k = 0; k < K; ++k)
+            count += a[j] <= thr[k] ? 1 : 0;
+        const uint32_t kk = index_from_count(a[j], count, K, zero);
+        inv[j] = inv_s[kk];
+        if (base + j < d)
+            idx[base + j] = static_cast<uint8_t>(kk);
+    }
+    for (int32_t r = 0; r < M; ++r) {
+        const float* row = g + static_cast<int64_t>(r) * ldg;
+        uint8_t* out = codes + static_cast<int64_t>(r) * ldc;
+        float v[8];
+        int32_t code[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            v[j] = base + j < d ? row[base + j] : 0.0f;
+        quantise_group(v, inv, s0, static_cast<uint64_t>(q), static_cast<uint32_t>(r), key0, key1, code);
+        if (BITS == 8) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (base + j < d)
+                    out[base + j] = static_cast<uint8_t>(code[j]);
+        } else if (BITS == 4) {
+            // the group's 8 codes fill whole bytes of its own (codes past d are 0)
+            *reinterpret_cast<uint32_t*>(out + base / 2) = pack_field<4>(code) | (pack_field<4>(code + 4) << 16);
+        } else {
+            *reinterpret_cast<uint16_t*>(out + base / 4) =
+                static_cast<uint16_t>(pack_field<2>(code) | (pack_field<2>(code + 4) << 8));
+        }
+    }
+}
+
+template <int ROWS, int BITS, bool NT>
+__global__ __launch_bounds__(kBlock) void k_index_quantise(const float* __restrict__ g, int64_t d, int32_t M,
+                                                           int64_t ldg, const float* __restrict__ wptr, ScaleSet S,
+                                                           uint32_t key0, uint32_t key1, uint8_t* __restrict__ idx,
+                                                           uint8_t* __restrict__ codes, int64_t ldc)
+{
+    __shared__ float inv_s[kMaxScales];  // s_k / W
+    __shared__ float inv_p[kMaxScales];  // s_k / W * 2^16 when pre
+    __shared__ float thr_s[kMaxScales];  // T_k
+    __shared__ uint2 tab_s[256];
+    const int lane = threadIdx.x & 63;
+    const int64_t ntiles = d >> 9;
+    const int32_t wave_in_block = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(threadIdx.x >> 6));
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave_in_block;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * (kBlock / 64);
+
+    // every row of the first tile goes out before W is read and the tables
+    // are formed
+    f32x4 A[ROWS], B[ROWS];
+    const auto load_rows = [&](int64_t T) {
+        const int64_t a_off = (T << 9) + 4 * lane;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            const float* row = g + static_cast<int64_t>(r < M ? r : M - 1) * ldg;
+            A[r] = load_nt(row + a_off);
+            B[r] = load_nt(row + a_off + 256);
+        }
+    };
+    if (first < ntiles)
+        load_rows(first);
+
+    const float W = *wptr;
+    const float s0 = S.s[0];
+    const int32_t K = S.K;
+    const float q0 = div_rn32(s0, W);
+    const bool zero = zero_path(W, q0);
+    const bool pre = zero || div_rn32(S.s_last, W) <= 0x1p100f;
+    if (threadIdx.x < K) {
+        const float inv = zero ? 0.0f : div_rn32(S.s[threadIdx.x], W);
+        inv_s[threadIdx.x] = inv;
+        inv_p[threadIdx.x] = pre ? inv * 65536.0f : inv;
+        thr_s[threadIdx.x] = zero ? 0.0f : index_threshold(inv, s0);
+    }
+    __syncthreads();
+    // thread e forms the table's entry e, as in k_index_quant_sum
+    int crowded = 0;
+    {
+        const uint32_t e = threadIdx.x;
+        int32_t above = 0, inside = 0;
+        uint32_t tin = 0u;
+        for (int k = 0; k < K; ++k) {
+            const uint32_t tb = __float_as_uint(thr_s[k]);
+            above += (tb >> 23) > e ? 1 : 0;
+            if ((tb >> 23) == e) {
+                ++inside;
+                tin = tb;
+            }
+        }
+        uint2 ent;
+        if (zero) {
+            ent.x = static_cast<uint32_t>(K - 2);
+            ent.y = 0xFFFFFFFFu;
+        } else {
+            crowded = inside > 1 ? 1 : 0;
+            const bool limit = inside > 0 && above > 0;
+            ent.x = static_cast<uint32_t>(above > 0 ? above - 1 : 0) - (limit ? 0u : 1u);
+            ent.y = limit ? tin : 0xFFFFFFFFu;
+        }
+        tab_s[e] = ent;
+    }
+    const bool by_table = __syncthreads_or(crowded) == 0;
+    uint32_t one2 = 0x00010001u;
+    asm("" : "+s"(one2));
+    const float s0x = pre ? s0 * 65536.0f : s0;
+
+    for (int64_t T = first; T < ntiles; T += stride) {
+        if (T != first)
+            load_rows(T);
+        if (pre)
+            index_quantise_tile<ROWS, BITS, true, NT>(A, B, M, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x, key0,
+                                                      key1, one2, idx, codes, ldc);
+        else
+            index_quantise_tile<ROWS, BITS, false, NT>(A, B, M, T, tab_s, by_table, thr_s, K, zero, inv_p, s0x, key0,
+                                                       key1, one2, idx, codes, ldc);
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 64)
+        index_quantise_tail<BITS>(g, d, ldg, M, ntiles, thr_s, K, zero, inv_s, s0, key0, key1, idx, codes, ldc);
 }
 
 // ---------------------------------------------------------------------------
@@ -2337,6 +2539,50 @@ hipError_t launch_index_quant_sum(const float* g, int64_t d, int32_t M, int64_t 
     else
         UQ_LAUNCH_IQS(16);
 #undef UQ_LAUNCH_IQS
+    return hipGetLastError();
+}
+
+hipError_t launch_index_quantise(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
+                                 const ScaleSet& S, uint64_t seed, int32_t bits, uint8_t* idx, uint8_t* codes,
+                                 int64_t ldc, hipStream_t stream)
+{
+    if (d == 0)
+        return hipSuccess;
+    const uint32_t key0 = static_cast<uint32_t>(seed);
+    const uint32_t key1 = static_cast<uint32_t>(seed >> 32);
+    const dim3 grid(one_shot(d >> 9, kBlock / 64));
+    // codes stored nontemporally past the quantiser's threshold, the index with them
+    const bool nt = static_cast<int64_t>(M) * ((d * bits + 7) / 8) > kCodesNontemporalBytes;
+#define UQ_LAUNCH_IQ_(ROWS, BITS, NT)                                                                             \
+    hipLaunchKernelGGL((k_index_quantise<ROWS, BITS, NT>), grid, dim3(kBlock), 0, stream, g, d, M, ldg, w, S, key0, \
+                       key1, idx, codes, ldc)
+#define UQ_LAUNCH_IQ_B(ROWS, NT)              \
+    do {                                      \
+        if (bits == 8)                        \
+            UQ_LAUNCH_IQ_(ROWS, 8, NT);       \
+        else if (bits == 4)                   \
+            UQ_LAUNCH_IQ_(ROWS, 4, NT);       \
+        else                                  \
+            UQ_LAUNCH_IQ_(ROWS, 2, NT);       \
+    } while (0)
+#define UQ_LAUNCH_IQ(ROWS)                   \
+    do {                                     \
+        if (nt)                              \
+            UQ_LAUNCH_IQ_B(ROWS, true);      \
+        else                                 \
+            UQ_LAUNCH_IQ_B(ROWS, false);     \
+    } while (0)
+    if (M <= 2)
+        UQ_LAUNCH_IQ(2);
+    else if (M <= 4)
+        UQ_LAUNCH_IQ(4);
+    else if (M <= 8)
+        UQ_LAUNCH_IQ(8);
+    else
+        UQ_LAUNCH_IQ(16);
+#undef UQ_LAUNCH_IQ
+#undef UQ_LAUNCH_IQ_B
+#undef UQ_LAUNCH_IQ_
     return hipGetLastError();
 }
 

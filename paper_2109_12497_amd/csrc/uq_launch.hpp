@@ -143,6 +143,11 @@ hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg
 hipError_t launch_index_quant_sum(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
                                   const ScaleSet& S, uint64_t seed, uint8_t* idx, int32_t* sum, float* out,
                                   hipStream_t stream);
+// several scales, M <= 16 rows: the shared index formed from the rows'
+// maxima (stored to idx) and every row's codes stored (bits 8, 4 or 2)
+hipError_t launch_index_quantise(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
+                                 const ScaleSet& S, uint64_t seed, int32_t bits, uint8_t* idx, uint8_t* codes,
+                                 int64_t ldc, hipStream_t stream);
 hipError_t launch_sum_packed(const uint8_t* packed, int64_t d, int32_t rows, int64_t ldp, int32_t bits,
                              int32_t accumulate, int32_t* sum, hipStream_t stream);
 hipError_t launch_sum(const int8_t* codes, int64_t d, int32_t rows, int64_t ldc, int32_t accumulate,

@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import torch
 
-from . import (_stream, uq_dequantize, uq_gather, uq_index_quantize_sum, uq_quantize_multi, uq_quantize_packed,
+from . import (_stream, uq_dequantize, uq_gather, uq_index_quantize, uq_index_quantize_sum, uq_quantize_multi, uq_quantize_packed,
                uq_quantize_single, uq_quantize_sum, uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale,
                uq_sum_codes, uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
 
@@ -32,10 +32,12 @@ class Step:
     (uq_quantize_sum) and never stored: one call per worker when streamed
     (the last one also reconstructs), one call for all workers otherwise.
     The default is True for a streamed step with fused=True, else False.
-    index_in_pass=True (all rows in one call, several scales, M <= 16): the
-    shared index is formed inside that call from the rows it holds
-    (uq_index_quantize_sum), so the shared-scale call forms W only.  The
-    default is True exactly when those conditions hold.
+    index_in_pass=True (resident rows, several scales, M <= 16): the shared
+    index is formed inside the call that quantises every row, from the rows
+    it holds (uq_index_quantize_sum with quant_sum, else uq_index_quantize,
+    which stores the codes), so the shared-scale call forms W only.  The
+    default is True when those conditions hold with quant_sum or with packed
+    codes; int8 codes stored keep the separate index pass unless asked.
     """
 
     def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None,
@@ -47,9 +49,10 @@ class Step:
         assert not (self.quant_sum and not fused), "quant_sum reconstructs in the same pass (fused)"
         self.scales = [float(s) for s in scales]
         self.K = len(self.scales)
-        can = self.quant_sum and not streamed and self.K > 1 and 1 <= M <= 16
-        self.index_in_pass = can if index_in_pass is None else index_in_pass
-        assert not (self.index_in_pass and not can), "index_in_pass needs all rows in one quant_sum call, K > 1, M <= 16"
+        can = not streamed and self.K > 1 and 1 <= M <= 16
+        default = can and (self.quant_sum or bits != 8)
+        self.index_in_pass = default if index_in_pass is None else index_in_pass
+        assert not (self.index_in_pass and not can), "index_in_pass needs resident rows, K > 1, M <= 16"
         self.streamed = streamed
         self.bits = bits
         row_bytes = (max(d, 1) * bits + 7) // 8
@@ -104,6 +107,10 @@ class Step:
         uq_quantize_sum(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed,
                         accumulate, self.sum, self.M, self.out if reconstruct else None, stream)
 
+    def index_quantize(self, g, seed: int, stream=None):
+        uq_index_quantize(g, self.d, self.M, g.stride(0), self.w, self.scales, self.K, seed, self.bits, self.idx,
+                          self.codes, self.codes.stride(0), stream)
+
     def index_quantize_sum(self, g, seed: int, stream=None):
         uq_index_quantize_sum(g, self.d, self.M, g.stride(0), self.w, self.scales, self.K, seed, self.idx, self.sum,
                               self.out, stream)
@@ -124,8 +131,14 @@ class Step:
         assert g.stride(1) == 1 and g.shape[1] >= self.d
         stream = _stream(stream)  # resolved once for the step's calls
         self.shared_scale(g, stream, w_only=self.index_in_pass)
-        if self.index_in_pass:
+        if self.index_in_pass and self.quant_sum:
             self.index_quantize_sum(g, seed, stream=stream)
+        elif self.index_in_pass:
+            self.index_quantize(g, seed, stream=stream)
+            if self.fused:
+                self.sum_dequantize(stream=stream)
+            else:
+                self.sum_codes(stream=stream)
         elif self.quant_sum and self.streamed:
             for m in range(self.M):
                 self.quantize_sum(g[m:m + 1], seed, rows=1, worker0=m, accumulate=1 if m > 0 else 0,

@@ -293,6 +293,34 @@ def test_index_quantize_sum_accepts_valid_no_ops():
     assert status_iqs(d=0, M=16) == uq.UQ_OK
 
 
+def status_iq(g=A, d=1000, M=4, ldg=1024, w=A, scales=(7.0, 112.0, 1792.0, 28672.0), K=4, seed=5, bits=4,
+              idx=A, codes=A, ldc=512):
+    hs = uq._HostScales(list(scales)) if scales is not None else None
+    return L.uq_index_quantize(g, d, M, ldg, w, hs.ptr if hs else None, K, seed, bits, idx, codes, ldc, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(g=None), "inval"), (dict(w=None), "inval"), (dict(w=A + 2), "align"), (dict(d=-1), "inval"),
+    (dict(M=0), "inval"), (dict(M=17), "range"), (dict(ldg=96), "inval"), (dict(ldg=1026), "align"),
+    (dict(g=A + 8), "align"), (dict(idx=None), "inval"), (dict(idx=A + 4), "align"), (dict(K=0), "range"),
+    (dict(scales=None), "inval"), (dict(bits=3), "range"), (dict(bits=16), "range"),
+    (dict(scales=(8.0, 128.0), K=2), "range"), (dict(bits=2, scales=(3.0, 48.0), K=2), "range"),
+    (dict(bits=8, scales=(128.0, 2048.0), K=2), "range"), (dict(codes=None), "inval"), (dict(codes=A + 4), "align"),
+    (dict(ldc=496), "inval"), (dict(ldc=504), "align"), (dict(bits=8, ldc=992), "inval"),
+])
+def test_index_quantize_rejects(kw, want):
+    """Argument checks of the index-forming quantiser with stored codes; d =
+    1000 needs 500 bytes per row of 4-bit codes, 1000 of int8 codes."""
+    assert status_iq(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
+def test_index_quantize_accepts_valid_no_ops():
+    assert status_iq(d=0) == uq.UQ_OK
+    assert status_iq(d=0, bits=8, scales=(127.0, 2032.0), K=2) == uq.UQ_OK
+    assert status_iq(d=0, bits=2, scales=(1.0, 16.0), K=2, M=16) == uq.UQ_OK
+
+
 def test_binding_raises_with_detail():
     with pytest.raises(uq.UQError) as e:
         uq.uq_quantize_single(A, 100, 2, 128, 0, A, 200, 1, A, 128, stream=0)

@@ -49,6 +49,23 @@ def test_index_in_pass_bytes(M):
     assert [s["kernels"] for s in st] == [["k_sumsq", "k_finish"], ["k_index_quant_sum"]]
 
 
+@pytest.mark.parametrize("M,bits", [(2, 4), (16, 4), (8, 2), (16, 8)])
+def test_index_quantize_bytes(M, bits):
+    """Several scales, codes stored, the index formed in the quantiser: the
+    one-scale norm pass (4M), the rows in and the index and every row's codes
+    out (4M + 1 + M b/8), then the codes, the index and the sums / output of
+    the sum with the reconstruction (M b/8 + 1 + 8)."""
+    d = 1 << 20
+    cb = d * bits // 8
+    b = bench.algorithmic_bytes(d, M, 4, False, bits, False, True)
+    assert b["shared_scale"] == 4 * M * d and b["index_quantize"] == 4 * M * d + d + M * cb
+    assert b["sum_dequantize"] == M * cb + 9 * d
+    assert b["total"] == 8 * M * d + 10 * d + 2 * M * cb
+    st = bench.plan_stages(d, M, 4, bits, False, False, True)
+    kq = "k_index_quantise" + ("" if bits == 8 else f"_{bits}bit")
+    assert [s["kernels"] for s in st] == [["k_sumsq", "k_finish"], [kq], ["k_sum_dequant"]]
+
+
 def test_streamed_bytes():
     d, M, K = 1 << 20, 16, 8
     # codes stored, then summed: the quantiser row by row (the index read by
