@@ -24,7 +24,8 @@ sample checked against the oracle's.  Extra modes:
   --composed            codes stored, then summed (separate calls)
   --index-pass          resident workers, several scales: the shared index
                         from the shared-scale call's own pass, not formed
-                        inside the quantise-and-sum
+                        inside the quantise-and-sum (or, with packed codes,
+                        inside the quantiser)
   --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
@@ -513,7 +514,7 @@ def main() -> int:
                          "quantise-and-sum (packed-code workloads always store their codes)")
     ap.add_argument("--index-pass", action="store_true",
                     help="resident workers with several scales: the shared index from the shared-scale call's own "
-                         "pass instead of formed inside the quantise-and-sum")
+                         "pass instead of formed inside the quantise-and-sum or, with packed codes, the quantiser")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work to aim for, for each of the two CPU figures")
