@@ -234,8 +234,8 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 // ---------------------------------------------------------------------------
 // Fused shared scale for several scales and at most kFuseRows rows: one pass
 // over the gradients forms the rows' tile sums of squares and, at every
-// coordinate, the top 16 bits of the largest usable |g| over the rows (a
-// key, uint16 [d] in the workspace); the index pass then reads the keys
+// coordinate, bits 30..15 of the largest usable |g| over the rows (a key,
+// uint16 [d] in the workspace); the index pass then reads the keys
 // instead of the M rows, and the rows of the rare coordinates whose key
 // equals a threshold's.
 //   k_norm_max   block t: tile t of every row (below)
@@ -296,7 +296,7 @@ __device__ __forceinline__ void norm_max_tail(const float* __restrict__ g, int64
         float mt = 0.0f;
         for (int32_t m = 0; m < M; ++m)
             mt = fmaxf(mt, usable_or_zero(g[static_cast<int64_t>(m) * ldg + tail]));
-        keys[tail] = static_cast<uint16_t>(__builtin_bit_cast(uint32_t, mt) >> 16);
+        keys[tail] = static_cast<uint16_t>(__builtin_bit_cast(uint32_t, mt) >> 15);
     }
 }
 
@@ -366,13 +366,13 @@ __device__ __forceinline__ void norm_max_tile(const float* __restrict__ g, int64
         o.y = fmaxf(fmaxf(m0.y, m1.y), fmaxf(m2.y, m3.y));
         o.z = fmaxf(fmaxf(m0.z, m1.z), fmaxf(m2.z, m3.z));
         o.w = fmaxf(fmaxf(m0.w, m1.w), fmaxf(m2.w, m3.w));
-        // the keys: the top halves of the four maxima (permute selector:
-        // bytes 2-3 of the second operand, then bytes 2-3 of the first).
+        // the keys: bits 30..15 of the four maxima (exponent and 8 mantissa
+        // bits; the sign bit of a maximum is 0), two to a word.
         // __float_as_uint takes the component's value; __builtin_bit_cast of
         // a vector component compiled to a read of component x here.
         u32x2 k;
-        k.x = __builtin_amdgcn_perm(__float_as_uint(o.y), __float_as_uint(o.x), 0x07060302u);
-        k.y = __builtin_amdgcn_perm(__float_as_uint(o.w), __float_as_uint(o.z), 0x07060302u);
+        k.x = (__float_as_uint(o.x) >> 15) | ((__float_as_uint(o.y) << 1) & 0xFFFF0000u);
+        k.y = (__float_as_uint(o.z) >> 15) | ((__float_as_uint(o.w) << 1) & 0xFFFF0000u);
         u32x2* dst = reinterpret_cast<u32x2*>(keys + (q << 2));
         if (NT)
             __builtin_nontemporal_store(k, dst);
@@ -455,15 +455,16 @@ __global__ __launch_bounds__(kBlock) void k_rowsum(const double* __restrict__ pa
 // thread: octets t, t + 256, ..., so each load and store of a wave is
 // contiguous), all loaded before the call's constants are read.  The norm
 // pass keeps, for each
-// coordinate, the top 16 bits of its largest usable |g| over the rows (a
-// key: the exponent field and 7 mantissa bits).  The per-coordinate rule
+// coordinate, bits 30..15 of its largest usable |g| over the rows (a key:
+// the exponent field and the top 8 mantissa bits; the sign bit is 0).  Keys
+// order like the values they truncate.  The per-coordinate rule
 // compares thresholds instead of forming products: a -> RN32(a * inv_k) is
 // non-decreasing for inv_k > 0, so RN32(a * inv_k) <= s_0 holds exactly for
 // a <= T_k, the largest binary32 that passes; k_index_prep finds T_k once
 // per call (a few ulp steps from s_0 / inv_k).  A key below T_k's key means a < T_k, a
 // key above it a > T_k; only a key equal to T_k's leaves the comparison open,
 // and then the coordinate's rows are read again for its exact maximum (at
-// the scales used here, one coordinate in several thousand).  The count
+// the scales used here, about one coordinate in ten thousand).  The count
 // #{k : a <= T_k} needs no loop over k when no binade holds two thresholds
 // (scales at least about twice apart, as 16^k): every T_k in a higher binade
 // than a's counts, none in a lower one, so a table over the 256 values of the
@@ -534,7 +535,7 @@ __device__ __forceinline__ uint32_t index_exact(const float* __restrict__ g, int
 // with their index lowered by one); `tie` collects a key equal to the limit's.
 __device__ __forceinline__ uint32_t index_from_key(const uint2* tab, uint32_t key, bool& tie)
 {
-    const uint2 t = tab[key >> 7];
+    const uint2 t = tab[key >> 8];
     tie |= key == t.y;
     return t.x + (key < t.y ? 1u : 0u);
 }
@@ -630,9 +631,9 @@ __global__ __launch_bounds__(kBlock) void k_index_prep(const double* __restrict_
     if (threadIdx.x < K) {
         const float t = zero ? 0.0f : index_threshold(div_rn32(S.s[threadIdx.x], W), s0);
         thr_s[threadIdx.x] = t;
-        hk_s[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 16;
+        hk_s[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 15;
         T->thr[threadIdx.x] = t;
-        T->hk[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 16;
+        T->hk[threadIdx.x] = __builtin_bit_cast(uint32_t, t) >> 15;
     }
     __syncthreads();
     int crowded = 0;
@@ -667,6 +668,7 @@ __global__ __launch_bounds__(kBlock) void k_index_prep(const double* __restrict_
         T->by_table = by_table ? 1 : 0;
 }
 
+template <bool NT>
 __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict__ keys,
                                                       const float* __restrict__ g, int64_t ldg, int64_t d,
                                                       int32_t M, const IndexTables* __restrict__ T, int32_t K,
@@ -719,7 +721,10 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict
                 u32x2 packed;
                 packed.x = ix[0] | (ix[1] << 8) | (ix[2] << 16) | (ix[3] << 24);
                 packed.y = ix[4] | (ix[5] << 8) | (ix[6] << 16) | (ix[7] << 24);
-                *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
+                if (NT)
+                    __builtin_nontemporal_store(packed, reinterpret_cast<u32x2*>(idx + (o << 3)));
+                else
+                    *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
                 ties |= tie ? 1u << j : 0u;
             }
         } else {
@@ -2388,6 +2393,9 @@ static unsigned one_shot(int64_t units, int64_t per_block)
 // (277 MB of keys), 3% slower at ResNet-50 size (51 MB), where the index pass
 // reads them back from the 256 MB Infinity Cache.
 constexpr int64_t kMaximaNontemporalBytes = int64_t(128) << 20;
+// The index pass stores the index (one byte per coordinate) nontemporally
+// beyond this many bytes, where the passes that read it back find it in HBM.
+constexpr int64_t kIndexNontemporalBytes = int64_t(256) << 20;
 
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
                                float* w, uint8_t* idx, void* ws, hipStream_t stream)
@@ -2435,7 +2443,12 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         // then S_m, W and the index pass's constants in one block
         hipLaunchKernelGGL(k_index_prep, dim3(1), dim3(kBlock), 0, stream, sub, plan.nsub, M, rows, w, S, tabs);
         const unsigned gx = one_shot((d + 7) / 8, kIndexTile);
-        hipLaunchKernelGGL(k_index_max, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K, idx);
+        if (d > kIndexNontemporalBytes)
+            hipLaunchKernelGGL(k_index_max<true>, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K,
+                               idx);
+        else
+            hipLaunchKernelGGL(k_index_max<false>, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K,
+                               idx);
         return hipGetLastError();
     }
     double* part = static_cast<double*>(ws);
