@@ -222,7 +222,9 @@ def stream_probe(workload: str, reps: int) -> None:
                       one chunk of one row (the norm pass's bytes);
       accumulate      4 + 1 + 4 bytes read and 4 written per coordinate of one
                       row (the fused quantise-and-sum of a streamed worker);
-      copy            one row copied (4 bytes read, 4 written)."""
+      copy            one row copied (4 bytes read, 4 written);
+      keys_index<o>   d 16-bit keys read, d bytes written (the index pass's
+                      bytes), o octets of keys per thread."""
     import ctypes
 
     import torch
@@ -240,6 +242,7 @@ def stream_probe(workload: str, reps: int) -> None:
     lib.uqp_rows_out_floats.restype = i64
     lib.uqp_accumulate.argtypes = [P, P, P, i64, P]
     lib.uqp_copy.argtypes = [P, P, i64, P]
+    lib.uqp_keys_index.argtypes = [P, i64, P, i32, P]
     g, cfg = synth.make_gradients(workload, device="cuda")
     M, d = cfg["M"], cfg["d"]
     n = g.numel() // 512 * 512
@@ -263,9 +266,13 @@ def stream_probe(workload: str, reps: int) -> None:
     t_rows = timed(lambda: lib.uqp_rows_read(g.data_ptr(), dn, M, g.stride(0), rows_out.data_ptr(), h))
     t_acc = timed(lambda: lib.uqp_accumulate(g.data_ptr(), idx.data_ptr(), acc.data_ptr(), dn, h))
     t_copy = timed(lambda: lib.uqp_copy(g.data_ptr(), dst.data_ptr(), dn, h))
+    # the keys are the first 2 dn bytes of the gradient buffer, the index the
+    # first dn bytes of the byte buffer
+    t_ki = {o: timed(lambda o=o: lib.uqp_keys_index(g.data_ptr(), dn, codes.data_ptr(), o, h)) for o in (2, 4, 8)}
     res = {"stream_probe": workload, "elements": n, "d": dn, "M": M}
     for name, nbytes, t in (("read", 4 * n, t_r), ("read4_write1", 5 * n, t_rw), ("rows_read", 4 * M * dn, t_rows),
-                            ("accumulate", 13 * dn, t_acc), ("copy", 8 * dn, t_copy)):
+                            ("accumulate", 13 * dn, t_acc), ("copy", 8 * dn, t_copy),
+                            *((f"keys_index{o}", 3 * dn, t) for o, t in t_ki.items())):
         res[f"{name}_us"] = round(t * 1e6, 2)
         res[f"{name}_GBps"] = round(nbytes / t / 1e9, 1)
     print(json.dumps(res))

@@ -20,6 +20,11 @@
 //                        idx and 4 of sum read, 4 of sum written, in the same
 //                        512-element wave tiles; sum[i] += idx[i] + (int)g[i].
 //   uqp_copy           : n fp32 copied (16-byte nontemporal loads and stores).
+//   uqp_keys_index     : the index pass's bytes with no work: d 16-bit keys
+//                        read (16-byte nontemporal loads, one octet of keys
+//                        per load) and d bytes written (8-byte nontemporal
+//                        stores, the low byte of each key); a block covers
+//                        256 * octs octets, thread t octets t, t + 256, ...
 // n (d for the row and accumulate probes) must be a multiple of 512; every
 // pointer 16-byte aligned; out holds uqp_read_out_floats(n) floats
 // (uqp_rows_read: uqp_rows_out_floats(d, M)).  Returns 0, or -1 on a bad
@@ -132,6 +137,33 @@ __global__ __launch_bounds__(kBlock) void k_copy(const float* __restrict__ src, 
         __builtin_nontemporal_store(ld(src + (q << 2)), reinterpret_cast<f32x4*>(dst + (q << 2)));
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int OCTS>
+__global__ __launch_bounds__(kBlock) void k_keys_index(const uint16_t* __restrict__ keys, uint8_t* __restrict__ idx,
+                                                       int64_t noct)
+{
+    const int64_t o0 = static_cast<int64_t>(blockIdx.x) * (kBlock * OCTS) + threadIdx.x;
+    u32x4 kv[OCTS];
+#pragma unroll
+    for (int j = 0; j < OCTS; ++j) {
+        const int64_t o = o0 + kBlock * j;
+        kv[j] = o < noct ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(keys + (o << 3)))
+                         : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < OCTS; ++j) {
+        const int64_t o = o0 + kBlock * j;
+        if (o < noct) {
+            u32x2 b;
+            b.x = __builtin_amdgcn_perm(kv[j].y, kv[j].x, 0x06040200u);
+            b.y = __builtin_amdgcn_perm(kv[j].w, kv[j].z, 0x06040200u);
+            __builtin_nontemporal_store(b, reinterpret_cast<u32x2*>(idx + (o << 3)));
+        }
+    }
+}
+
 int64_t blocks_for(int64_t units, int64_t per_block)
 {
     const int64_t b = (units + per_block - 1) / per_block;
@@ -216,6 +248,24 @@ int uqp_copy(const float* src, float* dst, int64_t n, void* stream)
         return -1;
     hipLaunchKernelGGL(k_copy, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), 0,
                        static_cast<hipStream_t>(stream), src, dst, n / 4);
+    return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+int uqp_keys_index(const uint16_t* keys, int64_t d, uint8_t* idx, int32_t octs, void* stream)
+{
+    if (!ok_args(keys, d, idx) || (octs != 2 && octs != 4 && octs != 8))
+        return -1;
+    const int64_t noct = d / 8;
+    const int64_t blocks = (noct + kBlock * octs - 1) / (kBlock * octs);
+    if (blocks > kMaxBlocks)
+        return -1;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (octs == 2)
+        hipLaunchKernelGGL(k_keys_index<2>, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), 0, s, keys, idx, noct);
+    else if (octs == 4)
+        hipLaunchKernelGGL(k_keys_index<4>, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), 0, s, keys, idx, noct);
+    else
+        hipLaunchKernelGGL(k_keys_index<8>, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), 0, s, keys, idx, noct);
     return hipGetLastError() == hipSuccess ? 0 : -5;
 }
 

@@ -28,6 +28,7 @@ def probe_lib():
     lib.uqp_rows_out_floats.restype = i64
     lib.uqp_accumulate.argtypes = [P, P, P, i64, P]
     lib.uqp_copy.argtypes = [P, P, i64, P]
+    lib.uqp_keys_index.argtypes = [P, i64, P, ctypes.c_int32, P]
     return lib
 
 
@@ -71,3 +72,21 @@ def test_row_accumulate_and_copy_probes(d, M):
     # out-of-range arguments are refused before any launch
     assert lib.uqp_rows_read(g.data_ptr(), d, M, d - 4, out.data_ptr(), s) == -1
     assert lib.uqp_accumulate(g.data_ptr(), idx.data_ptr(), acc.data_ptr(), d + 1, s) == -1
+
+
+@pytest.mark.parametrize("octs", [2, 4, 8])
+@pytest.mark.parametrize("d", [512, 512 * 77, 512 * 5000 + 512])
+def test_keys_index_probe(d, octs):
+    """Every key read and its low byte written, whatever the octets per thread
+    (tiles past d partly filled)."""
+    lib = probe_lib()
+    s = torch.cuda.current_stream().cuda_stream
+    keys = torch.randint(0, 1 << 16, (d,), dtype=torch.int32, device="cuda").to(torch.int16)
+    idx = torch.zeros(d + 64, dtype=torch.uint8, device="cuda")
+    assert lib.uqp_keys_index(keys.data_ptr(), d, idx.data_ptr(), octs, s) == 0
+    torch.cuda.synchronize()
+    want = (keys.cpu().numpy().view(np.uint16) & 0xFF).astype(np.uint8)
+    got = idx.cpu().numpy()
+    assert np.array_equal(got[:d], want)
+    assert not got[d:].any()
+    assert lib.uqp_keys_index(keys.data_ptr(), d, idx.data_ptr(), 3, s) == -1
