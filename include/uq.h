@@ -123,8 +123,8 @@ int uq_shared_scale_noalloc(const float* g, int64_t d, int32_t M, int64_t ldg,
 
 /* Workspace bytes uq_shared_scale needs for (d, M) and any K; 0 never
  * returned.  With 2 <= M <= 16 this includes 2 * d bytes: with several scales
- * the norm pass also keeps the top 16 bits of the largest |g| over the rows
- * at every coordinate, so that the index pass need not read the gradients
+ * the norm pass also keeps a 16-bit key of the largest |g| over the rows
+ * (its exponent and top 8 mantissa bits) at every coordinate, so that the index pass need not read the gradients
  * again (except at the rare coordinates whose key equals a scale limit's). */
 size_t uq_workspace_bytes(int64_t d, int32_t M);
 
