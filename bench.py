@@ -26,6 +26,8 @@ sample checked against the oracle's.  Extra modes:
                         from the shared-scale call's own pass, not formed
                         inside the quantise-and-sum (or, with packed codes,
                         inside the quantiser)
+  --byte-index          the shared index as bytes, not 4-bit fields, where the
+                        quantise-and-sum reads a separately formed one
   --graph               time replays of the step captured in a HIP graph
   --no-cpu-baseline     skip the oracle leg (for profiling runs)
   --copy-probe BYTES    time and run only a plain device copy (counter calibration)
@@ -86,11 +88,18 @@ def quantize_bytes_per_launch(d: int, rows: int, K: int, bits: int = 8) -> int:
     return rows * (4 * d + code_bytes(d, bits)) + (d if K > 1 else 0)
 
 
-def quant_sum_bytes_per_call(d: int, rows: int, K: int, accumulate: bool, reconstruct: bool) -> int:
+def index_bytes(d: int, index_bits: int = 8) -> int:
+    """The shared index: one byte per coordinate, or 4-bit fields."""
+    return d if index_bits == 8 else (d + 1) // 2
+
+
+def quant_sum_bytes_per_call(d: int, rows: int, K: int, accumulate: bool, reconstruct: bool,
+                             index_bits: int = 8) -> int:
     """One fused quantise-and-sum call: the rows' gradients and (several
     scales) the shared index in, the int32 sums out (the old sums in too when
     accumulating) and, when it reconstructs, the output."""
-    return 4 * rows * d + (d if K > 1 else 0) + (4 * d if accumulate else 0) + 4 * d + (4 * d if reconstruct else 0)
+    return (4 * rows * d + (index_bytes(d, index_bits) if K > 1 else 0) + (4 * d if accumulate else 0) + 4 * d
+            + (4 * d if reconstruct else 0))
 
 
 def scale_kernels(M: int, K: int) -> list:
@@ -102,7 +111,7 @@ def scale_kernels(M: int, K: int) -> list:
     return ["k_sumsq", "k_finish", "k_index"]
 
 
-def shared_scale_bytes(d: int, M: int, K: int) -> int:
+def shared_scale_bytes(d: int, M: int, K: int, index_bits: int = 8) -> int:
     """The gradients read once for the norm; with several scales and 2 to 16
     workers that pass also writes a 16-bit key of the largest |g| over the
     workers (2 bytes per coordinate), which the index pass reads instead of
@@ -110,16 +119,18 @@ def shared_scale_bytes(d: int, M: int, K: int) -> int:
     gradient again.  The index is written once."""
     if K == 1:
         return 4 * M * d
+    ib = index_bytes(d, index_bits)
     if 2 <= M <= FUSED_MAX_ROWS:
-        return 4 * M * d + 2 * d + 2 * d + d
-    return 4 * M * d + 4 * M * d + d
+        return 4 * M * d + 2 * d + 2 * d + ib
+    return 4 * M * d + 4 * M * d + ib
 
 
 def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, quant_sum: bool = False,
-                index_in_pass: bool = False) -> list:
+                index_in_pass: bool = False, index_bits: int = 8) -> list:
     """The library calls of one step as stages: name, the kernel it launches
     (several for the shared scale, the longest first), calls per step and the
-    algorithmic bytes per call."""
+    algorithmic bytes per call.  index_bits = 4: the shared index held as
+    4-bit fields (the quantise-and-sum with a separate index pass)."""
     multi = K > 1
     ib = d if multi else 0
     cb = code_bytes(d, bits)
@@ -137,25 +148,26 @@ def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, q
         return [dict(name="shared_scale", kernels=scale_kernels(M, 1), calls=1, bytes=shared_scale_bytes(d, M, 1)),
                 dict(name="index_quantize", kernels=[iq], calls=1, bytes=4 * M * d + d + M * cb),
                 dict(name="sum_dequantize", kernels=["k_sum_dequant"], calls=1, bytes=M * cb + 4 * d + 4 * d + ib)]
-    st = [dict(name="shared_scale", kernels=scale_kernels(M, K), calls=1, bytes=shared_scale_bytes(d, M, K))]
+    xb = index_bits if quant_sum else 8
+    st = [dict(name="shared_scale", kernels=scale_kernels(M, K), calls=1, bytes=shared_scale_bytes(d, M, K, xb))]
     if quant_sum and streamed:
         # one worker per call into the running sum; the last call reconstructs
         if M == 1:
             st.append(dict(name="quant_sum_last", kernels=["k_quant_sum_set_deq"], calls=1,
-                           bytes=quant_sum_bytes_per_call(d, 1, K, False, True)))
+                           bytes=quant_sum_bytes_per_call(d, 1, K, False, True, xb)))
         else:
             st.append(dict(name="quant_sum_first", kernels=["k_quant_sum_set"], calls=1,
-                           bytes=quant_sum_bytes_per_call(d, 1, K, False, False)))
+                           bytes=quant_sum_bytes_per_call(d, 1, K, False, False, xb)))
             if M > 2:
                 st.append(dict(name="quant_sum", kernels=["k_quant_sum_acc"], calls=M - 2,
-                               bytes=quant_sum_bytes_per_call(d, 1, K, True, False)))
+                               bytes=quant_sum_bytes_per_call(d, 1, K, True, False, xb)))
             st.append(dict(name="quant_sum_last", kernels=["k_quant_sum_acc_deq"], calls=1,
-                           bytes=quant_sum_bytes_per_call(d, 1, K, True, True)))
+                           bytes=quant_sum_bytes_per_call(d, 1, K, True, True, xb)))
     elif quant_sum:
         # one scale and 5 to 16 rows: a tile's rows split over a block's waves
         kern = "k_quant_sum_split" if K == 1 and 4 < M <= FUSED_MAX_ROWS else "k_quant_sum_set_deq"
         st.append(dict(name="quant_sum", kernels=[kern], calls=1,
-                       bytes=quant_sum_bytes_per_call(d, M, K, False, True)))
+                       bytes=quant_sum_bytes_per_call(d, M, K, False, True, xb)))
     elif streamed:
         # the codes of one worker per call, then summed into the running sum
         st.append(dict(name="quantize", kernels=[qk], calls=M, bytes=quantize_bytes_per_launch(d, 1, K, bits)))
@@ -172,11 +184,11 @@ def plan_stages(d: int, M: int, K: int, bits: int = 8, streamed: bool = False, q
 
 
 def algorithmic_bytes(d: int, M: int, K: int, streamed: bool, bits: int = 8, quant_sum: bool = False,
-                      index_in_pass: bool = False) -> dict:
+                      index_in_pass: bool = False, index_bits: int = 8) -> dict:
     """Bytes each stage must move at minimum (reads + writes) per step, and
     their total."""
     b = {}
-    for s in plan_stages(d, M, K, bits, streamed, quant_sum, index_in_pass):
+    for s in plan_stages(d, M, K, bits, streamed, quant_sum, index_in_pass, index_bits):
         b[s["name"]] = b.get(s["name"], 0) + s["calls"] * s["bytes"]
     b["total"] = sum(b.values())
     return b
@@ -385,7 +397,7 @@ def parity_on_sample(step, ref, dn: int, d: int, bits: int) -> str:
         a = int(np.float32(step.w[0].item()).view(np.int32))
         ok = abs(a - int(np.float32(ref["W_oracle"]).view(np.int32))) <= 1
     if ref["idx"] is not None:
-        ok = ok and np.array_equal(step.idx[:dn].cpu().numpy(), ref["idx"])
+        ok = ok and np.array_equal(step.index_host(0, dn), ref["idx"])
     if step.codes is not None and not step.streamed:
         if bits == 8:
             ok = ok and np.array_equal(step.codes[:, :dn].cpu().numpy(), ref["codes"])
@@ -522,6 +534,9 @@ def main() -> int:
     ap.add_argument("--index-pass", action="store_true",
                     help="resident workers with several scales: the shared index from the shared-scale call's own "
                          "pass instead of formed inside the quantise-and-sum or, with packed codes, the quantiser")
+    ap.add_argument("--byte-index", action="store_true",
+                    help="the quantise-and-sum reads a separately formed shared index as one byte per coordinate "
+                         "instead of 4-bit fields")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work to aim for, for each of the two CPU figures")
@@ -565,8 +580,11 @@ def main() -> int:
     # int8 codes: quantised and summed in one fused call unless asked for;
     # packed codes are stored (their packing is what those workloads show)
     quant_sum = bits == 8 and not args.composed
+    # the quantise-and-sum calls that read a separately formed index read it
+    # as 4-bit fields unless asked for bytes
+    index_bits = 4 if quant_sum and K > 1 and (streamed or args.index_pass) and not args.byte_index else 8
     step = Step(d, M, scales, device="cuda", streamed=streamed, bits=bits, quant_sum=quant_sum,
-                index_in_pass=False if args.index_pass else None)
+                index_in_pass=False if args.index_pass else None, index_bits=index_bits)
     torch.cuda.synchronize()
 
     # -- timed region: K whole steps (host launches, or with --graph replays
@@ -587,7 +605,7 @@ def main() -> int:
     # -- per-stage times: each stage's call repeated back to back between two
     # events on the stream (mean over rounds), so host launch overhead does
     # not enter them; a stage's share of the step is calls x time per call
-    stages = plan_stages(d, M, K, bits, streamed, quant_sum, step.index_in_pass)
+    stages = plan_stages(d, M, K, bits, streamed, quant_sum, step.index_in_pass, step.index_bits)
     fns = stage_fns(step, g, seed, M)
     reps = stage_reps(args.steps, elapsed / args.steps)
     for st in stages:
@@ -625,6 +643,7 @@ def main() -> int:
                             else "quantise-and-sum fused" if quant_sum
                             else "codes stored with the index formed in the quantiser, then summed"
                             if step.index_in_pass else "codes stored, then summed"),
+                   "index_bits": step.index_bits if K > 1 else None,
                    "launch": "hip graph replay per step" if args.graph else "host launches",
                    "parallelism": "one GPU, M workers simulated"},
         "pct_hbm_peak": round(100 * step_bytes / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 2),

@@ -96,6 +96,21 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg,
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * uq_shared_scale with the shared index stored as 4-bit fields: coordinate i's
+ * k*_i in the low nibble of idx4[i / 2] for even i and in the high nibble for
+ * odd i (the high nibble of the last byte is 0 when d is odd).  Bit for bit
+ * the same W and index values as uq_shared_scale (Sec. 3.2, Eq. (11) with
+ * scale sharing); the index takes half the bytes, and so does every pass
+ * that reads it (uq_quantize_sum_idx4).
+ *   idx4   [(d + 1) / 2] uint8 (written), 16-byte aligned
+ *   every other argument and check as for uq_shared_scale; K < 2 returns
+ *   UQ_EINVAL (one scale has no index)
+ */
+int uq_shared_scale_idx4(const float* g, int64_t d, int32_t M, int64_t ldg,
+                         const float* scales, int32_t K, float* w, uint8_t* idx4,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
  * uq_shared_scale for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
  * the same checks, kernels and results, bit for bit, with the scratch taken
@@ -220,6 +235,21 @@ int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_
                     const float* w, const float* scales, int32_t K, const uint8_t* idx,
                     uint64_t seed, int32_t accumulate, int32_t* sum, int32_t M, float* out,
                     void* stream);
+
+/*
+ * uq_quantize_sum reading the shared index as 4-bit fields (the layout of
+ * uq_shared_scale_idx4): bit for bit the same sum and out as uq_quantize_sum
+ * given the same index values (Eq. (12), the all-reduce of Algorithm 2 and
+ * Eq. (13)).  A streamed worker then reads half a byte of index per
+ * coordinate instead of one.
+ *   idx4   [(d + 1) / 2] uint8 (read), 16-byte aligned
+ *   every other argument and check as for uq_quantize_sum; K < 2 returns
+ *   UQ_EINVAL
+ */
+int uq_quantize_sum_idx4(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                         const float* w, const float* scales, int32_t K, const uint8_t* idx4,
+                         uint64_t seed, int32_t accumulate, int32_t* sum, int32_t M, float* out,
+                         void* stream);
 
 /*
  * The shared scale index of Sec. 3.2 (the rule of Eq. (11) with scale

@@ -52,6 +52,7 @@ def _load() -> ctypes.CDLL:
         raise ImportError(f"two HIP runtimes are mapped in this process: {sorted(runtimes)}")
     P, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
     L.uq_shared_scale.argtypes = [P, i64, i32, i64, P, i32, P, P, P, sz, P]
+    L.uq_shared_scale_idx4.argtypes = [P, i64, i32, i64, P, i32, P, P, P, sz, P]
     L.uq_shared_scale_noalloc.argtypes = [P, i64, i32, i64, P, i32, P, P, P]
     L.uq_workspace_bytes.argtypes = [i64, i32]
     L.uq_workspace_bytes.restype = sz
@@ -62,6 +63,7 @@ def _load() -> ctypes.CDLL:
     L.uq_sum_dequantize.argtypes = [P, i64, i32, i64, i32, i32, P, i32, P, P, i32, P, P, P]
     L.uq_quantize_packed.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i64, P]
     L.uq_quantize_sum.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i32, P, P]
+    L.uq_quantize_sum_idx4.argtypes = [P, i64, i32, i64, i32, P, P, i32, P, u64, i32, P, i32, P, P]
     L.uq_index_quantize_sum.argtypes = [P, i64, i32, i64, P, P, i32, u64, P, P, P, P]
     L.uq_index_quantize.argtypes = [P, i64, i32, i64, P, P, i32, u64, i32, P, P, i64, P]
     L.uq_sum_packed.argtypes = [P, i64, i32, i64, i32, i32, P, P]
@@ -76,8 +78,9 @@ def _load() -> ctypes.CDLL:
     L.uq_strerror.restype = ctypes.c_char_p
     L.uq_last_error.argtypes = []
     L.uq_last_error.restype = ctypes.c_char_p
-    for name in ("uq_shared_scale", "uq_shared_scale_noalloc", "uq_quantize_single", "uq_quantize_multi", "uq_sum_codes",
-                 "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed", "uq_sum_packed", "uq_quantize_sum",
+    for name in ("uq_shared_scale", "uq_shared_scale_idx4", "uq_shared_scale_noalloc", "uq_quantize_single",
+                 "uq_quantize_multi", "uq_sum_codes", "uq_dequantize", "uq_sum_dequantize", "uq_quantize_packed",
+                 "uq_sum_packed", "uq_quantize_sum", "uq_quantize_sum_idx4",
                  "uq_index_quantize_sum", "uq_index_quantize",
                  "uq_randk_select", "uq_gather",
                  "uq_scatter", "uq_set_grid_cap", "uq_set_randk_mode"):
@@ -161,6 +164,12 @@ def uq_shared_scale(g, d, M, ldg, scales, K, w, idx, ws, ws_bytes, stream=None) 
                                _stream(stream)))
 
 
+def uq_shared_scale_idx4(g, d, M, ldg, scales, K, w, idx4, ws, ws_bytes, stream=None) -> None:
+    hs = _host_scales(scales)
+    _check(lib.uq_shared_scale_idx4(_ptr(g), d, M, ldg, hs.ptr, K, _ptr(w), _ptr(idx4), _ptr(ws), ws_bytes,
+                                    _stream(stream)))
+
+
 def uq_shared_scale_noalloc(g, d, M, ldg, scales, K, w, idx, stream=None) -> None:
     hs = _host_scales(scales)
     _check(lib.uq_shared_scale_noalloc(_ptr(g), d, M, ldg, hs.ptr, K, _ptr(w), _ptr(idx), _stream(stream)))
@@ -203,6 +212,13 @@ def uq_quantize_sum(g, d, rows, ldg, worker0, w, scales, K, idx, seed, accumulat
     hs = _host_scales(scales)
     _check(lib.uq_quantize_sum(_ptr(g), d, rows, ldg, worker0, _ptr(w), hs.ptr, K, _ptr(idx), seed, accumulate,
                                _ptr(sum), M, _ptr(out), _stream(stream)))
+
+
+def uq_quantize_sum_idx4(g, d, rows, ldg, worker0, w, scales, K, idx4, seed, accumulate, sum, M, out,
+                         stream=None) -> None:
+    hs = _host_scales(scales)
+    _check(lib.uq_quantize_sum_idx4(_ptr(g), d, rows, ldg, worker0, _ptr(w), hs.ptr, K, _ptr(idx4), seed,
+                                    accumulate, _ptr(sum), M, _ptr(out), _stream(stream)))
 
 
 def uq_index_quantize_sum(g, d, M, ldg, w, scales, K, seed, idx, sum, out, stream=None) -> None:

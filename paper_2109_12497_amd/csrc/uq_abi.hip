@@ -276,8 +276,8 @@ size_t uq_workspace_bytes(int64_t d, int32_t M)
     return bytes;
 }
 
-int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
-                    float* w, uint8_t* idx, void* ws, size_t ws_bytes, void* stream)
+static int shared_scale_common(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
+                               float* w, uint8_t* idx, void* ws, size_t ws_bytes, void* stream, int32_t idx_bits)
 {
     UQ_TRY(check_dims(d, M, "M"));
     UQ_TRY(check_rows(g, d, M, ldg, 4, "g"));
@@ -297,7 +297,22 @@ int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const flo
     if (ws_bytes < uq_workspace_bytes(d, M))
         return fail(UQ_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", ws_bytes,
                     uq_workspace_bytes(d, M));
-    return launched(uq::launch_shared_scale(g, d, M, ldg, S, w, idx, ws, static_cast<hipStream_t>(stream)));
+    return launched(
+        uq::launch_shared_scale(g, d, M, ldg, S, w, idx, ws, static_cast<hipStream_t>(stream), idx_bits));
+}
+
+int uq_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
+                    float* w, uint8_t* idx, void* ws, size_t ws_bytes, void* stream)
+{
+    return shared_scale_common(g, d, M, ldg, scales, K, w, idx, ws, ws_bytes, stream, 8);
+}
+
+int uq_shared_scale_idx4(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
+                         float* w, uint8_t* idx4, void* ws, size_t ws_bytes, void* stream)
+{
+    if (K < 2)
+        return fail(UQ_EINVAL, "K = %d: the 4-bit index needs several scales", K);
+    return shared_scale_common(g, d, M, ldg, scales, K, w, idx4, ws, ws_bytes, stream, 4);
 }
 
 int uq_shared_scale_noalloc(const float* g, int64_t d, int32_t M, int64_t ldg, const float* scales, int32_t K,
@@ -420,9 +435,10 @@ int uq_sum_dequantize(const uint8_t* codes, int64_t d, int32_t rows, int64_t ldc
                                            static_cast<hipStream_t>(stream)));
 }
 
-int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
-                    const float* scales, int32_t K, const uint8_t* idx, uint64_t seed, int32_t accumulate,
-                    int32_t* sum, int32_t M, float* out, void* stream)
+static int quantize_sum_common(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
+                               const float* w, const float* scales, int32_t K, const uint8_t* idx, uint64_t seed,
+                               int32_t accumulate, int32_t* sum, int32_t M, float* out, void* stream,
+                               int32_t idx_bits)
 {
     uq::ScaleSet S;
     UQ_TRY(check_scales(scales, K, &S));
@@ -447,7 +463,25 @@ int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_
         UQ_TRY(check_reconstruction(d, M, w, scales, K, idx, out, &S2));
     }
     return launched(uq::launch_quant_sum(g, d, rows, ldg, worker0, w, S, idx, seed, accumulate, sum, M, out,
-                                         static_cast<hipStream_t>(stream)));
+                                         static_cast<hipStream_t>(stream), idx_bits));
+}
+
+int uq_quantize_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                    const float* scales, int32_t K, const uint8_t* idx, uint64_t seed, int32_t accumulate,
+                    int32_t* sum, int32_t M, float* out, void* stream)
+{
+    return quantize_sum_common(g, d, rows, ldg, worker0, w, scales, K, idx, seed, accumulate, sum, M, out, stream,
+                               8);
+}
+
+int uq_quantize_sum_idx4(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
+                         const float* scales, int32_t K, const uint8_t* idx4, uint64_t seed, int32_t accumulate,
+                         int32_t* sum, int32_t M, float* out, void* stream)
+{
+    if (K < 2)
+        return fail(UQ_EINVAL, "K = %d: the 4-bit index needs several scales", K);
+    return quantize_sum_common(g, d, rows, ldg, worker0, w, scales, K, idx4, seed, accumulate, sum, M, out, stream,
+                               4);
 }
 
 int uq_index_quantize_sum(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w, const float* scales,

@@ -185,6 +185,9 @@ __device__ __forceinline__ f32x4 rows_amax(const float* __restrict__ g, int64_t 
     return amax;
 }
 
+// NIB: the index stored as 4-bit fields, two coordinates a byte (the low
+// nibble first); a quad's four fields are one 16-bit store.
+template <bool NIB>
 __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, int64_t d, int32_t M,
                                                   int64_t ldg, const float* __restrict__ wptr,
                                                   ScaleSet S, uint8_t* __restrict__ idx)
@@ -215,19 +218,36 @@ __global__ __launch_bounds__(kBlock) void k_index(const float* __restrict__ g, i
 
     for (int64_t q = first; q < nquad; q += stride) {
         const f32x4 amax = q == first ? amax0 : rows_amax(g, q, M, ldg);
+        const int sh = NIB ? 4 : 8;
         const uint32_t packed = index_of(amax.x, inv, K, s0, zero) |
-                                (index_of(amax.y, inv, K, s0, zero) << 8) |
-                                (index_of(amax.z, inv, K, s0, zero) << 16) |
-                                (index_of(amax.w, inv, K, s0, zero) << 24);
-        *reinterpret_cast<uint32_t*>(idx + (q << 2)) = packed;
+                                (index_of(amax.y, inv, K, s0, zero) << sh) |
+                                (index_of(amax.z, inv, K, s0, zero) << (2 * sh)) |
+                                (index_of(amax.w, inv, K, s0, zero) << (3 * sh));
+        if (NIB)
+            *reinterpret_cast<uint16_t*>(idx + (q << 1)) = static_cast<uint16_t>(packed);
+        else
+            *reinterpret_cast<uint32_t*>(idx + (q << 2)) = packed;
     }
-    // trailing d % 4 coordinates
+    // trailing d % 4 coordinates (with 4-bit fields one thread forms their
+    // bytes, which two coordinates share)
     const int64_t t = (nquad << 2) + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (blockIdx.x == 0 && t < d) {
-        float amax = 0.0f;
-        for (int32_t m = 0; m < M; ++m)
-            amax = fmaxf(amax, usable_or_zero(g[static_cast<int64_t>(m) * ldg + t]));
-        idx[t] = static_cast<uint8_t>(index_of(amax, inv, K, s0, zero));
+    if (blockIdx.x == 0 && t < d && (!NIB || threadIdx.x == 0)) {
+        uint32_t nib = 0u;
+        for (int64_t i = t; i < (NIB ? d : t + 1); ++i) {
+            float amax = 0.0f;
+            for (int32_t m = 0; m < M; ++m)
+                amax = fmaxf(amax, usable_or_zero(g[static_cast<int64_t>(m) * ldg + i]));
+            const uint32_t v = index_of(amax, inv, K, s0, zero);
+            if (!NIB) {
+                idx[i] = static_cast<uint8_t>(v);
+            } else {
+                nib |= v << (4 * ((i - t) & 1));
+                if (((i - t) & 1) || i + 1 == d) {
+                    idx[i >> 1] = static_cast<uint8_t>(nib);
+                    nib = 0u;
+                }
+            }
+        }
     }
 }
 
@@ -668,7 +688,9 @@ __global__ __launch_bounds__(kBlock) void k_index_prep(const double* __restrict_
         T->by_table = by_table ? 1 : 0;
 }
 
-template <bool NT>
+// NIB: the index stored as 4-bit fields (an octet's eight in one 32-bit
+// store), as in k_index.
+template <bool NT, bool NIB>
 __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict__ keys,
                                                       const float* __restrict__ g, int64_t ldg, int64_t d,
                                                       int32_t M, const IndexTables* __restrict__ T, int32_t K,
@@ -718,13 +740,22 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict
 #pragma unroll
                 for (int c = 0; c < 8; ++c)
                     ix[c] = index_from_key(tab_s, k8[c], tie);
-                u32x2 packed;
-                packed.x = ix[0] | (ix[1] << 8) | (ix[2] << 16) | (ix[3] << 24);
-                packed.y = ix[4] | (ix[5] << 8) | (ix[6] << 16) | (ix[7] << 24);
-                if (NT)
-                    __builtin_nontemporal_store(packed, reinterpret_cast<u32x2*>(idx + (o << 3)));
-                else
-                    *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
+                if (NIB) {
+                    const uint32_t packed = ix[0] | (ix[1] << 4) | (ix[2] << 8) | (ix[3] << 12) | (ix[4] << 16) |
+                                            (ix[5] << 20) | (ix[6] << 24) | (ix[7] << 28);
+                    if (NT)
+                        __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(idx + (o << 2)));
+                    else
+                        *reinterpret_cast<uint32_t*>(idx + (o << 2)) = packed;
+                } else {
+                    u32x2 packed;
+                    packed.x = ix[0] | (ix[1] << 8) | (ix[2] << 16) | (ix[3] << 24);
+                    packed.y = ix[4] | (ix[5] << 8) | (ix[6] << 16) | (ix[7] << 24);
+                    if (NT)
+                        __builtin_nontemporal_store(packed, reinterpret_cast<u32x2*>(idx + (o << 3)));
+                    else
+                        *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
+                }
                 ties |= tie ? 1u << j : 0u;
             }
         } else {
@@ -741,12 +772,17 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict
 #pragma unroll 1
                 for (int c = 0; c < 8; ++c) {
                     const uint32_t v = index_from_keys(hk_s, K, octet_key(kj, c), tie);
-                    if (c < 4)
+                    if (NIB)
+                        packed.x |= v << (4 * c);
+                    else if (c < 4)
                         packed.x |= v << (8 * c);
                     else
                         packed.y |= v << (8 * (c - 4));
                 }
-                *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
+                if (NIB)
+                    *reinterpret_cast<uint32_t*>(idx + (o << 2)) = packed.x;
+                else
+                    *reinterpret_cast<u32x2*>(idx + (o << 3)) = packed;
                 ties |= tie ? 1u << j : 0u;
             }
         }
@@ -757,28 +793,44 @@ __global__ __launch_bounds__(kBlock) void k_index_max(const uint16_t* __restrict
             ties &= ties - 1u;
             const int64_t o = t0 + threadIdx.x + kBlock * j;
             const u32x4 kj = load_nt(reinterpret_cast<const uint32_t*>(keys + (o << 3)));
+            uint32_t word = 0u;  // NIB: the octet's eight fields, stored again whole
 #pragma unroll 1
             for (int c = 0; c < 8; ++c) {
                 bool tc = false;
                 const uint32_t key = octet_key(kj, c);
-                if (by_table)
-                    index_from_key(tab_s, key, tc);
-                else
-                    index_from_keys(hk_s, K, key, tc);
+                uint32_t v = by_table ? index_from_key(tab_s, key, tc) : index_from_keys(hk_s, K, key, tc);
                 if (tc)
-                    idx[(o << 3) + c] = static_cast<uint8_t>(index_exact(g, ldg, M, (o << 3) + c, thr_s, K));
+                    v = index_exact(g, ldg, M, (o << 3) + c, thr_s, K);
+                if (NIB)
+                    word |= v << (4 * c);
+                else if (tc)
+                    idx[(o << 3) + c] = static_cast<uint8_t>(v);
             }
+            if (NIB)
+                *reinterpret_cast<uint32_t*>(idx + (o << 2)) = word;
         }
     }
-    // the d % 8 trailing coordinates: threads of block 0
+    // the d % 8 trailing coordinates: threads of block 0 (with 4-bit fields
+    // thread 0 alone, since two coordinates share a byte)
     const int64_t t = (noct << 3) + threadIdx.x;
-    if (blockIdx.x == 0 && t < d) {
-        bool tie = false;
-        const uint32_t key = keys[t];
-        uint32_t v = by_table ? index_from_key(tab_s, key, tie) : index_from_keys(hk_s, K, key, tie);
-        if (tie)
-            v = index_exact(g, ldg, M, t, thr_s, K);
-        idx[t] = static_cast<uint8_t>(v);
+    if (blockIdx.x == 0 && t < d && (!NIB || threadIdx.x == 0)) {
+        uint32_t nib = 0u;
+        for (int64_t i = t; i < (NIB ? d : t + 1); ++i) {
+            bool tie = false;
+            const uint32_t key = keys[i];
+            uint32_t v = by_table ? index_from_key(tab_s, key, tie) : index_from_keys(hk_s, K, key, tie);
+            if (tie)
+                v = index_exact(g, ldg, M, i, thr_s, K);
+            if (!NIB) {
+                idx[i] = static_cast<uint8_t>(v);
+            } else {
+                nib |= v << (4 * ((i - t) & 1));
+                if (((i - t) & 1) || i + 1 == d) {
+                    idx[i >> 1] = static_cast<uint8_t>(nib);
+                    nib = 0u;
+                }
+            }
+        }
     }
 }
 // ---------------------------------------------------------------------------
@@ -919,15 +971,37 @@ struct TileIn {
     uint32_t ka, kb;
 };
 
-template <bool MULTI>
+// The four 4-bit index fields of a 16-bit word (coordinate 2j in the low
+// nibble of byte j) spread to the four bytes of a word, the byte layout.
+__device__ __forceinline__ uint32_t nibbles_to_bytes(uint32_t h)
+{
+    return (h & 0xFu) | ((h << 4) & 0xF00u) | ((h << 8) & 0xF0000u) | ((h << 12) & 0xF000000u);
+}
+
+// Index k*_i of the 4-bit layout: the low nibble of byte i / 2 for even i,
+// the high nibble for odd i.
+__device__ __forceinline__ uint32_t nibble_at(const uint8_t* __restrict__ idx4, int64_t i)
+{
+    return (static_cast<uint32_t>(idx4[i >> 1]) >> ((i & 1) * 4)) & 0xFu;
+}
+
+// NIB: the index is held as 4-bit fields (two coordinates a byte); its
+// fields are spread to bytes here, so that everything after the load is the
+// byte layout's.
+template <bool MULTI, bool NIB = false>
 __device__ __forceinline__ TileIn load_tile(const float* __restrict__ row, const uint8_t* __restrict__ idx,
                                             int64_t a_off)
 {
     TileIn in;
     in.A = load_nt(row + a_off);
     in.B = load_nt(row + a_off + 256);
-    in.ka = MULTI ? *reinterpret_cast<const uint32_t*>(idx + a_off) : 0u;
-    in.kb = MULTI ? *reinterpret_cast<const uint32_t*>(idx + a_off + 256) : 0u;
+    if (MULTI && NIB) {
+        in.ka = nibbles_to_bytes(*reinterpret_cast<const uint16_t*>(idx + (a_off >> 1)));
+        in.kb = nibbles_to_bytes(*reinterpret_cast<const uint16_t*>(idx + ((a_off + 256) >> 1)));
+    } else {
+        in.ka = MULTI ? *reinterpret_cast<const uint32_t*>(idx + a_off) : 0u;
+        in.kb = MULTI ? *reinterpret_cast<const uint32_t*>(idx + a_off + 256) : 0u;
+    }
     return in;
 }
 
@@ -1542,8 +1616,8 @@ __device__ __forceinline__ void quant_sum_tile(const float* __restrict__ g, int6
 // The coordinates past the last whole tile (fewer than 512): lane t of one
 // wave takes the 8 contiguous coordinates of group ntiles * 64 + t for every
 // row, then stores their sums (and reconstruction).  inv_s holds s_k / W (not
-// scaled).
-template <bool MULTI, bool ACC, bool DEQ>
+// scaled).  NIB as for load_tile.
+template <bool MULTI, bool ACC, bool DEQ, bool NIB = false>
 __device__ __forceinline__ void quant_sum_tail(const float* __restrict__ g, int64_t d, int64_t ldg, int32_t rows,
                                                uint32_t worker0, const uint8_t* __restrict__ idx, int64_t ntiles,
                                                const float* inv_s, float inv0, float s0, uint32_t kmax,
@@ -1558,7 +1632,8 @@ __device__ __forceinline__ void quant_sum_tail(const float* __restrict__ g, int6
     uint32_t kk[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        kk[j] = MULTI ? min(static_cast<uint32_t>(base + j < d ? idx[base + j] : 0), kmax) : 0u;
+        const uint32_t raw = base + j < d ? (NIB ? nibble_at(idx, base + j) : static_cast<uint32_t>(idx[base + j])) : 0u;
+        kk[j] = MULTI ? min(raw, kmax) : 0u;
         inv[j] = MULTI ? inv_s[kk[j]] : inv0;
     }
     int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -1586,8 +1661,8 @@ __device__ __forceinline__ void quant_sum_tail(const float* __restrict__ g, int6
 }
 
 // ROW1: the one-row form (a streamed worker), compiled apart so that it does
-// not carry the row loop's registers.
-template <bool MULTI, bool ACC, bool DEQ, bool NT, bool ROW1>
+// not carry the row loop's registers.  NIB: the index as 4-bit fields.
+template <bool MULTI, bool ACC, bool DEQ, bool NT, bool ROW1, bool NIB>
 __global__ __launch_bounds__(kBlock) void k_quant_sum(const float* __restrict__ g, int64_t d, int32_t rows,
                                                       int64_t ldg, int32_t worker0, const float* __restrict__ wptr,
                                                       ScaleSet S, const uint8_t* __restrict__ idx, uint32_t key0,
@@ -1610,7 +1685,7 @@ __global__ __launch_bounds__(kBlock) void k_quant_sum(const float* __restrict__ 
     i32x4 oldA0 = {0, 0, 0, 0}, oldB0 = {0, 0, 0, 0};
     if (first < ntiles) {
         const int64_t a_off = (first << 9) + 4 * lane;
-        in0 = load_tile<MULTI>(g, idx, a_off);
+        in0 = load_tile<MULTI, NIB>(g, idx, a_off);
         if (ACC) {
             oldA0 = load_sum4<NT>(sum + a_off);
             oldB0 = load_sum4<NT>(sum + a_off + 256);
@@ -1651,7 +1726,7 @@ __global__ __launch_bounds__(kBlock) void k_quant_sum(const float* __restrict__ 
     if (stride < ntiles) {
         for (int64_t T = first + stride; T < ntiles; T += stride) {
             const int64_t a_off = (T << 9) + 4 * lane;
-            const TileIn in = load_tile<MULTI>(g, idx, a_off);
+            const TileIn in = load_tile<MULTI, NIB>(g, idx, a_off);
             i32x4 oldA = {0, 0, 0, 0}, oldB = {0, 0, 0, 0};
             if (ACC) {
                 oldA = load_sum4<NT>(sum + a_off);
@@ -1666,7 +1741,7 @@ __global__ __launch_bounds__(kBlock) void k_quant_sum(const float* __restrict__ 
         }
     }
     if (blockIdx.x == 0 && threadIdx.x < 64)
-        quant_sum_tail<MULTI, ACC, DEQ>(g, d, ldg, rows, w0, idx, ntiles, inv_s, inv0, s0, kmax, key0, key1, sum,
+        quant_sum_tail<MULTI, ACC, DEQ, NIB>(g, d, ldg, rows, w0, idx, ntiles, inv_s, inv0, s0, kmax, key0, key1, sum,
                                         deq_s, out);
 }
 
@@ -2398,8 +2473,9 @@ constexpr int64_t kMaximaNontemporalBytes = int64_t(128) << 20;
 constexpr int64_t kIndexNontemporalBytes = int64_t(256) << 20;
 
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
-                               float* w, uint8_t* idx, void* ws, hipStream_t stream)
+                               float* w, uint8_t* idx, void* ws, hipStream_t stream, int32_t idx_bits)
 {
+    const bool nib = idx_bits == 4;
     if (use_fused(d, M, S.K)) {
         const FusedPlan plan = fused_plan(d);
         const FusedLayout L = fused_layout(d, M);
@@ -2443,12 +2519,15 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
         // then S_m, W and the index pass's constants in one block
         hipLaunchKernelGGL(k_index_prep, dim3(1), dim3(kBlock), 0, stream, sub, plan.nsub, M, rows, w, S, tabs);
         const unsigned gx = one_shot((d + 7) / 8, kIndexTile);
-        if (d > kIndexNontemporalBytes)
-            hipLaunchKernelGGL(k_index_max<true>, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K,
-                               idx);
-        else
-            hipLaunchKernelGGL(k_index_max<false>, dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K,
-                               idx);
+#define UQ_LAUNCH_INDEX_MAX(NT, NIB)                                                                            \
+    hipLaunchKernelGGL((k_index_max<NT, NIB>), dim3(gx), dim3(kBlock), 0, stream, keys, g, ldg, d, M, tabs, S.K, idx)
+        // the index is stored nontemporally beyond kIndexNontemporalBytes
+        if ((nib ? (d + 1) / 2 : d) > kIndexNontemporalBytes) {
+            if (nib) UQ_LAUNCH_INDEX_MAX(true, true); else UQ_LAUNCH_INDEX_MAX(true, false);
+        } else {
+            if (nib) UQ_LAUNCH_INDEX_MAX(false, true); else UQ_LAUNCH_INDEX_MAX(false, false);
+        }
+#undef UQ_LAUNCH_INDEX_MAX
         return hipGetLastError();
     }
     double* part = static_cast<double*>(ws);
@@ -2463,7 +2542,10 @@ hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg
     hipLaunchKernelGGL(k_finish, dim3(1), dim3(kFinishThreads), 0, stream, part, plan.nchunks, M, w);
     if (S.K > 1 && d > 0) {
         const unsigned gx = one_shot((d + 3) / 4, kBlock);
-        hipLaunchKernelGGL(k_index, dim3(gx), dim3(kBlock), 0, stream, g, d, M, ldg, w, S, idx);
+        if (nib)
+            hipLaunchKernelGGL(k_index<true>, dim3(gx), dim3(kBlock), 0, stream, g, d, M, ldg, w, S, idx);
+        else
+            hipLaunchKernelGGL(k_index<false>, dim3(gx), dim3(kBlock), 0, stream, g, d, M, ldg, w, S, idx);
     }
     return hipGetLastError();
 }
@@ -2510,8 +2592,9 @@ hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg,
 
 hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
                             const ScaleSet& S, const uint8_t* idx, uint64_t seed, int32_t accumulate, int32_t* sum,
-                            int32_t M, float* out, hipStream_t stream)
+                            int32_t M, float* out, hipStream_t stream, int32_t idx_bits)
 {
+    const bool nib = idx_bits == 4;
     if (d == 0)
         return hipSuccess;
     const uint32_t key0 = static_cast<uint32_t>(seed);
@@ -2544,14 +2627,23 @@ hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg
 #undef UQ_LAUNCH_SPLIT
         return hipGetLastError();
     }
-#define UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, NT)                                                                        \
+#define UQ_LAUNCH_QSUM_(MULTI, ACC, DEQ, NT, NIB)                                                                   \
     do {                                                                                                           \
         if (rows == 1)                                                                                             \
-            hipLaunchKernelGGL((k_quant_sum<MULTI, ACC, DEQ, NT, true>), grid, dim3(kBlock), 0, stream, g, d, rows, \
-                               ldg, worker0, w, S, idx, key0, key1, sum, M, out);                                  \
-        else                                                                                                       \
-            hipLaunchKernelGGL((k_quant_sum<MULTI, ACC, DEQ, NT, false>), grid, dim3(kBlock), 0, stream, g, d,      \
+            hipLaunchKernelGGL((k_quant_sum<MULTI, ACC, DEQ, NT, true, NIB>), grid, dim3(kBlock), 0, stream, g, d,  \
                                rows, ldg, worker0, w, S, idx, key0, key1, sum, M, out);                            \
+        else                                                                                                       \
+            hipLaunchKernelGGL((k_quant_sum<MULTI, ACC, DEQ, NT, false, NIB>), grid, dim3(kBlock), 0, stream, g, d, \
+                               rows, ldg, worker0, w, S, idx, key0, key1, sum, M, out);                            \
+    } while (0)
+    // the 4-bit index layout only matters with several scales (NIB = MULTI
+    // there, so one scale compiles no second instance)
+#define UQ_LAUNCH_QSUM(MULTI, ACC, DEQ, NT)                  \
+    do {                                                     \
+        if (nib)                                             \
+            UQ_LAUNCH_QSUM_(MULTI, ACC, DEQ, NT, MULTI);     \
+        else                                                 \
+            UQ_LAUNCH_QSUM_(MULTI, ACC, DEQ, NT, false);     \
     } while (0)
 #define UQ_LAUNCH_QSUM_NT(MULTI, ACC, DEQ)  \
     do {                                    \
@@ -2575,6 +2667,7 @@ hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg
 #undef UQ_LAUNCH_QSUM_DEQ
 #undef UQ_LAUNCH_QSUM_NT
 #undef UQ_LAUNCH_QSUM
+#undef UQ_LAUNCH_QSUM_
     return hipGetLastError();
 }
 

@@ -128,18 +128,20 @@ constexpr int64_t kMinOneShotCap = 8;
 bool set_one_shot_cap(int64_t blocks);
 
 // ws: at least uq_workspace_bytes(d, M) bytes (norm partials, or the fused
-// path's layout)
+// path's layout); idx_bits as for launch_quant_sum
 hipError_t launch_shared_scale(const float* g, int64_t d, int32_t M, int64_t ldg, const ScaleSet& S,
-                               float* w, uint8_t* idx, void* ws, hipStream_t stream);
+                               float* w, uint8_t* idx, void* ws, hipStream_t stream, int32_t idx_bits = 8);
 // bits = 8: int8 codes [rows][ldc]; bits = 4 or 2: packed codes, ldc in bytes
 hipError_t launch_quantise(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0,
                            const float* w, const ScaleSet& S, const uint8_t* idx, uint64_t seed,
                            void* codes, int64_t ldc, int32_t bits, hipStream_t stream);
 // quantise `rows` rows and add their codes into sum (= or +=) without storing
-// them; out != nullptr: also the reconstruction of the stored sums (M workers)
+// them; out != nullptr: also the reconstruction of the stored sums (M workers);
+// idx_bits 8: one byte per coordinate, 4: two coordinates a byte (low nibble
+// first)
 hipError_t launch_quant_sum(const float* g, int64_t d, int32_t rows, int64_t ldg, int32_t worker0, const float* w,
                             const ScaleSet& S, const uint8_t* idx, uint64_t seed, int32_t accumulate, int32_t* sum,
-                            int32_t M, float* out, hipStream_t stream);
+                            int32_t M, float* out, hipStream_t stream, int32_t idx_bits = 8);
 hipError_t launch_index_quant_sum(const float* g, int64_t d, int32_t M, int64_t ldg, const float* w,
                                   const ScaleSet& S, uint64_t seed, uint8_t* idx, int32_t* sum, float* out,
                                   hipStream_t stream);

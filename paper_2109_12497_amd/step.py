@@ -8,11 +8,13 @@ No arithmetic of the method happens here.
 """
 from __future__ import annotations
 
+import numpy as np
 import torch
 
 from . import (_stream, uq_dequantize, uq_gather, uq_index_quantize, uq_index_quantize_sum, uq_quantize_multi, uq_quantize_packed,
-               uq_quantize_single, uq_quantize_sum, uq_randk_select, uq_randk_workspace_bytes, uq_scatter, uq_shared_scale,
-               uq_sum_codes, uq_sum_dequantize, uq_sum_packed, uq_workspace_bytes)
+               uq_quantize_single, uq_quantize_sum, uq_quantize_sum_idx4, uq_randk_select, uq_randk_workspace_bytes,
+               uq_scatter, uq_shared_scale, uq_shared_scale_idx4, uq_sum_codes, uq_sum_dequantize, uq_sum_packed,
+               uq_workspace_bytes)
 
 
 def round_up(x: int, m: int) -> int:
@@ -38,11 +40,15 @@ class Step:
     which stores the codes), so the shared-scale call forms W only.  The
     default is True when those conditions hold with quant_sum or with packed
     codes; int8 codes stored keep the separate index pass unless asked.
+    index_bits=4 (several scales, quant_sum, index not formed in the pass):
+    the shared index is held as 4-bit fields, two coordinates a byte
+    (uq_shared_scale_idx4, uq_quantize_sum_idx4), so each call that reads it
+    reads half the bytes; index_host() gives its values either way.
     """
 
     def __init__(self, d: int, M: int, scales, device="cuda", streamed: bool = False, ldc: int | None = None,
                  bits: int = 8, fused: bool = True, quant_sum: bool | None = None,
-                 index_in_pass: bool | None = None):
+                 index_in_pass: bool | None = None, index_bits: int = 8):
         self.d, self.M = d, M
         self.fused = fused
         self.quant_sum = (streamed and fused) if quant_sum is None else quant_sum
@@ -55,13 +61,18 @@ class Step:
         assert not (self.index_in_pass and not can), "index_in_pass needs resident rows, K > 1, M <= 16"
         self.streamed = streamed
         self.bits = bits
+        assert index_bits in (8, 4), "index_bits is 8 or 4"
+        assert index_bits == 8 or (self.quant_sum and self.K > 1 and not self.index_in_pass), \
+            "the 4-bit index serves the quantise-and-sum with several scales and a separate index pass"
+        self.index_bits = index_bits
         row_bytes = (max(d, 1) * bits + 7) // 8
         self.ldc = round_up(row_bytes, 256) if ldc is None else ldc
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
         self.w = torch.zeros(4, dtype=torch.float32, device=device)  # W lives in w[0]
-        self.idx = torch.zeros(round_up(max(d, 1), 256), dtype=torch.uint8, device=device) if self.K > 1 else None
+        idx_bytes = max(d, 1) if index_bits == 8 else (max(d, 1) + 1) // 2
+        self.idx = torch.zeros(round_up(idx_bytes, 256), dtype=torch.uint8, device=device) if self.K > 1 else None
         self.ws_bytes = uq_workspace_bytes(d, M)
         self.ws = torch.zeros(self.ws_bytes // 8, dtype=torch.float64, device=device)
         rows = 1 if streamed else M
@@ -76,6 +87,9 @@ class Step:
             # W does not depend on the scales: the one-scale call forms it alone
             uq_shared_scale(g, self.d, self.M, g.stride(0), self.scales[:1], 1, self.w, None, self.ws,
                             self.ws_bytes, stream)
+        elif self.index_bits == 4:
+            uq_shared_scale_idx4(g, self.d, self.M, g.stride(0), self.scales, self.K, self.w, self.idx, self.ws,
+                                 self.ws_bytes, stream)
         else:
             uq_shared_scale(g, self.d, self.M, g.stride(0), self.scales, self.K, self.w, self.idx, self.ws,
                             self.ws_bytes, stream)
@@ -104,8 +118,20 @@ class Step:
     def quantize_sum(self, g, seed: int, rows: int | None = None, worker0: int = 0, accumulate: int = 0,
                      reconstruct: bool = True, stream=None):
         rows = self.M if rows is None else rows
-        uq_quantize_sum(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed,
-                        accumulate, self.sum, self.M, self.out if reconstruct else None, stream)
+        call = uq_quantize_sum_idx4 if self.index_bits == 4 else uq_quantize_sum
+        call(g, self.d, rows, g.stride(0), worker0, self.w, self.scales, self.K, self.idx, seed, accumulate,
+             self.sum, self.M, self.out if reconstruct else None, stream)
+
+    def index_host(self, i0: int = 0, i1: int | None = None) -> np.ndarray:
+        """The shared index k*_i for i in [i0, i1) as host uint8 values (the
+        4-bit layout's fields read out: the low nibble of byte i / 2 for even
+        i, the high one for odd i)."""
+        i1 = self.d if i1 is None else i1
+        if self.index_bits == 8:
+            return self.idx[i0:i1].cpu().numpy()
+        b = self.idx[i0 // 2:(i1 + 1) // 2].cpu().numpy()
+        fields = np.stack([b & 0xF, b >> 4], axis=1).reshape(-1)
+        return fields[i0 - 2 * (i0 // 2):i0 - 2 * (i0 // 2) + (i1 - i0)]
 
     def index_quantize(self, g, seed: int, stream=None):
         uq_index_quantize(g, self.d, self.M, g.stride(0), self.w, self.scales, self.K, seed, self.bits, self.idx,

@@ -126,6 +126,24 @@ def test_shared_scale_rejects(kw, want):
     assert uq.uq_last_error() != ""
 
 
+def status_shared4(g=A, d=100, M=2, ldg=128, scales=S4, K=4, w=A, idx=A, ws=A, ws_bytes=1 << 20):
+    hs = uq._HostScales(scales)
+    return L.uq_shared_scale_idx4(g, d, M, ldg, hs.ptr, K, w, idx, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    # one scale has no index to hold
+    (dict(K=1, scales=S127), "inval"), (dict(K=1, scales=None, idx=None), "inval"),
+    # then the checks of uq_shared_scale
+    (dict(g=None), "inval"), (dict(M=0), "inval"), (dict(ldg=130), "align"), (dict(w=None), "inval"),
+    (dict(ws=None), "inval"), (dict(ws_bytes=8), "ws"), (dict(idx=None), "inval"), (dict(idx=A + 1), "align"),
+    (dict(K=17, scales=[float(i + 1) for i in range(17)]), "range"), (dict(K=2, scales=[3.0, 2.5]), "range"),
+])
+def test_shared_scale_idx4_rejects(kw, want):
+    assert status_shared4(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
 def status_noalloc(g=A, d=100, M=2, ldg=128, scales=S127, K=1, w=A, idx=A):
     hs = uq._HostScales(scales)
     return L.uq_shared_scale_noalloc(g, d, M, ldg, hs.ptr, K, w, idx, None)
@@ -254,6 +272,28 @@ def status_qsum(g=A, d=100, rows=2, ldg=128, worker0=0, w=A, scales=S4, K=4, idx
 def test_quantize_sum_rejects(kw, want):
     assert status_qsum(**kw) == E[want]
     assert uq.uq_last_error() != ""
+
+
+def status_qsum4(g=A, d=100, rows=2, ldg=128, worker0=0, w=A, scales=S4, K=4, idx=A, seed=1, acc=0, sum_=A,
+                 M=2, out=A):
+    hs = uq._HostScales(scales)
+    return L.uq_quantize_sum_idx4(g, d, rows, ldg, worker0, w, hs.ptr, K, idx, seed, acc, sum_, M, out, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(K=1, scales=S127), "inval"),
+    (dict(g=None), "inval"), (dict(rows=0), "inval"), (dict(ldg=102), "align"), (dict(worker0=-1), "range"),
+    (dict(idx=None), "inval"), (dict(idx=A + 4), "align"), (dict(scales=[127.0, 100.0, 200.0, 300.0]), "range"),
+    (dict(sum_=None), "inval"), (dict(acc=2), "inval"), (dict(M=0), "inval"), (dict(out=A + 4), "align"),
+])
+def test_quantize_sum_idx4_rejects(kw, want):
+    assert status_qsum4(**kw) == E[want]
+    assert uq.uq_last_error() != ""
+
+
+def test_quantize_sum_idx4_accepts_a_valid_no_op():
+    """d = 0 with several scales passes every check and launches nothing."""
+    assert status_qsum4(d=0, out=None) == uq.UQ_OK
 
 
 def test_quantize_sum_reconstruction_checks_only_with_out():

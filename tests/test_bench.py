@@ -83,6 +83,20 @@ def test_streamed_bytes():
     assert per_coord(1, K, True, quant_sum=True) == per_coord(1, K, False, quant_sum=True)
 
 
+def test_four_bit_index_bytes():
+    """The index as 4-bit fields: the index pass writes (d + 1) / 2 bytes and
+    every quantise-and-sum call reads as many."""
+    d, M, K = 1 << 20, 16, 8
+    assert bench.index_bytes(1001, 4) == 501 and bench.index_bytes(1001, 8) == 1001
+    f = bench.algorithmic_bytes(d, M, K, True, quant_sum=True, index_bits=4)
+    assert f["shared_scale"] == (4 * M + 2 + 2) * d + d // 2
+    assert f["quant_sum_first"] == 8 * d + d // 2 and f["quant_sum"] == (M - 2) * (12 * d + d // 2)
+    assert f["quant_sum_last"] == 16 * d + d // 2
+    assert 2 * f["total"] == (2 * (17 * M + 5) - (M + 1)) * d
+    # the composed path reads the byte index whatever is asked
+    assert bench.algorithmic_bytes(d, M, K, True, index_bits=4) == bench.algorithmic_bytes(d, M, K, True)
+
+
 def test_packed_bytes():
     assert bench.code_bytes(1001, 4) == 501 and bench.code_bytes(1001, 2) == 251
     assert bench.quantize_bytes_per_launch(1000, 3, 1, 4) == 3 * (4000 + 500)
@@ -154,11 +168,21 @@ def test_cpu_baseline_on_a_small_sample():
 class FakeStep:
     """The buffers bench.py reads back from a step, as host tensors."""
 
-    def __init__(self, torch, ref, M, d, bits, streamed=False):
+    def __init__(self, torch, ref, M, d, bits, streamed=False, index_bits=8):
         from oracle import oracle
 
+        self.d, self.index_bits = d, index_bits
         self.w = torch.tensor([float(ref["W"])], dtype=torch.float32)
-        self.idx = None if ref["idx"] is None else torch.from_numpy(ref["idx"].copy())
+        if ref["idx"] is None:
+            self.idx = None
+        elif index_bits == 8:
+            self.idx = torch.from_numpy(ref["idx"].copy())
+        else:
+            # 4-bit fields, the low nibble first (written out here by hand)
+            nib = np.zeros((d + 1) // 2 + 7, dtype=np.uint8)
+            for i, v in enumerate(ref["idx"]):
+                nib[i // 2] |= np.uint8(int(v) << (4 * (i % 2)))
+            self.idx = torch.from_numpy(nib)
         self.sum = torch.from_numpy(ref["sum"].copy())
         self.out = torch.from_numpy(ref["out"].copy())
         self.streamed = streamed
@@ -173,6 +197,11 @@ class FakeStep:
                 p = oracle.pack_codes(ref["codes"][m], bits)
                 packed[m, :p.size] = p
             self.codes = torch.from_numpy(packed)
+
+    def index_host(self, i0=0, i1=None):
+        from paper_2109_12497_amd.step import Step
+
+        return Step.index_host(self, i0, i1)
 
 
 @pytest.mark.parametrize("bits,scales", [(8, [127.0]), (8, [127.0, 2032.0]), (4, [7.0]), (4, [7.0, 112.0]),
@@ -189,6 +218,13 @@ def test_parity_on_sample_reads_every_code_width(bits, scales, streamed):
     ref = oracle.pipeline(g, scales, 9, d=d)
     st = FakeStep(torch, ref, M, d, bits, streamed)
     assert bench.parity_on_sample(st, ref, d, d, bits) == "bit-exact"
+    if len(scales) > 1:
+        # the index held as 4-bit fields reads out the same; a changed field
+        # is caught
+        st = FakeStep(torch, ref, M, d, bits, streamed, index_bits=4)
+        assert ref["idx"].any() and bench.parity_on_sample(st, ref, d, d, bits) == "bit-exact"
+        st.idx[250] ^= 0x10
+        assert bench.parity_on_sample(st, ref, d, d, bits) == "MISMATCH"
     st.sum[5] += 1
     assert bench.parity_on_sample(st, ref, d, d, bits) == "MISMATCH"
     st = FakeStep(torch, ref, M, d, bits, streamed)

@@ -69,13 +69,16 @@ def check_roofline(j, share_lo=0.4, share_hi=1.3):
 
 def test_default_bench_line():
     """`python bench.py` with no workload: 2^30 coordinates, 16 workers
-    streamed through the fused quantise-and-sum, eight scales."""
+    streamed through the fused quantise-and-sum, eight scales, the shared
+    index as 4-bit fields."""
     j = run_bench(workload=None, steps=3, warmup=1)
     cfg = j["config"]
     assert (cfg["workload"], cfg["d"], cfg["M"], len(cfg["scales"]), cfg["streamed"]) == \
         ("student-t", 1 << 30, 16, 8, True)
-    assert cfg["path"] == "quantise-and-sum fused"
-    assert j["step_bytes"] == (17 * 16 + 5) * (1 << 30)
+    assert cfg["path"] == "quantise-and-sum fused" and cfg["index_bits"] == 4
+    # 17 M + 5 bytes per coordinate with a byte index; its 4-bit fields save
+    # half a byte in the index pass and in each of the M workers' calls
+    assert j["step_bytes"] == (2 * (17 * 16 + 5) - 17) * (1 << 29)
     check_roofline(j, 0.85, 1.15)
     assert j["roofline"]["stage"] == "quant_sum" and j["roofline"]["launches_per_step"] == 14
     assert j["cpu_baseline"]["one_core"]["value"] > 0

@@ -58,7 +58,7 @@ def compare_in_chunks(step, g, d, scales, seed, with_codes):
         host = g[:, c0:c1].cpu().numpy()
         ref = O.window(host, W, scales, seed, i0=c0, threads=threads)
         if ref["idx"] is not None:
-            got = step.idx[c0:c1].cpu().numpy()
+            got = step.index_host(c0, c1)
             bad = np.flatnonzero(got != ref["idx"])
             assert bad.size == 0, f"scale index differs at {(c0 + bad[:5]).tolist()}"
         if with_codes:
@@ -122,15 +122,25 @@ def test_vgg16_4bit_every_coordinate_equals_int8(name):
 
 def test_student_t_every_coordinate():
     """2^30 coordinates, 16 workers streamed through the fused
-    quantise-and-sum (no code rows), eight scales: the index, the sums and
-    the reconstruction at every coordinate."""
+    quantise-and-sum (no code rows), eight scales, the shared index held as
+    4-bit fields (the benchmark's form): the index, the sums and the
+    reconstruction at every coordinate; then the same step with the index as
+    bytes, equal at every coordinate."""
     g, cfg = synth.make_gradients("student-t", device=DEV)
     d, M, scales, seed = cfg["d"], cfg["M"], cfg["scales"], cfg["seed"]
-    step = Step(d, M, scales, device=DEV, streamed=True)
+    step = Step(d, M, scales, device=DEV, streamed=True, index_bits=4)
     assert step.quant_sum
     step.run(g, seed)
     torch.cuda.synchronize()
     check_norm(g, d, np.float32(step.w[0].item()))
     compare_in_chunks(step, g, d, scales, seed, with_codes=False)
-    del g, step
+    byte = Step(d, M, scales, device=DEV, streamed=True, index_bits=8)
+    byte.run(g, seed)
+    torch.cuda.synchronize()
+    assert torch.equal(byte.w[:1], step.w[:1])
+    nib = step.idx[:(d + 1) // 2]
+    assert torch.equal(torch.stack([nib & 0xF, nib >> 4], dim=1).reshape(-1)[:d], byte.idx[:d])
+    assert torch.equal(byte.sum[:d], step.sum[:d])
+    assert torch.equal(byte.out[:d].view(torch.int32), step.out[:d].view(torch.int32))
+    del g, step, byte
     torch.cuda.empty_cache()
